@@ -1,0 +1,232 @@
+/*
+ * Reference oracle for batched paged decode attention and the KV append.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, obviously correct
+ * CPU definition that the GPU library is checked against.  Only the test
+ * suite, the smoke check and the benchmark's CPU-baseline leg may load it.
+ * It shares no code, header, table or helper with the GPU library and is
+ * compiled by gcc, never by hipcc.
+ *
+ * What is computed.  The paper (beLLMan, Sec. 3, "Our key proposal" and
+ * "Setup and trace") serves an LLM through vLLM and watches the
+ * time-between-tokens of the decode loop; the cost of each decode step is
+ * attention of one new query token per request over that request's KV cache,
+ * whose length is the prompt plus the tokens generated so far.  The paper
+ * itself prints no attention formula; the definition below is textbook
+ * scaled dot-product attention with grouped-query heads:
+ *
+ *   for request b and query head h (kv head g = h / G, G = H_q / H_kv):
+ *     s_t   = scale * sum_d q[b,h,d] * k_t[d]          for t < L_b
+ *     w_t   = exp(s_t - max_u s_u),   Z = sum_t w_t
+ *     out   = sum_t (w_t / Z) * v_t
+ *
+ * everything in IEEE binary64, with no reordering, blocking or splitting.
+ *
+ * Paged layout read here (the library's contract, restated independently):
+ *   K pool  [NP, H_kv, D/x, 16, x]   x = 16 bytes / element size
+ *   V pool  [NP, H_kv, D, 16]
+ *   token t of request b lives in page block_table[b][t/16], slot t%16.
+ * Element codes: bf16 (the upper half of an IEEE binary32) or OCP fp8
+ * e4m3fn (1 sign, 4 exponent bits with bias 7, 3 mantissa bits, subnormals at
+ * exponent 0, S.1111.111 is NaN, no infinities).  For fp8 pools each
+ * (request, kv head) carries one fp32 scale for K and one for V; the real value
+ * of a code is decode(code) * scale, formed exactly in binary64.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_PAGE 16
+
+enum { ORACLE_BF16 = 1, ORACLE_FP8_E4M3FN = 2 };
+
+/* bf16 bit pattern -> binary64.  A bf16 value is exactly the binary32 whose
+ * upper 16 bits are the pattern and whose lower 16 bits are zero. */
+double oracle_bf16_to_f64(uint16_t bits)
+{
+    uint32_t w = (uint32_t)bits << 16;
+    float f;
+    memcpy(&f, &w, sizeof f);
+    return (double)f;
+}
+
+/* OCP e4m3fn code -> binary64, from the format definition. */
+double oracle_e4m3fn_to_f64(uint8_t code)
+{
+    int sign = (code >> 7) & 1;
+    int e = (code >> 3) & 0xF;
+    int m = code & 0x7;
+    double mag;
+    if (e == 0xF && m == 0x7)
+        return NAN;
+    if (e == 0)
+        mag = ldexp((double)m / 8.0, 1 - 7);          /* subnormal */
+    else
+        mag = ldexp(1.0 + (double)m / 8.0, e - 7);    /* normal */
+    return sign ? -mag : mag;
+}
+
+static double load_code(const void *base, int64_t idx, int dtype)
+{
+    if (dtype == ORACLE_BF16)
+        return oracle_bf16_to_f64(((const uint16_t *)base)[idx]);
+    return oracle_e4m3fn_to_f64(((const uint8_t *)base)[idx]);
+}
+
+static int elem_bytes(int dtype) { return dtype == ORACLE_BF16 ? 2 : 1; }
+
+/* Offset (in elements) of K element (page, kv head g, slot, dim d). */
+static int64_t k_offset(int64_t page, int g, int slot, int d, int H_kv, int D, int x)
+{
+    int64_t tile = page * H_kv + g;                 /* one (page, head) tile */
+    int64_t chunk = tile * (D / x) + d / x;         /* x-element chunk of dims */
+    return (chunk * ORACLE_PAGE + slot) * x + d % x;
+}
+
+/* Offset (in elements) of V element (page, kv head g, dim d, slot). */
+static int64_t v_offset(int64_t page, int g, int slot, int d, int H_kv, int D)
+{
+    int64_t tile = page * H_kv + g;
+    return (tile * D + d) * ORACLE_PAGE + slot;
+}
+
+/*
+ * Decode attention, one full forward step, in binary64.
+ *   q        [B, H_q, D] bf16 bit patterns
+ *   k_scale, v_scale  [B, H_kv] fp32, used only for fp8 pools (may be NULL
+ *            for bf16)
+ *   seq_lens [B] attention lengths (the length after this step's append)
+ *   out      [B, H_q, D] binary64
+ * A request with length 0 gets an all-zero output row.
+ * Returns 0, or -1 when a used block-table entry or a length is out of range.
+ */
+int oracle_decode_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
+                            const uint16_t *q,
+                            const void *k_pages, const void *v_pages, int64_t num_pages,
+                            const float *k_scale, const float *v_scale,
+                            const int32_t *block_table, int max_pages,
+                            const int32_t *seq_lens, float scale, double *out)
+{
+    const int G = H_q / H_kv;
+    const int x = 16 / elem_bytes(kv_dtype);
+    int bad = 0;
+
+    for (int b = 0; b < B; ++b) {
+        int L = seq_lens[b];
+        if (L < 0 || L > max_pages * ORACLE_PAGE)
+            return -1;
+        for (int p = 0; p < (L + ORACLE_PAGE - 1) / ORACLE_PAGE; ++p) {
+            int32_t pg = block_table[(int64_t)b * max_pages + p];
+            if (pg < 0 || pg >= num_pages)
+                return -1;
+        }
+    }
+
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < H_q; ++h) {
+            const int g = h / G;
+            const int L = seq_lens[b];
+            double *o = out + ((int64_t)b * H_q + h) * D;
+            const uint16_t *qrow = q + ((int64_t)b * H_q + h) * D;
+            double ks = 1.0, vs = 1.0;
+            double *s;
+            double m, Z;
+
+            for (int d = 0; d < D; ++d)
+                o[d] = 0.0;
+            if (L == 0)
+                continue;
+            if (kv_dtype == ORACLE_FP8_E4M3FN) {
+                ks = (double)k_scale[(int64_t)b * H_kv + g];
+                vs = (double)v_scale[(int64_t)b * H_kv + g];
+            }
+            s = (double *)malloc(sizeof(double) * (size_t)L);
+            if (!s) {
+                bad = 1;
+                continue;
+            }
+
+            /* scores */
+            for (int t = 0; t < L; ++t) {
+                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
+                int slot = t % ORACLE_PAGE;
+                double dot = 0.0;
+                for (int d = 0; d < D; ++d) {
+                    double kv = load_code(k_pages, k_offset(pg, g, slot, d, H_kv, D, x), kv_dtype) * ks;
+                    dot += oracle_bf16_to_f64(qrow[d]) * kv;
+                }
+                s[t] = (double)scale * dot;
+            }
+
+            /* softmax weights */
+            m = s[0];
+            for (int t = 1; t < L; ++t)
+                if (s[t] > m)
+                    m = s[t];
+            Z = 0.0;
+            for (int t = 0; t < L; ++t) {
+                s[t] = exp(s[t] - m);
+                Z += s[t];
+            }
+
+            /* weighted sum of values */
+            for (int t = 0; t < L; ++t) {
+                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
+                int slot = t % ORACLE_PAGE;
+                double w = s[t] / Z;
+                for (int d = 0; d < D; ++d) {
+                    double vv = load_code(v_pages, v_offset(pg, g, slot, d, H_kv, D), kv_dtype) * vs;
+                    o[d] += w * vv;
+                }
+            }
+            free(s);
+        }
+    }
+    return bad ? -2 : 0;
+}
+
+/*
+ * KV append, on host copies of the pools: for each request b the new token's
+ * K and V rows ([B, H_kv, D] codes of the pool's element type) are copied
+ * byte for byte into page block_table[b][L/16], slot L%16, with L =
+ * seq_lens[b]; then seq_lens[b] becomes L + 1.  Nothing else is written.
+ * Returns 0, or -1 (and writes nothing) when a slot falls outside the block
+ * table or the page pool.
+ */
+int oracle_kv_append(int B, int H_kv, int D, int kv_dtype,
+                     const void *k_new, const void *v_new,
+                     void *k_pages, void *v_pages, int64_t num_pages,
+                     const int32_t *block_table, int max_pages, int32_t *seq_lens)
+{
+    const int eb = elem_bytes(kv_dtype);
+    const int x = 16 / eb;
+
+    for (int b = 0; b < B; ++b) {
+        int L = seq_lens[b];
+        int32_t pg;
+        if (L < 0 || L / ORACLE_PAGE >= max_pages)
+            return -1;
+        pg = block_table[(int64_t)b * max_pages + L / ORACLE_PAGE];
+        if (pg < 0 || pg >= num_pages)
+            return -1;
+    }
+
+    for (int b = 0; b < B; ++b) {
+        int L = seq_lens[b];
+        int64_t pg = block_table[(int64_t)b * max_pages + L / ORACLE_PAGE];
+        int slot = L % ORACLE_PAGE;
+        for (int g = 0; g < H_kv; ++g) {
+            for (int d = 0; d < D; ++d) {
+                int64_t src = ((int64_t)b * H_kv + g) * D + d;
+                memcpy((char *)k_pages + k_offset(pg, g, slot, d, H_kv, D, x) * eb,
+                       (const char *)k_new + src * eb, (size_t)eb);
+                memcpy((char *)v_pages + v_offset(pg, g, slot, d, H_kv, D) * eb,
+                       (const char *)v_new + src * eb, (size_t)eb);
+            }
+        }
+        seq_lens[b] = L + 1;
+    }
+    return 0;
+}
