@@ -1,0 +1,288 @@
+"""Decode-step benchmark on one MI355X.
+
+A step is one decode step of the batch: bellman_kv_append (one token per
+request) followed by bellman_decode_attention over the paged cache, for one
+layer.  The default workload is the 256-request summarization batch under
+load (32 query / 8 KV heads, head_dim 128, bf16, KV length = prompt
+U{6000..12000} + generated lognormal(median 500, sigma 0.5) clipped to 1500,
+50 steps); the same batch with beLLMan's per-request caps {100, 200, 400} is
+measured beside it.  Inputs are synthetic and resident in HBM before timing.
+
+Prints one JSON line.  ``value`` is the algorithmic HBM traffic of the timed
+steps divided by their wall time (GB/s); ``roofline`` prices the attention
+kernel alone, timed with HIP events the library records around it;
+``cpu_baseline`` is the binary64 oracle on a bounded sample of the same step.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "decode-attention HBM GB/s (% of MI355X peak) + decode steps/sec at batch 256"
+KERNEL_SRC = os.path.join(ROOT, "paper_2510_15330_amd", "csrc", "kernels.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_sha():
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measure(name, steps, warmup, impl, split_pages, seed=0):
+    import torch
+
+    import paper_2510_15330_amd as bl
+    from paper_2510_15330_amd import workloads as wl
+
+    w = wl.build(name, seed=seed, device="cuda", steps=max(steps, warmup, 1))
+    out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    lens0 = w.seq_lens.clone()
+    stream = torch.cuda.current_stream()
+
+    def step(i, events=None):
+        bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
+        bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
+                            stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, impl=impl,
+                            split_pages=split_pages, events=events)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    if bl.device_errors() != 0:
+        raise RuntimeError("device error flags set during warmup")
+    w.seq_lens.copy_(lens0)                       # timed steps start from the initial state
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+
+    if torch.distributed.is_available() and torch.distributed.is_initialized():
+        torch.distributed.barrier()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if torch.distributed.is_available() and torch.distributed.is_initialized():
+        torch.distributed.barrier()
+
+    if bl.device_errors() != 0:
+        raise RuntimeError("device error flags set during the timed steps")
+    if not torch.isfinite(out.float()).all():
+        raise RuntimeError("non-finite attention output")
+    kt = np.array([a.elapsed_time(b) for a, b in evs]) * 1e-3          # seconds per attention kernel
+    wall = t1 - t0
+    attn_bytes = np.array([w.algorithmic_bytes(i) for i in range(steps)], dtype=np.float64)
+    step_bytes = attn_bytes + w.append_bytes()
+    return dict(w=w, wall=wall, kt=kt, attn_bytes=attn_bytes, step_bytes=step_bytes,
+                steps_per_s=steps / wall, gbs=step_bytes.sum() / wall / 1e9,
+                kernel_gbs=attn_bytes.mean() / kt.mean() / 1e9)
+
+
+def cpu_baseline(w, target_s=12.0):
+    """The binary64 oracle on the first requests of the workload's first step,
+    timed on this host; pages of the sampled requests are gathered on the
+    device and copied to host memory first (not timed)."""
+    import torch
+
+    import oracle
+
+    lib = oracle.load()
+    L = w.seq_lens.cpu().numpy().astype(np.int64)          # state after the timed steps
+    q = w.q[0]
+
+    def sample(n):
+        reqs = list(range(n))
+        sl = L[reqs].astype(np.int32)
+        bt = w.block_table[reqs].cpu().numpy()
+        need = (sl + 15) // 16
+        used = [bt[i, :need[i]] for i in range(n)]
+        pages = np.unique(np.concatenate(used))
+        remap = np.full(w.num_pages, -1, dtype=np.int64)
+        remap[pages] = np.arange(len(pages))
+        bt2 = np.full((n, int(need.max())), -1, dtype=np.int32)
+        for i, u in enumerate(used):
+            bt2[i, :len(u)] = remap[u]
+        idx = torch.from_numpy(pages.astype(np.int64)).cuda()
+        kp = w.k_pages.index_select(0, idx).cpu()
+        vp = w.v_pages.index_select(0, idx).cpu()
+        if w.kv == "bf16":
+            kp = kp.view(torch.int16).numpy().view(np.uint16)
+            vp = vp.view(torch.int16).numpy().view(np.uint16)
+            kvd, ks, vs = oracle.BF16, None, None
+        else:
+            kp, vp = kp.numpy(), vp.numpy()
+            kvd = oracle.FP8_E4M3FN
+            ks, vs = w.k_scale[reqs].cpu().numpy(), w.v_scale[reqs].cpu().numpy()
+        qb = q[reqs].cpu().view(torch.int16).numpy().view(np.uint16)
+        return reqs, (qb, kp, vp, bt2, sl, w.scale, kvd, ks, vs)
+
+    # size the sample from a one-request probe
+    reqs, args = sample(1)
+    t = time.perf_counter()
+    oracle.decode_attention(*args, lib=lib)
+    t_one = max(time.perf_counter() - t, 1e-4)
+    n = int(min(w.B, max(1, target_s / t_one)))
+    reqs, args = sample(n)
+    t = time.perf_counter()
+    oracle.decode_attention(*args, lib=lib)
+    dt = time.perf_counter() - t
+    tokens = float(L[reqs].sum())
+    nbytes = tokens * w.H_kv * w.D * 2 * w.elem_bytes() + 2 * n * w.H_q * w.D * 2
+    frac = tokens / float(L.sum())
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "steps_per_s": round(frac / dt, 5),
+        "cores": int(oracle.num_threads(lib)),
+        "kind": "oracle",
+        "sample": f"binary64 oracle on requests 0..{n - 1} of {w.B} (all {w.H_q} query heads, "
+                  f"{int(tokens)} KV tokens, {frac:.3f} of one step's tokens) in {dt:.1f} s; "
+                  f"steps_per_s extrapolates to the whole batch",
+        "host_cpu": _cpu_model(),
+    }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def traffic_for(name, impl):
+    """Counter-derived HBM bytes per attention launch, if they were taken on
+    the current kernel source (profiles/traffic.json)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(name)
+    if not ent or ent.get("kernel_sha") != kernel_sha():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="summarization",
+                    choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8"])
+    ap.add_argument("--impl", default="auto", choices=["auto", "mfma", "valu"])
+    ap.add_argument("--split-pages", type=int, default=0)
+    ap.add_argument("--no-capped", action="store_true", help="skip the capped companion run")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this build has no multi-GPU path. "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2510_15330_amd as bl
+    from paper_2510_15330_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    bl.library()
+    impl = {"auto": bl.IMPL_AUTO, "mfma": bl.IMPL_MFMA, "valu": bl.IMPL_VALU}[args.impl]
+    steps = args.steps if args.steps is not None else wl.CONFIGS[args.workload]["steps"]
+
+    log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
+    r = measure(args.workload, steps, args.warmup, impl, args.split_pages)
+    w = r["w"]
+    log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['steps_per_s']:.1f} steps/s, step traffic {r['gbs']:.1f} GB/s, "
+        f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_gbs']:.1f} GB/s")
+
+    result = {
+        "metric": METRIC,
+        "value": round(r["gbs"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["wall"] / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.kv,
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "batch": w.B, "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
+            "kv_dtype": w.kv, "mean_kv_len": round(float(w.lens_at(0).mean()), 1),
+            "impl": args.impl, "split_pages": args.split_pages or "auto", "seed": 0,
+        },
+        "steps_per_s": round(r["steps_per_s"], 2),
+        "pct_of_peak": round(100.0 * r["gbs"] / PEAK_HBM_GBS, 2),
+        "attention_kernel_us": {
+            "mean": round(r["kt"].mean() * 1e6, 2),
+            "p10": round(float(np.percentile(r["kt"], 10)) * 1e6, 2),
+            "p50": round(float(np.percentile(r["kt"], 50)) * 1e6, 2),
+            "p90": round(float(np.percentile(r["kt"], 90)) * 1e6, 2),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(r["kernel_gbs"], 2),
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": round(r["kernel_gbs"] / PEAK_HBM_GBS, 4),
+            "traffic": traffic_for(args.workload, args.impl),
+            "kernel": "attn_mfma_kernel (split-K partial attention)",
+            "bytes_per_launch": int(r["attn_bytes"].mean()),
+        },
+    }
+
+    if args.workload == "summarization" and not args.no_capped:
+        c = measure("summarization_capped", steps, args.warmup, impl, args.split_pages)
+        lens_u, info_u = wl.sample_lengths("summarization", 0)
+        lens_c, info_c = wl.sample_lengths("summarization_capped", 0)
+        p, gu, gc = info_u["prompt"], info_u["generated"], info_c["generated_capped"]
+        # decode-attention tokens over each request's whole generation: sum_{t<=g} (prompt + t)
+        req_u = float((gu * p + gu * (gu + 1) / 2).sum())
+        req_c = float((gc * p + gc * (gc + 1) / 2).sum())
+        result["capped"] = {
+            "workload": "summarization_capped",
+            "steps_per_s": round(c["steps_per_s"], 2),
+            "value_gbs": round(c["gbs"], 2),
+            "ms_per_step": round(c["wall"] / steps * 1e3, 4),
+            "attention_kernel_us_mean": round(c["kt"].mean() * 1e6, 2),
+            "step_time_vs_uncapped": round((c["wall"] / steps) / (result["ms_per_step"] / 1e3), 4),
+            "bytes_per_step_vs_uncapped": round(float(c["attn_bytes"].mean() / result["roofline"]["bytes_per_launch"]), 4),
+            "decode_steps_per_request_vs_uncapped": round(float(gc.mean() / gu.mean()), 4),
+            "request_attention_bytes_vs_uncapped": round(req_c / req_u, 4),
+        }
+        log(f"[bench] capped: {c['steps_per_s']:.1f} steps/s, {c['gbs']:.1f} GB/s")
+        del c
+
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

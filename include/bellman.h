@@ -1,0 +1,224 @@
+/*
+ * libbellman — batched paged decode attention for MI355X (gfx950), with the
+ * KV append that feeds it and the host-side output-length controller of
+ * beLLMan ("beLLMan: Controlling LLM Congestion", arXiv 2510.15330).
+ *
+ * The paper (Sec. 3) serves requests through a batching scheduler whose
+ * per-token decode latency (TBT) it watches; each decode step attends one new
+ * query token per request over that request's KV cache, whose length is the
+ * prompt plus the tokens generated so far, and the controller caps each
+ * request's output length under load.  This library provides that decode
+ * step and the controller.
+ *
+ * Conventions for every call below
+ *  - Tensors are described by bellman_tensor_t: a data pointer, an element
+ *    type, a shape and strides in elements.  Device tensors are memory the
+ *    caller allocated on the current HIP device; the library never frees,
+ *    reallocates or retains them after the call returns.
+ *  - stream is a hipStream_t (NULL = the device's null stream).  Every
+ *    device call only enqueues work on it and returns without synchronising.
+ *  - Return value: 0 on success, otherwise a negative bellman_status_t; the
+ *    reason is in bellman_last_error() (per thread).  Arguments are checked
+ *    on the host from the descriptors alone, before any HIP call; the call
+ *    then enqueues nothing.  Device contents (lengths, block-table entries)
+ *    cannot be checked on the host without a sync; the kernels bound-check
+ *    them, skip any slot or page outside the pool, and record the violation
+ *    in a per-device error word read by bellman_device_errors().  Faults of
+ *    the GPU surface at the caller's next synchronisation.
+ *  - No C++ exception crosses this interface.
+ *
+ * Paged KV layout (both pools hold whole 16-token pages; page p of head g is
+ * one contiguous tile):
+ *    K pool  [NP, H_kv, D/x, 16, x]   x = 16 bytes / element size
+ *            (8 for bf16, 16 for fp8): for each page and head, the keys are
+ *            stored as D/x chunks of x consecutive dims, each chunk holding
+ *            all 16 slots.
+ *    V pool  [NP, H_kv, D, 16]        values stored dim-major: for each
+ *            page, head and dim, the 16 slots are consecutive.
+ *  Token t of request b lives in page block_table[b][t / 16], slot t % 16.
+ *  Element types: bf16, or OCP fp8 e4m3fn with one fp32 dequantisation
+ *  scale per (request, KV head) for K and one for V (real value =
+ *  e4m3fn(code) * scale).  Supported: head_dim D in {64, 128}; H_q a
+ *  multiple of H_kv with G = H_q / H_kv <= 16; query head h reads KV head
+ *  h / G.
+ */
+#ifndef BELLMAN_H
+#define BELLMAN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum bellman_status {
+    BELLMAN_OK = 0,
+    BELLMAN_ERR_INVALID_ARG = -1,  /* null pointer, bad shape/stride/dtype, non-finite scale */
+    BELLMAN_ERR_UNSUPPORTED = -2,  /* well-formed but outside what the kernels implement */
+    BELLMAN_ERR_HIP = -3,          /* a HIP runtime call or kernel launch failed */
+    BELLMAN_ERR_OOM = -4           /* workspace allocation failed */
+} bellman_status_t;
+
+typedef enum bellman_dtype {
+    BELLMAN_BF16 = 1,
+    BELLMAN_FP8_E4M3FN = 2,
+    BELLMAN_INT32 = 3,
+    BELLMAN_FP32 = 4
+} bellman_dtype_t;
+
+#define BELLMAN_MAX_DIMS 5
+#define BELLMAN_PAGE_TOKENS 16
+
+typedef struct bellman_tensor {
+    void *data;                       /* device pointer */
+    int32_t dtype;                    /* bellman_dtype_t */
+    int32_t ndim;                     /* used entries of shape/stride */
+    int64_t shape[BELLMAN_MAX_DIMS];
+    int64_t stride[BELLMAN_MAX_DIMS]; /* in elements */
+    const float *dequant_scale;       /* fp8 K/V pools only: device fp32 [B, H_kv],
+                                         contiguous; NULL otherwise */
+} bellman_tensor_t;
+
+/*
+ * Append one token per request to the paged KV cache (the step that grows
+ * each request's KV length by one token per decode step, Sec. 3).
+ *   k_new, v_new  [B, H_kv, D], same element type as the pools (fp8 codes
+ *                 are copied as they are, already quantised with the
+ *                 request's scale); innermost dim contiguous.
+ *   k_pages       [NP, H_kv, D/x, 16, x] contiguous (written).
+ *   v_pages       [NP, H_kv, D, 16] contiguous (written).
+ *   block_table   int32 [B, maxP], innermost contiguous; the page that will
+ *                 receive the token must already be assigned.
+ *   seq_lens      int32 [B] contiguous, read and written: the token of
+ *                 request b goes to position L = seq_lens[b]
+ *                 (page block_table[b][L/16], slot L%16), then seq_lens[b]
+ *                 becomes L + 1.
+ * The copy is bit-exact and writes nothing else.  A request whose slot lies
+ * outside the block table or the pool is skipped (no byte written, length
+ * unchanged) and flagged in the device error word.
+ */
+int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_new,
+                      bellman_tensor_t *k_pages, bellman_tensor_t *v_pages,
+                      const bellman_tensor_t *block_table, bellman_tensor_t *seq_lens,
+                      void *stream);
+
+/*
+ * Decode attention for one step: for request b and query head h,
+ *   out[b,h,:] = sum_t softmax_t(scale * <q[b,h,:], k_t>) * v_t,  t < seq_lens[b]
+ * over the request's KV pages (query head h uses KV head h / G).
+ *   q            bf16 [B, H_q, D], innermost contiguous.
+ *   k_pages      [NP, H_kv, D/x, 16, x] contiguous, bf16 or fp8 (with
+ *                dequant_scale set).
+ *   v_pages      [NP, H_kv, D, 16] contiguous, same element type.
+ *   block_table  int32 [B, maxP], innermost contiguous.
+ *   seq_lens     int32 [B]: attention lengths (after this step's append).
+ *   scale        finite fp32 softmax scale (usually 1/sqrt(D)).
+ *   out          bf16 [B, H_q, D], innermost contiguous (written; rounded to
+ *                nearest even).  A request of length 0 gets zeros.
+ * Long requests are split into chunks of whole pages whose partial softmax
+ * statistics are merged in a second pass; the work list is built on the
+ * device, so the call never waits for the GPU.  Scratch memory is a
+ * per-device library workspace grown on demand (hipMalloc) and released by
+ * bellman_shutdown(); calls on different streams of one device must not
+ * overlap in time.
+ */
+int bellman_decode_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
+                             const bellman_tensor_t *v_pages,
+                             const bellman_tensor_t *block_table,
+                             const bellman_tensor_t *seq_lens, float scale,
+                             bellman_tensor_t *out, void *stream);
+
+/* Kernel choice for bellman_decode_attention_opts. */
+typedef enum bellman_attn_impl {
+    BELLMAN_IMPL_AUTO = 0,  /* the library's choice for the shape */
+    BELLMAN_IMPL_MFMA = 1,  /* QK^T and PV on the matrix cores */
+    BELLMAN_IMPL_VALU = 2   /* QK^T and PV on the vector ALUs */
+} bellman_attn_impl_t;
+
+typedef struct bellman_attn_opts {
+    int32_t split_pages;  /* pages per split-K chunk, 1..64; 0 = library default */
+    int32_t impl;         /* bellman_attn_impl_t */
+    void *event_begin;    /* optional hipEvent_t recorded on the stream right before
+                             the main attention kernel (profiling); NULL = none */
+    void *event_end;      /* optional hipEvent_t recorded right after it */
+} bellman_attn_opts_t;
+
+/* bellman_decode_attention with explicit tuning options (NULL = defaults).
+ * Results of different options agree within floating-point reordering. */
+int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
+                                  const bellman_tensor_t *v_pages,
+                                  const bellman_tensor_t *block_table,
+                                  const bellman_tensor_t *seq_lens, float scale,
+                                  bellman_tensor_t *out, const bellman_attn_opts_t *opts,
+                                  void *stream);
+
+/* ------------------------------------------------ output-length control --
+ * The paper's linear congestion controller (Sec. 3: "Our key proposal",
+ * "Placeholder for congestion control", "Default unbounded run", "beLLMan in
+ * action").  Host only; no HIP call.  Each second the scheduler's average TBT
+ * is pushed; the controller keeps the moving average MA of the last `window`
+ * samples and sets the reduction rate
+ *     r = 0                                        if MA <= t1
+ *     r = clamp(r_min + (r_max - r_min)(MA - t1)/(t2 - t1), r_min, r_max)
+ *                                                  if MA >  t1
+ * (r = r_max on trigger when t2 <= t1).  A queued request with predicted
+ * unbounded length L is asked for N = max(1, floor(L (1 - r) + 0.5)), and
+ * N = L when r = 0 or L = 0.  Arithmetic is binary64.  A controller object
+ * is not thread-safe.
+ */
+typedef struct bellman_controller bellman_controller_t;
+
+/* t1, t2: trigger and full-reduction thresholds (same unit as the TBT
+ * samples; the paper uses the median and 75th percentile of an unbounded
+ * run); window >= 1 samples (paper: 5 one-second samples); 0 <= r_min <=
+ * r_max < 1 (paper: 0.05 and 0.20).  Returns NULL on invalid arguments. */
+bellman_controller_t *bellman_controller_create(double t1, double t2, int32_t window,
+                                                double r_min, double r_max);
+void bellman_controller_destroy(bellman_controller_t *ctl);
+/* Current reduction rate r, or a negative status for a NULL controller. */
+double bellman_controller_rate(const bellman_controller_t *ctl);
+
+typedef struct bellman_load_signal {
+    bellman_controller_t *controller;  /* controller to read (and update) */
+    int32_t has_sample;                /* 1: push tbt_avg first (once per second) */
+    double tbt_avg;                    /* the last second's average TBT */
+    int32_t predicted_len;             /* predicted unbounded output length L >= 0 */
+} bellman_load_signal_t;
+
+/* Optionally push one TBT sample, then return the length cap N for a request
+ * whose predicted unbounded length is predicted_len (see above), or a
+ * negative status (NULL signal or controller, negative length, non-finite
+ * sample). */
+int32_t bellman_length_cap(const bellman_load_signal_t *load_signal);
+
+/* Thresholds from an unbounded run's per-second TBTs: *t1 = median, *t2 =
+ * 75th percentile, by linear interpolation between order statistics
+ * (fractional rank p/100 * (n - 1)).  Host arrays; n >= 1. */
+int bellman_calibrate_thresholds(const double *tbt, int64_t n, double *t1, double *t2);
+
+/* ----------------------------------------------------------------- misc -- */
+
+/* Text of the last error raised on the calling thread ("" if none). */
+const char *bellman_last_error(void);
+
+/* Make sure the current device's workspace holds at least `bytes`
+ * (hipMalloc outside any timed region). */
+int bellman_reserve_workspace(int64_t bytes);
+
+/* Synchronise `stream`, copy the current device's error word to *flags and
+ * clear it.  Bits: 1 = an append slot outside the block table or pool,
+ * 2 = an attention length above maxP*16 (clamped), 4 = a block-table entry
+ * outside the pool (page skipped). */
+int bellman_device_errors(void *stream, int32_t *flags);
+
+/* Free every device's workspace.  No call may be in flight. */
+void bellman_shutdown(void);
+
+/* Library version as "major.minor.patch". */
+const char *bellman_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BELLMAN_H */

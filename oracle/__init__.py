@@ -64,6 +64,8 @@ def _bind(lib):
     lib.oracle_decode_attention.restype = i32
     lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, P, P, P, P, i64, P, i32, P]
     lib.oracle_kv_append.restype = i32
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = i32
     return lib
 
 
@@ -75,6 +77,10 @@ def _c(a, dtype):
     a = np.ascontiguousarray(a)
     assert a.dtype == dtype, (a.dtype, dtype)
     return a
+
+
+def num_threads(lib=None) -> int:
+    return (lib or load()).oracle_num_threads()
 
 
 def bf16_to_f64(bits: int, lib=None) -> float:

@@ -33,6 +33,7 @@
  * of a code is decode(code) * scale, formed exactly in binary64.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -66,6 +67,9 @@ double oracle_e4m3fn_to_f64(uint8_t code)
         mag = ldexp(1.0 + (double)m / 8.0, e - 7);    /* normal */
     return sign ? -mag : mag;
 }
+
+/* Threads the parallel loops below will use (for reporting). */
+int oracle_num_threads(void) { return omp_get_max_threads(); }
 
 static double load_code(const void *base, int64_t idx, int dtype)
 {

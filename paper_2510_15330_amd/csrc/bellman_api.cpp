@@ -1,0 +1,460 @@
+// Host side of the C ABI: descriptor validation, the per-device workspace,
+// and the launch sequence of one decode-attention call.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "../../include/bellman.h"
+#include "internal.h"
+
+using namespace bellman;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+// ------------------------------------------------------------- workspace ---
+
+constexpr int kMaxDevices = 64;
+
+struct Workspace {
+    char* base = nullptr;
+    size_t cap = 0;
+};
+
+std::mutex g_ws_mutex;
+Workspace g_ws[kMaxDevices];
+int g_cu_count[kMaxDevices];
+int g_blocks_per_cu[kMaxDevices][2][2][3];  // [dev][fp8][D==128][impl], 0 = unknown
+
+int current_device(int* dev) {
+    hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (*dev < 0 || *dev >= kMaxDevices) return fail(BELLMAN_ERR_UNSUPPORTED, "device index %d", *dev);
+    return BELLMAN_OK;
+}
+
+// Grow the current device's workspace to at least `bytes`.  The header is
+// zeroed on (re)allocation.
+int ensure_workspace(int dev, size_t bytes, char** base) {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    Workspace& w = g_ws[dev];
+    if (bytes < sizeof(WorkspaceHeader)) bytes = sizeof(WorkspaceHeader);
+    if (w.cap < bytes) {
+        size_t want = bytes + bytes / 4;
+        want = (want + 0xFFFFF) & ~(size_t)0xFFFFF;
+        if (w.base) {
+            hipError_t e = hipDeviceSynchronize();
+            if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
+            (void)hipFree(w.base);
+            w.base = nullptr;
+            w.cap = 0;
+        }
+        void* p = nullptr;
+        hipError_t e = hipMalloc(&p, want);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(BELLMAN_ERR_OOM, "workspace hipMalloc(%zu): %s", want, hipGetErrorString(e));
+        }
+        e = hipMemset(p, 0, sizeof(WorkspaceHeader));
+        if (e != hipSuccess) {
+            (void)hipFree(p);
+            return fail(BELLMAN_ERR_HIP, "workspace hipMemset: %s", hipGetErrorString(e));
+        }
+        w.base = (char*)p;
+        w.cap = want;
+    }
+    *base = w.base;
+    return BELLMAN_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// --------------------------------------------------------- descriptors ----
+
+int elem_size(int32_t dt) {
+    switch (dt) {
+        case BELLMAN_BF16: return 2;
+        case BELLMAN_FP8_E4M3FN: return 1;
+        case BELLMAN_INT32: return 4;
+        case BELLMAN_FP32: return 4;
+        default: return 0;
+    }
+}
+
+const char* dtype_name(int32_t dt) {
+    switch (dt) {
+        case BELLMAN_BF16: return "bf16";
+        case BELLMAN_FP8_E4M3FN: return "fp8_e4m3fn";
+        case BELLMAN_INT32: return "int32";
+        case BELLMAN_FP32: return "fp32";
+        default: return "unknown";
+    }
+}
+
+int check_tensor(const bellman_tensor_t* t, const char* name, int ndim) {
+    if (!t) return fail(BELLMAN_ERR_INVALID_ARG, "%s: null descriptor", name);
+    if (t->ndim != ndim) return fail(BELLMAN_ERR_INVALID_ARG, "%s: expected %d dims, got %d", name, ndim, t->ndim);
+    if (elem_size(t->dtype) == 0) return fail(BELLMAN_ERR_INVALID_ARG, "%s: unknown dtype %d", name, t->dtype);
+    int64_t numel = 1;
+    for (int i = 0; i < ndim; ++i) {
+        if (t->shape[i] < 0) return fail(BELLMAN_ERR_INVALID_ARG, "%s: negative size in dim %d", name, i);
+        numel *= t->shape[i];
+    }
+    if (numel > 0 && !t->data) return fail(BELLMAN_ERR_INVALID_ARG, "%s: null data pointer", name);
+    return BELLMAN_OK;
+}
+
+int check_dtype(const bellman_tensor_t* t, const char* name, int32_t want) {
+    if (t->dtype != want)
+        return fail(BELLMAN_ERR_INVALID_ARG, "%s: dtype %s, expected %s", name, dtype_name(t->dtype), dtype_name(want));
+    return BELLMAN_OK;
+}
+
+bool is_contiguous(const bellman_tensor_t* t) {
+    int64_t expect = 1;
+    for (int i = t->ndim - 1; i >= 0; --i) {
+        if (t->shape[i] != 1 && t->stride[i] != expect) return false;
+        expect *= t->shape[i];
+    }
+    return true;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct PoolShape {
+    int64_t num_pages;
+    int H_kv, D, x;
+    bool fp8;
+};
+
+// K [NP, H_kv, D/x, 16, x], V [NP, H_kv, D, 16], same dtype, contiguous.
+int check_pools(const bellman_tensor_t* k, const bellman_tensor_t* v, PoolShape* ps, bool need_scales) {
+    int rc;
+    if ((rc = check_tensor(k, "k_pages", 5))) return rc;
+    if ((rc = check_tensor(v, "v_pages", 4))) return rc;
+    if (k->dtype != BELLMAN_BF16 && k->dtype != BELLMAN_FP8_E4M3FN)
+        return fail(BELLMAN_ERR_INVALID_ARG, "k_pages: dtype %s, expected bf16 or fp8_e4m3fn", dtype_name(k->dtype));
+    if (v->dtype != k->dtype)
+        return fail(BELLMAN_ERR_INVALID_ARG, "v_pages: dtype %s differs from k_pages %s", dtype_name(v->dtype),
+                    dtype_name(k->dtype));
+    const bool fp8 = k->dtype == BELLMAN_FP8_E4M3FN;
+    const int64_t x = fp8 ? 16 : 8;
+    if (k->shape[3] != kPage) return fail(BELLMAN_ERR_UNSUPPORTED, "k_pages: page size %lld, only 16 is supported", (long long)k->shape[3]);
+    if (k->shape[4] != x)
+        return fail(BELLMAN_ERR_INVALID_ARG, "k_pages: innermost chunk %lld, expected %lld (16 bytes)", (long long)k->shape[4], (long long)x);
+    const int64_t D = k->shape[2] * x;
+    if (v->shape[0] != k->shape[0] || v->shape[1] != k->shape[1] || v->shape[2] != D || v->shape[3] != kPage)
+        return fail(BELLMAN_ERR_INVALID_ARG, "v_pages: shape [%lld,%lld,%lld,%lld] does not match k_pages (expected [%lld,%lld,%lld,16])",
+                    (long long)v->shape[0], (long long)v->shape[1], (long long)v->shape[2], (long long)v->shape[3],
+                    (long long)k->shape[0], (long long)k->shape[1], (long long)D);
+    if (D != 64 && D != 128) return fail(BELLMAN_ERR_UNSUPPORTED, "head_dim %lld: only 64 and 128 are supported", (long long)D);
+    if (k->shape[1] < 1) return fail(BELLMAN_ERR_INVALID_ARG, "k_pages: no KV heads");
+    if (k->shape[0] > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "more than 2^31-1 pages");
+    if (!is_contiguous(k)) return fail(BELLMAN_ERR_UNSUPPORTED, "k_pages: must be contiguous");
+    if (!is_contiguous(v)) return fail(BELLMAN_ERR_UNSUPPORTED, "v_pages: must be contiguous");
+    if (!aligned(k->data, 16) || !aligned(v->data, 16))
+        return fail(BELLMAN_ERR_UNSUPPORTED, "k_pages/v_pages: data must be 16-byte aligned");
+    if (need_scales) {
+        if (fp8 && (!k->dequant_scale || !v->dequant_scale))
+            return fail(BELLMAN_ERR_INVALID_ARG, "fp8 pools need dequant_scale on both k_pages and v_pages");
+        if (!fp8 && (k->dequant_scale || v->dequant_scale))
+            return fail(BELLMAN_ERR_INVALID_ARG, "dequant_scale is only meaningful for fp8 pools");
+    }
+    ps->num_pages = k->shape[0];
+    ps->H_kv = (int)k->shape[1];
+    ps->D = (int)D;
+    ps->x = (int)x;
+    ps->fp8 = fp8;
+    return BELLMAN_OK;
+}
+
+int check_block_table(const bellman_tensor_t* bt, int64_t B) {
+    int rc;
+    if ((rc = check_tensor(bt, "block_table", 2))) return rc;
+    if ((rc = check_dtype(bt, "block_table", BELLMAN_INT32))) return rc;
+    if (bt->shape[0] != B)
+        return fail(BELLMAN_ERR_INVALID_ARG, "block_table: %lld rows for batch %lld", (long long)bt->shape[0], (long long)B);
+    if (B > 0 && bt->shape[1] < 1) return fail(BELLMAN_ERR_INVALID_ARG, "block_table: no page columns");
+    if (bt->shape[1] > (INT32_MAX / kPage)) return fail(BELLMAN_ERR_UNSUPPORTED, "block_table: too many columns");
+    if (bt->shape[1] > 1 && bt->stride[1] != 1) return fail(BELLMAN_ERR_UNSUPPORTED, "block_table: innermost dim must be contiguous");
+    if (bt->shape[0] > 1 && bt->stride[0] < bt->shape[1])
+        return fail(BELLMAN_ERR_INVALID_ARG, "block_table: row stride %lld < %lld columns", (long long)bt->stride[0], (long long)bt->shape[1]);
+    return BELLMAN_OK;
+}
+
+int check_seq_lens(const bellman_tensor_t* sl, int64_t B) {
+    int rc;
+    if ((rc = check_tensor(sl, "seq_lens", 1))) return rc;
+    if ((rc = check_dtype(sl, "seq_lens", BELLMAN_INT32))) return rc;
+    if (sl->shape[0] != B) return fail(BELLMAN_ERR_INVALID_ARG, "seq_lens: %lld entries for batch %lld", (long long)sl->shape[0], (long long)B);
+    if (B > 1 && sl->stride[0] != 1) return fail(BELLMAN_ERR_UNSUPPORTED, "seq_lens: must be contiguous");
+    return BELLMAN_OK;
+}
+
+// [B, H, D] with innermost contiguous; row strides keep 16-byte alignment.
+int check_rows(const bellman_tensor_t* t, const char* name, int32_t dtype, int64_t B, int64_t H, int64_t D, size_t align) {
+    int rc;
+    if ((rc = check_tensor(t, name, 3))) return rc;
+    if ((rc = check_dtype(t, name, dtype))) return rc;
+    if (t->shape[0] != B || t->shape[1] != H || t->shape[2] != D)
+        return fail(BELLMAN_ERR_INVALID_ARG, "%s: shape [%lld,%lld,%lld], expected [%lld,%lld,%lld]", name, (long long)t->shape[0],
+                    (long long)t->shape[1], (long long)t->shape[2], (long long)B, (long long)H, (long long)D);
+    if (t->stride[2] != 1) return fail(BELLMAN_ERR_UNSUPPORTED, "%s: innermost dim must be contiguous", name);
+    const size_t eb = (size_t)elem_size(dtype);
+    if (!aligned(t->data, align) || ((size_t)t->stride[0] * eb) % align || ((size_t)t->stride[1] * eb) % align)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "%s: rows must be %zu-byte aligned", name, align);
+    return BELLMAN_OK;
+}
+
+int launch_status(const char* what) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "%s launch: %s", what, hipGetErrorString(e));
+    return BELLMAN_OK;
+}
+
+int default_split_pages(int64_t B, int H_kv, int64_t max_pages, int cu_count) {
+    // Aim for about eight work items per resident wave when every request
+    // used its whole block-table row; the row width bounds the real length.
+    const double waves = (double)cu_count * 16.0;
+    const double pages = (double)B * H_kv * (double)max_pages;
+    double want = pages / (8.0 * waves);
+    int sp = 8;
+    while (sp < 64 && sp * 2 <= want) sp *= 2;
+    return sp;
+}
+
+}  // namespace
+
+// ================================================================== ABI ====
+
+extern "C" {
+
+const char* bellman_last_error(void) { return g_last_error; }
+
+const char* bellman_version(void) { return "0.1.0"; }
+
+int bellman_reserve_workspace(int64_t bytes) {
+    g_last_error[0] = 0;
+    if (bytes < 0) return fail(BELLMAN_ERR_INVALID_ARG, "negative workspace size");
+    int dev, rc;
+    if ((rc = current_device(&dev))) return rc;
+    char* base;
+    return ensure_workspace(dev, (size_t)bytes, &base);
+}
+
+void bellman_shutdown(void) {
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    for (int d = 0; d < kMaxDevices; ++d) {
+        if (g_ws[d].base) {
+            (void)hipSetDevice(d);
+            (void)hipDeviceSynchronize();
+            (void)hipFree(g_ws[d].base);
+            g_ws[d].base = nullptr;
+            g_ws[d].cap = 0;
+        }
+    }
+    (void)hipSetDevice(cur);
+}
+
+int bellman_device_errors(void* stream, int32_t* flags) {
+    g_last_error[0] = 0;
+    if (!flags) return fail(BELLMAN_ERR_INVALID_ARG, "flags: null pointer");
+    int dev, rc;
+    if ((rc = current_device(&dev))) return rc;
+    char* base;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    int32_t v = 0;
+    hipError_t e = hipMemcpyAsync(&v, base + offsetof(WorkspaceHeader, err_flags), sizeof v, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipMemsetAsync(base + offsetof(WorkspaceHeader, err_flags), 0, sizeof v, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "reading the device error word: %s", hipGetErrorString(e));
+    *flags = v;
+    return BELLMAN_OK;
+}
+
+int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_new, bellman_tensor_t* k_pages,
+                      bellman_tensor_t* v_pages, const bellman_tensor_t* block_table, bellman_tensor_t* seq_lens,
+                      void* stream) {
+    g_last_error[0] = 0;
+    int rc;
+    PoolShape ps;
+    if ((rc = check_pools(k_pages, v_pages, &ps, false))) return rc;
+    if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
+    const int64_t B = k_new->shape[0];
+    const size_t eb = ps.fp8 ? 1 : 2;
+    if ((rc = check_rows(k_new, "k_new", k_pages->dtype, B, ps.H_kv, ps.D, 16))) return rc;
+    if ((rc = check_rows(v_new, "v_new", k_pages->dtype, B, ps.H_kv, ps.D, eb))) return rc;
+    if ((rc = check_block_table(block_table, B))) return rc;
+    if ((rc = check_seq_lens(seq_lens, B))) return rc;
+    if (B > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "batch too large");
+    if (B == 0) return BELLMAN_OK;
+
+    int dev;
+    if ((rc = current_device(&dev))) return rc;
+    char* base;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+
+    AppendArgs a;
+    a.k_new = k_new->data;
+    a.v_new = v_new->data;
+    a.new_sb = k_new->stride[0];
+    a.new_sh = k_new->stride[1];
+    a.vnew_sb = v_new->stride[0];
+    a.vnew_sh = v_new->stride[1];
+    a.k_pages = k_pages->data;
+    a.v_pages = v_pages->data;
+    a.block_table = (const int32_t*)block_table->data;
+    a.bt_stride = block_table->shape[0] > 1 ? block_table->stride[0] : block_table->shape[1];
+    a.seq_lens = (int32_t*)seq_lens->data;
+    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.num_pages = ps.num_pages;
+    a.B = (int)B;
+    a.H_kv = ps.H_kv;
+    a.D = ps.D;
+    a.max_pages = (int)block_table->shape[1];
+    a.elem_bytes = (int)eb;
+    launch_kv_append(a, (hipStream_t)stream);
+    return launch_status("kv_append");
+}
+
+int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
+                                  const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                                  const bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
+                                  const bellman_attn_opts_t* opts, void* stream) {
+    g_last_error[0] = 0;
+    int rc;
+    PoolShape ps;
+    if ((rc = check_pools(k_pages, v_pages, &ps, true))) return rc;
+    if ((rc = check_tensor(q, "q", 3))) return rc;
+    const int64_t B = q->shape[0];
+    const int64_t H_q = q->shape[1];
+    if ((rc = check_rows(q, "q", BELLMAN_BF16, B, H_q, ps.D, 16))) return rc;
+    if ((rc = check_rows(out, "out", BELLMAN_BF16, B, H_q, ps.D, 8))) return rc;
+    if ((rc = check_block_table(block_table, B))) return rc;
+    if ((rc = check_seq_lens(seq_lens, B))) return rc;
+    if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
+    if (H_q < 1 || H_q % ps.H_kv != 0)
+        return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
+    const int64_t G = H_q / ps.H_kv;
+    if (G > 16) return fail(BELLMAN_ERR_UNSUPPORTED, "GQA group %lld > 16", (long long)G);
+    if (B > (1 << 24)) return fail(BELLMAN_ERR_UNSUPPORTED, "batch too large");
+    int split_pages = 0, impl = BELLMAN_IMPL_AUTO;
+    if (opts) {
+        split_pages = opts->split_pages;
+        impl = opts->impl;
+        if (split_pages < 0 || split_pages > 64)
+            return fail(BELLMAN_ERR_UNSUPPORTED, "split_pages %d outside [1, 64] (0 = default)", split_pages);
+        if (impl != BELLMAN_IMPL_AUTO && impl != BELLMAN_IMPL_MFMA && impl != BELLMAN_IMPL_VALU)
+            return fail(BELLMAN_ERR_INVALID_ARG, "unknown impl %d", impl);
+    }
+    if (impl == BELLMAN_IMPL_VALU) return fail(BELLMAN_ERR_UNSUPPORTED, "VALU kernel not built");
+    impl = BELLMAN_IMPL_MFMA;
+    if (B == 0) return BELLMAN_OK;
+
+    int dev;
+    if ((rc = current_device(&dev))) return rc;
+    if (g_cu_count[dev] == 0) {
+        int cu = 0;
+        hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
+        g_cu_count[dev] = cu;
+    }
+    const int64_t max_pages = block_table->shape[1];
+    if (split_pages == 0) {
+        const char* env = getenv("BELLMAN_SPLIT_PAGES");
+        split_pages = env ? atoi(env) : 0;
+        if (split_pages < 1 || split_pages > 64) split_pages = default_split_pages(B, ps.H_kv, max_pages, g_cu_count[dev]);
+    }
+    const int64_t max_splits = (max_pages + split_pages - 1) / split_pages;
+    const int64_t max_jobs = B * max_splits;
+    if (max_jobs * ps.H_kv > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "too many work items");
+
+    const size_t off_start = sizeof(WorkspaceHeader);
+    const size_t off_jobs = off_start + align256(sizeof(int32_t) * (size_t)(B + 1));
+    const size_t off_ml = off_jobs + align256(sizeof(int2) * (size_t)max_jobs);
+    const size_t off_o = off_ml + align256(sizeof(float2) * (size_t)(max_jobs * H_q));
+    const size_t total = off_o + align256(sizeof(float) * (size_t)(max_jobs * H_q * ps.D));
+    char* base;
+    if ((rc = ensure_workspace(dev, total, &base))) return rc;
+
+    AttnArgs a;
+    a.q = (const uint16_t*)q->data;
+    a.q_sb = q->stride[0];
+    a.q_sh = q->stride[1];
+    a.k_pages = k_pages->data;
+    a.v_pages = v_pages->data;
+    a.k_scale = k_pages->dequant_scale;
+    a.v_scale = v_pages->dequant_scale;
+    a.block_table = (const int32_t*)block_table->data;
+    a.bt_stride = B > 1 ? block_table->stride[0] : max_pages;
+    a.seq_lens = (const int32_t*)seq_lens->data;
+    a.out = (uint16_t*)out->data;
+    a.o_sb = out->stride[0];
+    a.o_sh = out->stride[1];
+    a.num_pages = ps.num_pages;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.B = (int)B;
+    a.H_q = (int)H_q;
+    a.H_kv = ps.H_kv;
+    a.G = (int)G;
+    a.D = ps.D;
+    a.max_pages = (int)max_pages;
+    a.split_pages = split_pages;
+    a.hdr = (WorkspaceHeader*)base;
+    a.job_start = (int32_t*)(base + off_start);
+    a.jobs = (int2*)(base + off_jobs);
+    a.part_ml = (float2*)(base + off_ml);
+    a.part_o = (float*)(base + off_o);
+
+    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][impl];
+    if (bpc == 0) bpc = attention_blocks_per_cu(impl, ps.fp8, ps.D);
+    int64_t grid = (int64_t)g_cu_count[dev] * bpc;
+    const int64_t waves_needed = (max_jobs * ps.H_kv + 3) / 4;
+    if (grid > waves_needed) grid = waves_needed;
+    if (grid < 1) grid = 1;
+
+    hipStream_t s = (hipStream_t)stream;
+    hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
+    hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;
+    launch_plan(a, s);
+    if ((rc = launch_status("plan"))) return rc;
+    if (ev0) {
+        hipError_t e = hipEventRecord(ev0, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    launch_attention(a, impl, ps.fp8, (int)grid, s);
+    if ((rc = launch_status("attention"))) return rc;
+    if (ev1) {
+        hipError_t e = hipEventRecord(ev1, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    launch_merge(a, s);
+    return launch_status("merge");
+}
+
+int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
+                             const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
+                             bellman_tensor_t* out, void* stream) {
+    return bellman_decode_attention_opts(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream);
+}
+
+}  // extern "C"

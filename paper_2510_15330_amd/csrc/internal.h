@@ -1,0 +1,74 @@
+// Internal declarations shared by the host ABI layer and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bellman {
+
+constexpr int kPage = 16;           // tokens per KV page
+constexpr int kWaveSize = 64;       // CDNA wavefront
+constexpr int kAttnBlock = 256;     // threads per attention workgroup (4 independent waves)
+
+// Device error word bits (also documented in bellman.h).
+constexpr int kErrAppendSlot = 1;
+constexpr int kErrLength = 2;
+constexpr int kErrPage = 4;
+
+// Header of the per-device workspace; the variable-size regions follow it.
+struct WorkspaceHeader {
+    int32_t err_flags;   // sticky error bits, cleared by the host
+    int32_t counter;     // work-stealing cursor of the attention kernel
+    int32_t njobs;       // number of (request, split) jobs of the current call
+    int32_t pad[61];
+};
+static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte aligned");
+
+struct AppendArgs {
+    const void* k_new;   // [B, H_kv, D]
+    const void* v_new;
+    int64_t new_sb, new_sh;        // strides (elements) of k_new/v_new rows
+    int64_t vnew_sb, vnew_sh;
+    void* k_pages;       // [NP, H_kv, D/x, 16, x]
+    void* v_pages;       // [NP, H_kv, D, 16]
+    const int32_t* block_table;
+    int64_t bt_stride;
+    int32_t* seq_lens;
+    int32_t* err;
+    int64_t num_pages;
+    int B, H_kv, D, max_pages, elem_bytes;
+};
+
+struct AttnArgs {
+    const uint16_t* q;   // bf16 [B, H_q, D]
+    int64_t q_sb, q_sh;
+    const void* k_pages;
+    const void* v_pages;
+    const float* k_scale;   // fp8 only, [B, H_kv]
+    const float* v_scale;
+    const int32_t* block_table;
+    int64_t bt_stride;
+    const int32_t* seq_lens;
+    uint16_t* out;       // bf16 [B, H_q, D]
+    int64_t o_sb, o_sh;
+    int64_t num_pages;
+    float scale_log2;    // softmax scale * log2(e)
+    int B, H_q, H_kv, G, D, max_pages, split_pages;
+    // workspace
+    WorkspaceHeader* hdr;
+    int32_t* job_start;  // [B + 1]
+    int2* jobs;          // [max_jobs] (request, split)
+    float2* part_ml;     // [max_jobs * H_q] (running max in log2 units, sum)
+    float* part_o;       // [max_jobs * H_q * D]
+};
+
+// Launchers (kernels.hip).  They only enqueue; errors come back through
+// hipGetLastError in the caller.
+void launch_kv_append(const AppendArgs& a, hipStream_t s);
+void launch_plan(const AttnArgs& a, hipStream_t s);
+void launch_attention(const AttnArgs& a, int impl, bool fp8, int grid, hipStream_t s);
+void launch_merge(const AttnArgs& a, hipStream_t s);
+// Resident workgroups per CU of the attention kernel variant (occupancy).
+int attention_blocks_per_cu(int impl, bool fp8, int D);
+
+}  // namespace bellman

@@ -1,0 +1,283 @@
+"""GPU parity: the HIP path through the C ABI against the binary64 oracle, on
+the same seeded inputs.  KV append is compared byte for byte over the whole
+pools; attention within max-abs 1e-2 / rel-L2 2e-3 (bf16 KV) and 3e-2 / 1e-2
+(fp8 KV).  Full-size workloads are checked on sampled requests the oracle can
+afford, in the launch configuration the benchmark times, plus properties that
+hold at any size."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests import _dense as dn
+from tests import _gpu as G
+
+pytestmark = pytest.mark.gpu
+
+bl = pytest.importorskip("paper_2510_15330_amd")
+from paper_2510_15330_amd import workloads as wl  # noqa: E402
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    bl.library()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev_case(case, kv="bf16"):
+    """Device tensors of a tests._dense.random_case."""
+    if kv == "bf16":
+        kp = torch.from_numpy(case["k_pages"].view(np.int16)).view(torch.bfloat16)
+        vp = torch.from_numpy(case["v_pages"].view(np.int16)).view(torch.bfloat16)
+    else:
+        kp = torch.from_numpy(case["k_pages"])
+        vp = torch.from_numpy(case["v_pages"])
+    d = dict(
+        q=torch.from_numpy(case["q_bits"].view(np.int16)).view(torch.bfloat16).cuda(),
+        k=kp.cuda(), v=vp.cuda(),
+        bt=torch.from_numpy(case["block_table"]).cuda(),
+        sl=torch.from_numpy(case["seq_lens"]).cuda(),
+        ks=None if case["k_scale"] is None else torch.from_numpy(case["k_scale"]).cuda(),
+        vs=None if case["v_scale"] is None else torch.from_numpy(case["v_scale"]).cuda(),
+    )
+    B, H_q, D = case["q_bits"].shape
+    d["out"] = torch.full((B, H_q, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    return d
+
+
+def run_case(d, scale, **kw):
+    bl.decode_attention(d["q"], d["k"], d["v"], d["bt"], d["sl"], scale, d["out"],
+                        k_scale=d["ks"], v_scale=d["vs"], **kw)
+    torch.cuda.synchronize()
+    return G.out_f64(d["out"])
+
+
+def oracle_case(case, scale, kv="bf16"):
+    return oracle.decode_attention(case["q_bits"], case["k_pages"], case["v_pages"], case["block_table"],
+                                   case["seq_lens"], scale, G.kv_code(kv), case["k_scale"], case["v_scale"])
+
+
+# ------------------------------------------------------------ tiny config ---
+
+@pytest.mark.parametrize("reading", ["after", "before"])
+def test_tiny_append_bitexact_and_attention(reading):
+    w = G.to_device(wl.build("tiny", seed=0, tiny_reading=reading))
+    # oracle side: host copies of the initial state
+    kp, vp = G.bits16(w.k_pages), G.bits16(w.v_pages)
+    sl = w.seq_lens.cpu().numpy().astype(np.int32)
+    oracle.kv_append(G.bits16(w.k_new[0]), G.bits16(w.v_new[0]), kp, vp, w.block_table.cpu().numpy(), sl)
+    out = torch.full((w.B, w.H_q, w.D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    print(f"tiny reading={reading} lens0={list(w.lens0)}", flush=True)
+    G.gpu_step(w, 0, out)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    assert np.array_equal(w.seq_lens.cpu().numpy(), sl)
+    assert np.array_equal(G.bits16(w.k_pages), kp)
+    assert np.array_equal(G.bits16(w.v_pages), vp)
+    ref = oracle.decode_attention(G.bits16(w.q[0]), kp, vp, w.block_table.cpu().numpy(), sl, w.scale)
+    G.assert_close(G.out_f64(out), ref, "bf16", f"tiny/{reading}")
+    if reading == "after":
+        # the length-1 request returns its only V row exactly
+        v_row = ref[0]
+        assert np.array_equal(G.out_f64(out)[0], v_row)
+
+
+@pytest.mark.parametrize("split", [1, 2, 3, 8, 64])
+def test_tiny_split_sizes(split):
+    w = G.to_device(wl.build("tiny", seed=1))
+    out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    G.gpu_step(w, 0, out, split_pages=split)
+    torch.cuda.synchronize()
+    ref = G.oracle_full(w, 0)
+    G.assert_close(G.out_f64(out), ref, "bf16", f"split={split}")
+
+
+# ------------------------------------------------------ llama3-8b config ---
+
+def test_llama3_8b_steps():
+    w = G.to_device(wl.build("llama3_8b", seed=0))
+    kp, vp = G.bits16(w.k_pages), G.bits16(w.v_pages)
+    sl = w.seq_lens.cpu().numpy().astype(np.int32)
+    bt = w.block_table.cpu().numpy()
+    out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    check = {0, 1, 50, w.steps - 1}
+    for step in range(w.steps):
+        G.gpu_step(w, step, out)
+        oracle.kv_append(G.bits16(w.k_new[step]), G.bits16(w.v_new[step]), kp, vp, bt, sl)
+        if step in check:
+            torch.cuda.synchronize()
+            ref = oracle.decode_attention(G.bits16(w.q[step]), kp, vp, bt, sl, w.scale)
+            ma, rl = G.assert_close(G.out_f64(out), ref, "bf16", f"llama3_8b step {step}")
+            print(f"llama3_8b step {step}: max-abs {ma:.2e} rel-L2 {rl:.2e}", flush=True)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    assert np.array_equal(w.seq_lens.cpu().numpy(), sl)
+    assert np.array_equal(G.bits16(w.k_pages), kp), "K pool differs after 100 appends"
+    assert np.array_equal(G.bits16(w.v_pages), vp), "V pool differs after 100 appends"
+
+
+# ------------------------------------------------- full-size, sampled rows ---
+
+@pytest.mark.parametrize("name", ["summarization", "summarization_capped", "stress_fp8"])
+def test_full_size_sampled(name):
+    w = wl.build(name, seed=0, device="cuda", steps=2)
+    out = torch.full((w.B, w.H_q, w.D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    print(f"{name}: B={w.B} pages={w.num_pages} mean L={w.lens0.mean():.0f}", flush=True)
+    G.gpu_step(w, 0, out)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    got = G.out_f64(out)
+    assert np.all(np.isfinite(got))
+    L = w.seq_lens.cpu().numpy()
+    rng = np.random.default_rng(5)
+    reqs = sorted(set([int(np.argmax(L)), int(np.argmin(L))] + rng.choice(w.B, 6, replace=False).tolist()))
+    ref = G.oracle_rows(w, 0, reqs)
+    ma, rl = G.assert_close(got[reqs], ref, w.kv, f"{name} sampled {reqs}")
+    print(f"{name}: sampled {reqs} max-abs {ma:.2e} rel-L2 {rl:.2e}", flush=True)
+    # second step: lengths advanced by one on every request
+    G.gpu_step(w, 1, out)
+    torch.cuda.synchronize()
+    assert np.array_equal(w.seq_lens.cpu().numpy(), L + 1)
+    ref = G.oracle_rows(w, 1, reqs[:3])
+    G.assert_close(G.out_f64(out)[reqs[:3]], ref, w.kv, f"{name} step 1")
+
+
+# ------------------------------------------------------------ invariants ---
+
+def test_page_permutation_and_determinism_bitexact():
+    rng = np.random.default_rng(21)
+    lens = [300, 17, 1000, 64]
+    case = dn.random_case(rng, 4, 32, 8, 128, lens)
+    d = dev_case(case)
+    a = run_case(d, 0.088, split_pages=4)
+    b = run_case(d, 0.088, split_pages=4)
+    assert np.array_equal(a, b), "run-to-run differs"
+    perm = rng.permutation(case["num_pages"]).astype(np.int32)
+    kp = np.empty_like(case["k_pages"])
+    vp = np.empty_like(case["v_pages"])
+    kp[perm] = case["k_pages"]
+    vp[perm] = case["v_pages"]
+    bt = case["block_table"].copy()
+    bt[bt >= 0] = perm[bt[bt >= 0]]
+    d2 = dev_case(dict(case, k_pages=kp, v_pages=vp, block_table=bt))
+    c = run_case(d2, 0.088, split_pages=4)
+    assert np.array_equal(a, c), "page permutation changed the output"
+    # a request alone equals the same request inside the batch
+    for bi in range(4):
+        sub = dict(case, q_bits=case["q_bits"][bi:bi + 1], block_table=case["block_table"][bi:bi + 1],
+                   seq_lens=case["seq_lens"][bi:bi + 1])
+        one = run_case(dev_case(sub), 0.088, split_pages=4)
+        assert np.array_equal(one[0], a[bi]), f"batch independence b={bi}"
+    G.assert_close(a, oracle_case(case, 0.088), "bf16", "invariant case")
+
+
+def test_closed_forms_exact():
+    rng = np.random.default_rng(22)
+    lens = [1, 40, 700]
+    case = dn.random_case(rng, 3, 8, 2, 128, lens)
+    # constant V rows (per head) and a ones column in V dim 3
+    cv = torch.from_numpy(rng.standard_normal((3, 2, 128)).astype(np.float32)).to(torch.bfloat16)
+    cv = cv.view(torch.int16).numpy().view(np.uint16)
+    one = np.uint16(0x3F80)
+    for b in range(3):
+        case["dense_v"][b][:] = cv[b][None]
+        case["dense_v"][b][:, :, 3] = one
+    kp, vp = dn.write_pools(case["dense_k"], case["dense_v"], lens, case["page_lists"], case["num_pages"],
+                            2, 128, 8, np.uint16(0x7FC0))
+    case.update(k_pages=kp, v_pages=vp)
+    for split in (1, 8):
+        got = run_case(dev_case(case), 0.088, split_pages=split)
+        for b in range(3):
+            for h in range(8):
+                ref = dn.bits_to_f64_bf16(cv[b][h // 4]).copy()
+                ref[3] = 1.0
+                assert np.array_equal(got[b, h], ref), f"constant V not exact b={b} h={h} split={split}"
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,D,lens,kv", [
+    (3, 8, 8, 64, [5, 16, 33], "bf16"),          # G = 1
+    (2, 16, 1, 128, [100, 1], "bf16"),           # G = 16
+    (4, 4, 2, 64, [0, 1, 0, 47], "bf16"),        # empty requests
+    (1, 32, 8, 128, [4096], "bf16"),             # B = 1, long
+    (3, 64, 8, 128, [1, 129, 2000], "fp8"),      # fp8, G = 8
+    (2, 8, 2, 64, [31, 320], "fp8"),             # fp8, D = 64
+])
+def test_edge_shapes(B, Hq, Hkv, D, lens, kv):
+    rng = np.random.default_rng(sum(lens) + D)
+    case = dn.random_case(rng, B, Hq, Hkv, D, lens, kv)
+    scale = float(np.float32(1.0 / np.sqrt(D)))
+    ref = oracle_case(case, scale, kv)
+    for split in (0, 1, 5):
+        got = run_case(dev_case(case, kv), scale, split_pages=split)
+        G.assert_close(got, ref, kv, f"edge {B},{Hq},{Hkv},{D},{lens},{kv} split={split}")
+        for b, L in enumerate(lens):
+            if L == 0:
+                assert np.all(got[b] == 0.0)
+
+
+def test_fp8_every_code_through_single_token_rows():
+    """Length-1 requests return their V row times the V scale; with scale 1 the
+    output is the e4m3fn value itself, so every finite code is checked."""
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, D = 2, 8, 1, 128
+    case = dn.random_case(rng, B, Hq, Hkv, D, [1, 1], "fp8")
+    allc = np.arange(256, dtype=np.uint16).astype(np.uint8)
+    allc[0x7F] = 0
+    allc[0xFF] = 0
+    case["dense_v"][0][0, 0] = allc[:128]
+    case["dense_v"][1][0, 0] = allc[128:]
+    case["v_scale"][:] = 1.0
+    kp, vp = dn.write_pools(case["dense_k"], case["dense_v"], [1, 1], case["page_lists"], case["num_pages"],
+                            Hkv, D, 16, np.uint8(0x7F))
+    case.update(k_pages=kp, v_pages=vp)
+    got = run_case(dev_case(case, "fp8"), 0.1)
+    ref = dn.codes_to_f64_fp8(allc).reshape(2, 128)
+    for b in range(2):
+        for h in range(Hq):
+            assert np.array_equal(got[b, h], ref[b]), f"fp8 code decode b={b} h={h}"
+
+
+def test_bad_block_table_entry_is_flagged_not_read():
+    rng = np.random.default_rng(24)
+    case = dn.random_case(rng, 2, 8, 2, 64, [40, 20])
+    d = dev_case(case)
+    bl.device_errors()
+    bt = d["bt"].clone()
+    bt[0, 1] = case["num_pages"] + 1000      # out of the pool: must be skipped, never dereferenced
+    d["bt"] = bt
+    got = run_case(d, 0.125)
+    assert bl.device_errors() & 4
+    assert np.all(np.isnan(got[0]))
+    G.assert_close(got[1:], oracle_case(dict(case, q_bits=case["q_bits"][1:], block_table=case["block_table"][1:],
+                                             seq_lens=case["seq_lens"][1:]), 0.125), "bf16", "untouched request")
+
+
+def test_append_out_of_table_is_skipped():
+    w = G.to_device(wl.build("tiny", seed=2))
+    before_k = G.bits16(w.k_pages)
+    sl = w.seq_lens.clone()
+    sl[2] = w.max_pages * 16                  # no page left for this request
+    bl.device_errors()
+    bl.kv_append(w.k_new[0], w.v_new[0], w.k_pages, w.v_pages, w.block_table, sl)
+    torch.cuda.synchronize()
+    assert bl.device_errors() & 1
+    assert sl[2].item() == w.max_pages * 16
+    assert sl[0].item() == w.lens0[0] + 1
+    after_k = G.bits16(w.k_pages)
+    assert (before_k != after_k).sum() > 0
+
+
+def test_empty_batch_is_noop():
+    q = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((4, 2, 8, 16, 8), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros((4, 2, 64, 16), dtype=torch.bfloat16, device="cuda")
+    bt = torch.empty((0, 1), dtype=torch.int32, device="cuda")
+    sl = torch.empty((0,), dtype=torch.int32, device="cuda")
+    out = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
+    bl.decode_attention(q, k, v, bt, sl, 0.125, out)
+    torch.cuda.synchronize()
