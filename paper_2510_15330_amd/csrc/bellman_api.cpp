@@ -164,6 +164,7 @@ int check_pools(const bellman_tensor_t* k, const bellman_tensor_t* v, PoolShape*
                     (long long)k->shape[0], (long long)k->shape[1], (long long)D);
     if (D != 64 && D != 128) return fail(BELLMAN_ERR_UNSUPPORTED, "head_dim %lld: only 64 and 128 are supported", (long long)D);
     if (k->shape[1] < 1) return fail(BELLMAN_ERR_INVALID_ARG, "k_pages: no KV heads");
+    if (k->shape[0] < 1) return fail(BELLMAN_ERR_INVALID_ARG, "k_pages: the pool has no pages");
     if (k->shape[0] > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "more than 2^31-1 pages");
     if (!is_contiguous(k)) return fail(BELLMAN_ERR_UNSUPPORTED, "k_pages: must be contiguous");
     if (!is_contiguous(v)) return fail(BELLMAN_ERR_UNSUPPORTED, "v_pages: must be contiguous");
@@ -227,14 +228,13 @@ int launch_status(const char* what) {
     return BELLMAN_OK;
 }
 
-int default_split_pages(int64_t B, int H_kv, int64_t max_pages, int cu_count) {
-    // Aim for about eight work items per resident wave when every request
-    // used its whole block-table row; the row width bounds the real length.
-    const double waves = (double)cu_count * 16.0;
+int default_split_pages(int64_t B, int H_kv, int64_t max_pages, int64_t resident_waves) {
+    // Largest split (fewest items, least per-item and merge overhead) that
+    // still gives every resident wave at least two items when each request
+    // filled its block-table row; the row width bounds the real length.
     const double pages = (double)B * H_kv * (double)max_pages;
-    double want = pages / (8.0 * waves);
-    int sp = 8;
-    while (sp < 64 && sp * 2 <= want) sp *= 2;
+    int sp = 64;
+    while (sp > 8 && pages / sp < 2.0 * (double)resident_waves) sp /= 2;
     return sp;
 }
 
@@ -379,10 +379,14 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         g_cu_count[dev] = cu;
     }
     const int64_t max_pages = block_table->shape[1];
+    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][impl];
+    if (bpc == 0) bpc = attention_blocks_per_cu(impl, ps.fp8, ps.D);
+    const int64_t resident_blocks = (int64_t)g_cu_count[dev] * bpc;
     if (split_pages == 0) {
         const char* env = getenv("BELLMAN_SPLIT_PAGES");
         split_pages = env ? atoi(env) : 0;
-        if (split_pages < 1 || split_pages > 64) split_pages = default_split_pages(B, ps.H_kv, max_pages, g_cu_count[dev]);
+        if (split_pages < 1 || split_pages > 64)
+            split_pages = default_split_pages(B, ps.H_kv, max_pages, resident_blocks * (kAttnBlock / kWaveSize));
     }
     const int64_t max_splits = (max_pages + split_pages - 1) / split_pages;
     const int64_t max_jobs = B * max_splits;
@@ -390,7 +394,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
 
     const size_t off_start = sizeof(WorkspaceHeader);
     const size_t off_jobs = off_start + align256(sizeof(int32_t) * (size_t)(B + 1));
-    const size_t off_ml = off_jobs + align256(sizeof(int2) * (size_t)max_jobs);
+    const size_t off_ml = off_jobs + align256(sizeof(int4) * (size_t)max_jobs);
     const size_t off_o = off_ml + align256(sizeof(float2) * (size_t)(max_jobs * H_q));
     const size_t total = off_o + align256(sizeof(float) * (size_t)(max_jobs * H_q * ps.D));
     char* base;
@@ -421,13 +425,11 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.split_pages = split_pages;
     a.hdr = (WorkspaceHeader*)base;
     a.job_start = (int32_t*)(base + off_start);
-    a.jobs = (int2*)(base + off_jobs);
+    a.jobs = (int4*)(base + off_jobs);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
 
-    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][impl];
-    if (bpc == 0) bpc = attention_blocks_per_cu(impl, ps.fp8, ps.D);
-    int64_t grid = (int64_t)g_cu_count[dev] * bpc;
+    int64_t grid = resident_blocks;
     const int64_t waves_needed = (max_jobs * ps.H_kv + 3) / 4;
     if (grid > waves_needed) grid = waves_needed;
     if (grid < 1) grid = 1;

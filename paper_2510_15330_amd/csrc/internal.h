@@ -57,7 +57,7 @@ struct AttnArgs {
     // workspace
     WorkspaceHeader* hdr;
     int32_t* job_start;  // [B + 1]
-    int2* jobs;          // [max_jobs] (request, split)
+    int4* jobs;          // [max_jobs] (request, split, clamped length, 0)
     float2* part_ml;     // [max_jobs * H_q] (running max in log2 units, sum)
     float* part_o;       // [max_jobs * H_q * D]
 };

@@ -83,8 +83,8 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 
 // -------------------------------------------------------------- planner ---
 // One workgroup: split each request into chunks of split_pages pages, lay
-// the (request, split) jobs out request-major with an exclusive scan, and
-// reset the work-stealing cursor.
+// the (request, split, clamped length) jobs out request-major with an
+// exclusive scan, and reset the work-stealing cursor.
 __global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
     __shared__ int scan[1024];
     __shared__ int carry;
@@ -94,9 +94,9 @@ __global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
     __syncthreads();
     for (int base = 0; base < a.B; base += 1024) {
         const int b = base + tid;
-        int ns = 0;
+        int ns = 0, L = 0;
         if (b < a.B) {
-            int L = a.seq_lens[b];
+            L = a.seq_lens[b];
             if (L < 0 || L > maxL) {
                 atomicOr(&a.hdr->err_flags, kErrLength);
                 L = L < 0 ? 0 : maxL;
@@ -115,7 +115,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
         const int excl = carry + scan[tid] - ns;
         if (b < a.B) {
             a.job_start[b] = excl;
-            for (int s = 0; s < ns; ++s) a.jobs[excl + s] = make_int2(b, s);
+            for (int s = 0; s < ns; ++s) a.jobs[excl + s] = make_int4(b, s, L, 0);
         }
         __syncthreads();
         if (tid == 1023) carry += scan[1023];
@@ -129,19 +129,22 @@ __global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------ partial attention (MFMA) --
-// Each wave repeatedly takes one work item = (request b, split s, KV head g)
-// from a device-wide cursor and streams the split's pages:
+// Each wave takes work items = (request b, split s, KV head g) in turn and
+// streams each split's pages two at a time:
 //   S^T[slot, head] = K_page[slot, :] . Q^T[:, head]   (v_mfma 16x16x32 bf16)
-//   online softmax per head in base 2
-//   O^T[dim, head] += V_page^T[dim, slot] . P^T[slot, head]   (v_mfma 16x16x16)
+//   online softmax per head in base 2, once per 32 tokens
+//   O^T[dim, head] += V_pair^T[dim, token] . P^T[token, head]  (v_mfma 16x16x32)
 // Lane l = 16*qg + n.  In the QK product n is the page slot (A row) and the
 // query head of the group (B column); the result leaves lane (qg, n) with the
-// scores of head n at slots 4qg..4qg+3, which are exactly the four B
-// elements the PV product needs from that lane, so no data crosses lanes
-// except the max/sum reductions over qg.  P enters the PV product as a bf16
-// pair hi + lo (hi = truncation, lo = rounded remainder), which keeps P to
-// about 2^-16 relative.  Slots past the request's length are excluded: their
-// scores become -inf and their V elements are replaced by zeros.
+// scores of head n at slots 4qg..4qg+3 of each page of the pair.  Those eight
+// scores are exactly the eight B elements the PV product needs from that lane
+// (the contraction index is paired with tokens the same way in the A operand),
+// so nothing crosses lanes except the max/sum reductions over qg.  P enters
+// the PV product as a bf16 pair hi + lo (hi = P truncated to bf16, lo = the
+// remainder truncated), which keeps P to about 2^-14 relative.  Slots past the
+// request's length are excluded: their scores become -inf and their V
+// elements are replaced by zeros.  O is rescaled only when a running max
+// grows (exact: otherwise the factor is 1).
 template <int D, bool FP8>
 struct PageRegs {
     static constexpr int NT = D / 16;
@@ -150,6 +153,14 @@ struct PageRegs {
     u32x4 k[KC];
     typename std::conditional<FP8, uint32_t, u32x2>::type v[NT];
 };
+
+// K/V pages are read exactly once per step: non-temporal loads keep them from
+// displacing reusable lines in the caches, which measurably raises the
+// sustained read rate of the gather.
+template <typename T>
+__device__ __forceinline__ T ld_stream(const char* p) {
+    return __builtin_nontemporal_load((const T*)p);
+}
 
 template <int D, bool FP8>
 __device__ __forceinline__ void load_page(PageRegs<D, FP8>& r, const char* kbase, const char* vbase,
@@ -160,37 +171,28 @@ __device__ __forceinline__ void load_page(PageRegs<D, FP8>& r, const char* kbase
         // covers 1 KiB contiguous.
 #pragma unroll
         for (int j = 0; j < PageRegs<D, FP8>::KC; ++j)
-            r.k[j] = *(const u32x4*)(kbase + ((size_t)((4 * j + qg) * kPage + n)) * 16);
-        // V dims 16t + n, slots 4qg..4qg+3: 8 bytes.
+            r.k[j] = ld_stream<u32x4>(kbase + ((size_t)((4 * j + qg) * kPage + n)) * 16);
+        // V dims 16t + n, slots 4qg..4qg+3: 8 bytes; 512 bytes contiguous per instruction.
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            r.v[t] = *(const u32x2*)(vbase + ((size_t)((16 * t + n) * kPage + 4 * qg)) * 2);
+            r.v[t] = ld_stream<u32x2>(vbase + ((size_t)((16 * t + n) * kPage + 4 * qg)) * 2);
     } else {
         // K chunk c = qg + 4i (16 dims), slot n: 16 bytes.
 #pragma unroll
         for (int i = 0; i < PageRegs<D, FP8>::KC; ++i)
-            r.k[i] = *(const u32x4*)(kbase + ((size_t)((qg + 4 * i) * kPage + n)) * 16);
+            r.k[i] = ld_stream<u32x4>(kbase + ((size_t)((qg + 4 * i) * kPage + n)) * 16);
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            r.v[t] = *(const uint32_t*)(vbase + (size_t)((16 * t + n) * kPage + 4 * qg));
+            r.v[t] = ld_stream<uint32_t>(vbase + (size_t)((16 * t + n) * kPage + 4 * qg));
     }
 }
 
+// Scores of one page: lane (qg, n) gets head n at slots 4qg..4qg+3.
 template <int D, bool FP8>
-struct AttnState {
-    f32x4 o[D / 16];
-    float m;   // running max, log2 units
-    float l;   // this lane's partial sum of weights
-};
-
-template <int D, bool FP8>
-__device__ __forceinline__ void attend_page(AttnState<D, FP8>& st, const PageRegs<D, FP8>& r,
-                                            const bf16x8 (&bq)[D / 32], float sl, int nv, int qg) {
-    constexpr int NT = D / 16;
-    constexpr int KS = D / 32;
-    f32x4 sacc = {0.f, 0.f, 0.f, 0.f};
+__device__ __forceinline__ f32x4 page_scores(const PageRegs<D, FP8>& r, const bf16x8 (&bq)[D / 32]) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < KS; ++j) {
+    for (int j = 0; j < D / 32; ++j) {
         u32x4 kk;
         if constexpr (!FP8) {
             kk = r.k[j];
@@ -203,58 +205,98 @@ __device__ __forceinline__ void attend_page(AttnState<D, FP8>& st, const PageReg
             kk.z = fp8x2_to_bf16x2(w1, false);
             kk.w = fp8x2_to_bf16x2(w1, true);
         }
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kk), bq[j], sacc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kk), bq[j], acc, 0, 0, 0);
     }
+    return acc;
+}
 
-    float x[4];
+// Four bf16 V elements (slots 4qg..4qg+3 of dim 16t + n) as the lane's half
+// of a PV A operand, zeroed at slots >= nv.
+template <int D, bool FP8>
+__device__ __forceinline__ u32x2 v_quad(const PageRegs<D, FP8>& r, int t, int nv, int qg) {
+    u32x2 vv;
+    if constexpr (!FP8) {
+        vv = r.v[t];
+    } else {
+        vv.x = fp8x2_to_bf16x2(r.v[t], false);
+        vv.y = fp8x2_to_bf16x2(r.v[t], true);
+    }
+    if (nv < kPage) {
+        const int k = nv - 4 * qg;  // live elements among this lane's four
+        vv.x &= k >= 2 ? 0xffffffffu : (k == 1 ? 0x0000ffffu : 0u);
+        vv.y &= k >= 4 ? 0xffffffffu : (k == 3 ? 0x0000ffffu : 0u);
+    }
+    return vv;
+}
+
+template <int D>
+struct AttnState {
+    f32x4 o[D / 16];
+    float m;   // running max, log2 units (same in the four qg lanes of a head)
+    float l;   // this lane's partial sum of weights
+};
+
+// Pack the upper halves of two fp32 bit patterns into one bf16 pair.
+__device__ __forceinline__ uint32_t pack_hi16(uint32_t lo, uint32_t hi) {
+    return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
+}
+
+template <int D, bool FP8>
+__device__ __forceinline__ void attend_pair(AttnState<D>& st, const PageRegs<D, FP8>& ra, const PageRegs<D, FP8>& rb,
+                                            const bf16x8 (&bq)[D / 32], float sl, int nva, int nvb, int qg) {
+    constexpr int NT = D / 16;
+    const f32x4 sa = page_scores<D, FP8>(ra, bq);
+    f32x4 sb = {0.f, 0.f, 0.f, 0.f};
+    if (nvb > 0) sb = page_scores<D, FP8>(rb, bq);
+
+    float x[8];
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        x[i] = (4 * qg + i < nv) ? sacc[i] * sl : -INFINITY;
-        mx = fmaxf(mx, x[i]);
+        x[i] = (4 * qg + i < nva) ? sa[i] * sl : -INFINITY;
+        x[4 + i] = (4 * qg + i < nvb) ? sb[i] * sl : -INFINITY;
+        mx = fmaxf(mx, fmaxf(x[i], x[4 + i]));
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float m_new = fmaxf(st.m, mx);
-    const float alpha = fast_exp2(st.m - m_new);
-    st.m = m_new;
+    if (__any(m_new > st.m)) {
+        const float alpha = fast_exp2(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) st.o[t] *= alpha;
+        st.m = m_new;
+    }
 
-    s16x4 ph, pl;
+    uint32_t ph[4], pl[4];
     float psum = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const float p = fast_exp2(x[i] - m_new);
-        psum += p;
-        const uint32_t u = __float_as_uint(p);
-        const float hi = __uint_as_float(u & 0xffff0000u);
-        ph[i] = (short)(u >> 16);
-        pl[i] = (short)f32_to_bf16_rne(p - hi);
+    for (int i = 0; i < 8; i += 2) {
+        const float p0 = fast_exp2(x[i] - st.m);
+        const float p1 = fast_exp2(x[i + 1] - st.m);
+        psum += p0 + p1;
+        const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
+        const float r0 = p0 - __uint_as_float(u0 & 0xffff0000u);
+        const float r1 = p1 - __uint_as_float(u1 & 0xffff0000u);
+        ph[i / 2] = pack_hi16(u0, u1);
+        pl[i / 2] = pack_hi16(__float_as_uint(r0), __float_as_uint(r1));
     }
-    st.l = st.l * alpha + psum;
+    st.l += psum;
+    const bf16x8 bph = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
+    const bf16x8 bpl = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
 
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        st.o[t] *= alpha;
-        u32x2 vv;
-        if constexpr (!FP8) {
-            vv = r.v[t];
-        } else {
-            vv.x = fp8x2_to_bf16x2(r.v[t], false);
-            vv.y = fp8x2_to_bf16x2(r.v[t], true);
-        }
-        s16x4 av = __builtin_bit_cast(s16x4, vv);
-        if (nv < kPage) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (4 * qg + i >= nv) av[i] = 0;
-        }
-        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, ph, st.o[t], 0, 0, 0);
-        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, pl, st.o[t], 0, 0, 0);
+        const u32x2 va = v_quad<D, FP8>(ra, t, nva, qg);
+        const u32x2 vb = v_quad<D, FP8>(rb, t, nvb, qg);
+        const bf16x8 av = __builtin_bit_cast(bf16x8, u32x4{va.x, va.y, vb.x, vb.y});
+        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bph, st.o[t], 0, 0, 0);
+        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bpl, st.o[t], 0, 0, 0);
     }
 }
 
 template <int D, bool FP8>
-__global__ void __launch_bounds__(kAttnBlock) attn_mfma_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu(2))) attn_mfma_kernel(AttnArgs a) {
     constexpr int NT = D / 16;
     constexpr int KS = D / 32;
     constexpr int EB = FP8 ? 1 : 2;
@@ -262,19 +304,20 @@ __global__ void __launch_bounds__(kAttnBlock) attn_mfma_kernel(AttnArgs a) {
     const int qg = lane >> 4;
     const int n = lane & 15;
     const int total = a.hdr->njobs * a.H_kv;
-    const int maxL = a.max_pages * kPage;
     const size_t tile_bytes = (size_t)D * kPage * EB;
+    const size_t page_stride = (size_t)a.H_kv * tile_bytes;
 
-    for (;;) {
-        int item = 0;
-        if (lane == 0) item = atomicAdd(&a.hdr->counter, 1);
-        item = __builtin_amdgcn_readfirstlane(item);
-        if (item >= total) break;
+    // Items are dealt round-robin over all resident waves: wave w takes items
+    // w, w + W, w + 2W, ...  Consecutive items are the KV heads of one
+    // (request, split) job, so neighbouring waves get equal-sized items and
+    // every wave's share averages over many jobs.
+    const int waves = gridDim.x * (kAttnBlock / kWaveSize);
+    for (int item = blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6); item < total; item += waves) {
+
         const int job = item / a.H_kv;
         const int g = item - job * a.H_kv;
-        const int2 js = a.jobs[job];
-        const int b = js.x, s = js.y;
-        const int L = min(max(a.seq_lens[b], 0), maxL);
+        const int4 js = a.jobs[job];
+        const int b = js.x, s = js.y, L = js.z;
         const int np_total = (L + kPage - 1) / kPage;
         const int nsplit = (np_total + a.split_pages - 1) / a.split_pages;
         const int p_begin = s * a.split_pages;
@@ -284,7 +327,7 @@ __global__ void __launch_bounds__(kAttnBlock) attn_mfma_kernel(AttnArgs a) {
         int my_pg = 0;
         if (lane < np) my_pg = a.block_table[(int64_t)b * a.bt_stride + p_begin + lane];
         const bool lane_bad = lane < np && (my_pg < 0 || (int64_t)my_pg >= a.num_pages);
-        const bool bad = __ballot(lane_bad) != 0;
+        const bool bad = __any(lane_bad);
         if (bad && lane == 0) atomicOr(&a.hdr->err_flags, kErrPage);
 
         // query operand: lane (qg, n) holds head g*G+n (zeros past the group)
@@ -303,59 +346,63 @@ __global__ void __launch_bounds__(kAttnBlock) attn_mfma_kernel(AttnArgs a) {
         }
         const float sl = FP8 ? a.scale_log2 * a.k_scale[(int64_t)b * a.H_kv + g] : a.scale_log2;
 
-        AttnState<D, FP8> st;
+        AttnState<D> st;
 #pragma unroll
         for (int t = 0; t < NT; ++t) st.o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         st.m = -INFINITY;
         st.l = 0.f;
 
-        if (!bad && np > 0) {
+        if (!bad) {
             const char* kpool = (const char*)a.k_pages + (size_t)g * tile_bytes;
             const char* vpool = (const char*)a.v_pages + (size_t)g * tile_bytes;
-            const size_t page_stride = (size_t)a.H_kv * tile_bytes;
             const int tok0 = p_begin * kPage;
-            PageRegs<D, FP8> ra, rb;
-            {
-                const int pg = __builtin_amdgcn_readlane(my_pg, 0);
-                load_page<D, FP8>(ra, kpool + pg * page_stride, vpool + pg * page_stride, qg, n);
-            }
-            for (int i = 0; i < np; i += 2) {
-                if (i + 1 < np) {
-                    const int pg = __builtin_amdgcn_readlane(my_pg, i + 1);
-                    load_page<D, FP8>(rb, kpool + pg * page_stride, vpool + pg * page_stride, qg, n);
-                }
-                attend_page<D, FP8>(st, ra, bq, sl, min(kPage, L - tok0 - i * kPage), qg);
-                if (i + 1 < np) {
-                    if (i + 2 < np) {
-                        const int pg = __builtin_amdgcn_readlane(my_pg, i + 2);
-                        load_page<D, FP8>(ra, kpool + pg * page_stride, vpool + pg * page_stride, qg, n);
-                    }
-                    attend_page<D, FP8>(st, rb, bq, sl, min(kPage, L - tok0 - (i + 1) * kPage), qg);
-                }
+            const int npairs = (np + 1) >> 1;
+            // Every iteration issues the same 24 loads (two pages of K and V)
+            // so that the wait before each pair covers only that pair's loads;
+            // indices are clamped, so the odd tail page and the prefetch past
+            // the last pair re-read an in-bounds page of this split (cache
+            // hits) whose slots are masked or never used.
+            PageRegs<D, FP8> r0a, r0b, r1a, r1b;
+            auto load_pair = [&](PageRegs<D, FP8>& ra, PageRegs<D, FP8>& rb, int pair) {
+                const int pa = __builtin_amdgcn_readlane(my_pg, min(2 * pair, np - 1));
+                const int pb = __builtin_amdgcn_readlane(my_pg, min(2 * pair + 1, np - 1));
+                load_page<D, FP8>(ra, kpool + pa * page_stride, vpool + pa * page_stride, qg, n);
+                load_page<D, FP8>(rb, kpool + pb * page_stride, vpool + pb * page_stride, qg, n);
+            };
+            auto live = [&](int page) { return page < np ? min(kPage, L - tok0 - page * kPage) : 0; };
+            load_pair(r0a, r0b, 0);
+            for (int pr = 0;;) {
+                load_pair(r1a, r1b, pr + 1);
+                attend_pair<D, FP8>(st, r0a, r0b, bq, sl, live(2 * pr), live(2 * pr + 1), qg);
+                if (++pr >= npairs) break;
+                load_pair(r0a, r0b, pr + 1);
+                attend_pair<D, FP8>(st, r1a, r1b, bq, sl, live(2 * pr), live(2 * pr + 1), qg);
+                if (++pr >= npairs) break;
             }
         }
 
         float l_tot = st.l + __shfl_xor(st.l, 16);
         l_tot += __shfl_xor(l_tot, 32);
         const float vs = FP8 ? a.v_scale[(int64_t)b * a.H_kv + g] : 1.f;
-        if (!hv) continue;
-        if (nsplit == 1) {
-            const float f = bad ? NAN : vs / l_tot;
-            uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
+        if (hv) {
+            if (nsplit == 1) {
+                const float f = bad ? NAN : vs / l_tot;
+                uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                u32x2 pk;
-                pk.x = (uint32_t)f32_to_bf16_rne(st.o[t][0] * f) | ((uint32_t)f32_to_bf16_rne(st.o[t][1] * f) << 16);
-                pk.y = (uint32_t)f32_to_bf16_rne(st.o[t][2] * f) | ((uint32_t)f32_to_bf16_rne(st.o[t][3] * f) << 16);
-                *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
+                for (int t = 0; t < NT; ++t) {
+                    u32x2 pk;
+                    pk.x = (uint32_t)f32_to_bf16_rne(st.o[t][0] * f) | ((uint32_t)f32_to_bf16_rne(st.o[t][1] * f) << 16);
+                    pk.y = (uint32_t)f32_to_bf16_rne(st.o[t][2] * f) | ((uint32_t)f32_to_bf16_rne(st.o[t][3] * f) << 16);
+                    *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
+                }
+            } else {
+                const int64_t pidx = (int64_t)job * a.H_q + h;
+                float* po = a.part_o + pidx * D;
+                const float f = bad ? NAN : vs;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) *(f32x4*)(po + 16 * t + 4 * qg) = st.o[t] * f;
+                if (qg == 0) a.part_ml[pidx] = make_float2(bad ? NAN : st.m, l_tot);
             }
-        } else {
-            const int64_t pidx = (int64_t)job * a.H_q + h;
-            float* po = a.part_o + pidx * D;
-            const float f = bad ? NAN : vs;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) *(f32x4*)(po + 16 * t + 4 * qg) = st.o[t] * f;
-            if (qg == 0) a.part_ml[pidx] = make_float2(bad ? NAN : st.m, l_tot);
         }
     }
 }

@@ -106,6 +106,8 @@ ATTN_CASES = [
     ("fp8 without scales", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 8, 16, 16]),
                                                   v=t(B_.FP8_E4M3FN, [100, 8, 128, 16])), ERR_INVALID, "dequant_scale"),
     ("bf16 with scales", lambda B_, g: g.update(k=t(B_.BF16, [100, 8, 16, 16, 8], scale=FAKE)), ERR_INVALID, "dequant_scale"),
+    ("empty pool", lambda B_, g: g.update(k=t(B_.BF16, [0, 8, 16, 16, 8]), v=t(B_.BF16, [0, 8, 128, 16])),
+     ERR_INVALID, "no pages"),
     ("fp8 wrong chunk", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 16, 16, 8], scale=FAKE),
                                                v=t(B_.FP8_E4M3FN, [100, 8, 128, 16], scale=FAKE)), ERR_INVALID, "chunk"),
 ]
