@@ -40,7 +40,7 @@ def kernel_sha():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measure(name, steps, warmup, impl, split_pages, seed=0):
+def measure(name, steps, warmup, impl, max_waves, seed=0):
     import torch
 
     import paper_2510_15330_amd as bl
@@ -55,7 +55,7 @@ def measure(name, steps, warmup, impl, split_pages, seed=0):
         bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
         bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
                             stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, impl=impl,
-                            split_pages=split_pages, events=events)
+                            max_waves=max_waves, events=events)
 
     for i in range(warmup):
         step(i)
@@ -189,7 +189,7 @@ def main():
     ap.add_argument("--workload", default="summarization",
                     choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8"])
     ap.add_argument("--impl", default="auto", choices=["auto", "mfma", "valu"])
-    ap.add_argument("--split-pages", type=int, default=0)
+    ap.add_argument("--max-waves", type=int, default=0, help="cap on waves sharing the work (0 = all resident)")
     ap.add_argument("--no-capped", action="store_true", help="skip the capped companion run")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -212,7 +212,7 @@ def main():
     steps = args.steps if args.steps is not None else wl.CONFIGS[args.workload]["steps"]
 
     log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
-    r = measure(args.workload, steps, args.warmup, impl, args.split_pages)
+    r = measure(args.workload, steps, args.warmup, impl, args.max_waves)
     w = r["w"]
     log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['steps_per_s']:.1f} steps/s, step traffic {r['gbs']:.1f} GB/s, "
         f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_gbs']:.1f} GB/s")
@@ -234,7 +234,7 @@ def main():
             "workload": args.workload,
             "batch": w.B, "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
             "kv_dtype": w.kv, "mean_kv_len": round(float(w.lens_at(0).mean()), 1),
-            "impl": args.impl, "split_pages": args.split_pages or "auto", "seed": 0,
+            "impl": args.impl, "max_waves": args.max_waves or "all resident", "seed": 0,
         },
         "steps_per_s": round(r["steps_per_s"], 2),
         "pct_of_peak": round(100.0 * r["gbs"] / PEAK_HBM_GBS, 2),
@@ -251,13 +251,13 @@ def main():
             "unit": "GB/s",
             "frac": round(r["kernel_gbs"] / PEAK_HBM_GBS, 4),
             "traffic": traffic_for(args.workload, args.impl),
-            "kernel": "attn_mfma_kernel (split-K partial attention)",
+            "kernel": "attn_mfma_kernel (paged decode attention, partial pieces)",
             "bytes_per_launch": int(r["attn_bytes"].mean()),
         },
     }
 
     if args.workload == "summarization" and not args.no_capped:
-        c = measure("summarization_capped", steps, args.warmup, impl, args.split_pages)
+        c = measure("summarization_capped", steps, args.warmup, impl, args.max_waves)
         lens_u, info_u = wl.sample_lengths("summarization", 0)
         lens_c, info_c = wl.sample_lengths("summarization_capped", 0)
         p, gu, gc = info_u["prompt"], info_u["generated"], info_c["generated_capped"]

@@ -115,9 +115,11 @@ int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_n
  *   scale        finite fp32 softmax scale (usually 1/sqrt(D)).
  *   out          bf16 [B, H_q, D], innermost contiguous (written; rounded to
  *                nearest even).  A request of length 0 gets zeros.
- * Long requests are split into chunks of whole pages whose partial softmax
- * statistics are merged in a second pass; the work list is built on the
- * device, so the call never waits for the GPU.  Scratch memory is a
+ * The (request, KV head, page) units of the batch are dealt to the GPU's
+ * resident wavefronts in equal contiguous shares; a request cut by a share
+ * boundary has its partial softmax statistics merged in a second pass.  The
+ * shares are planned on the device, so the call never waits for the GPU.
+ * Limits: B <= 8192 and B * H_kv * maxP < 2^31.  Scratch memory is a
  * per-device library workspace grown on demand (hipMalloc) and released by
  * bellman_shutdown(); calls on different streams of one device must not
  * overlap in time.
@@ -136,7 +138,9 @@ typedef enum bellman_attn_impl {
 } bellman_attn_impl_t;
 
 typedef struct bellman_attn_opts {
-    int32_t split_pages;  /* pages per split-K chunk, 1..64; 0 = library default */
+    int32_t max_waves;    /* cap on the waves that share the work; 0 = every wave the
+                             GPU can keep resident.  Fewer waves split fewer
+                             requests (results agree within rounding). */
     int32_t impl;         /* bellman_attn_impl_t */
     void *event_begin;    /* optional hipEvent_t recorded on the stream right before
                              the main attention kernel (profiling); NULL = none */

@@ -33,7 +33,7 @@ class Tensor(ctypes.Structure):
 
 
 class AttnOpts(ctypes.Structure):
-    _fields_ = [("split_pages", ctypes.c_int32), ("impl", ctypes.c_int32),
+    _fields_ = [("max_waves", ctypes.c_int32), ("impl", ctypes.c_int32),
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
@@ -159,7 +159,7 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None
 
 
 def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
-                     k_scale=None, v_scale=None, split_pages=0, impl=IMPL_AUTO, events=None):
+                     k_scale=None, v_scale=None, max_waves=0, impl=IMPL_AUTO, events=None):
     """bellman_decode_attention(_opts): one decode step over the paged cache.
 
     ``events`` is an optional pair of recorded-once torch.cuda.Event objects
@@ -168,7 +168,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
     lib = library()
     args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
             desc(seq_lens), ctypes.c_float(scale), desc(out))
-    if split_pages == 0 and impl == IMPL_AUTO and events is None:
+    if max_waves == 0 and impl == IMPL_AUTO and events is None:
         _check(lib.bellman_decode_attention(*args, _stream(stream)))
     else:
         ev0 = ev1 = None
@@ -176,7 +176,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
             ev0, ev1 = events[0].cuda_event, events[1].cuda_event
             if not ev0 or not ev1:
                 raise ValueError("record each event once before passing it")
-        opts = AttnOpts(int(split_pages), int(impl), ev0, ev1)
+        opts = AttnOpts(int(max_waves), int(impl), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 

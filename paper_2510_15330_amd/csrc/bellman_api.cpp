@@ -30,6 +30,7 @@ int fail(int code, const char* fmt, ...) {
 // ------------------------------------------------------------- workspace ---
 
 constexpr int kMaxDevices = 64;
+constexpr int kMaxAttnBatch = 8192;  // request starts the planner keeps in LDS
 
 struct Workspace {
     char* base = nullptr;
@@ -228,16 +229,6 @@ int launch_status(const char* what) {
     return BELLMAN_OK;
 }
 
-int default_split_pages(int64_t B, int H_kv, int64_t max_pages, int64_t resident_waves) {
-    // Largest split (fewest items, least per-item and merge overhead) that
-    // still gives every resident wave at least two items when each request
-    // filled its block-table row; the row width bounds the real length.
-    const double pages = (double)B * H_kv * (double)max_pages;
-    int sp = 64;
-    while (sp > 8 && pages / sp < 2.0 * (double)resident_waves) sp /= 2;
-    return sp;
-}
-
 }  // namespace
 
 // ================================================================== ABI ====
@@ -356,13 +347,15 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
     const int64_t G = H_q / ps.H_kv;
     if (G > 16) return fail(BELLMAN_ERR_UNSUPPORTED, "GQA group %lld > 16", (long long)G);
-    if (B > (1 << 24)) return fail(BELLMAN_ERR_UNSUPPORTED, "batch too large");
-    int split_pages = 0, impl = BELLMAN_IMPL_AUTO;
+    if (B > kMaxAttnBatch) return fail(BELLMAN_ERR_UNSUPPORTED, "batch %lld > %d", (long long)B, kMaxAttnBatch);
+    const int64_t max_pages = block_table->shape[1];
+    if ((double)B * ps.H_kv * (double)max_pages >= 2147483647.0)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "batch x KV heads x block-table width must stay below 2^31 pages");
+    int max_waves = 0, impl = BELLMAN_IMPL_AUTO;
     if (opts) {
-        split_pages = opts->split_pages;
+        max_waves = opts->max_waves;
         impl = opts->impl;
-        if (split_pages < 0 || split_pages > 64)
-            return fail(BELLMAN_ERR_UNSUPPORTED, "split_pages %d outside [1, 64] (0 = default)", split_pages);
+        if (max_waves < 0) return fail(BELLMAN_ERR_INVALID_ARG, "max_waves %d < 0", max_waves);
         if (impl != BELLMAN_IMPL_AUTO && impl != BELLMAN_IMPL_MFMA && impl != BELLMAN_IMPL_VALU)
             return fail(BELLMAN_ERR_INVALID_ARG, "unknown impl %d", impl);
     }
@@ -378,25 +371,20 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
         g_cu_count[dev] = cu;
     }
-    const int64_t max_pages = block_table->shape[1];
     int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][impl];
     if (bpc == 0) bpc = attention_blocks_per_cu(impl, ps.fp8, ps.D);
-    const int64_t resident_blocks = (int64_t)g_cu_count[dev] * bpc;
-    if (split_pages == 0) {
-        const char* env = getenv("BELLMAN_SPLIT_PAGES");
-        split_pages = env ? atoi(env) : 0;
-        if (split_pages < 1 || split_pages > 64)
-            split_pages = default_split_pages(B, ps.H_kv, max_pages, resident_blocks * (kAttnBlock / kWaveSize));
-    }
-    const int64_t max_splits = (max_pages + split_pages - 1) / split_pages;
-    const int64_t max_jobs = B * max_splits;
-    if (max_jobs * ps.H_kv > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "too many work items");
+    // Every resident wave takes an equal share of the flattened page stream.
+    int64_t waves = (int64_t)g_cu_count[dev] * bpc * (kAttnBlock / kWaveSize);
+    if (max_waves > 0 && waves > max_waves) waves = max_waves;
+    const int64_t grid = (waves + (kAttnBlock / kWaveSize) - 1) / (kAttnBlock / kWaveSize);
 
-    const size_t off_start = sizeof(WorkspaceHeader);
-    const size_t off_jobs = off_start + align256(sizeof(int32_t) * (size_t)(B + 1));
-    const size_t off_ml = off_jobs + align256(sizeof(int4) * (size_t)max_jobs);
-    const size_t off_o = off_ml + align256(sizeof(float2) * (size_t)(max_jobs * H_q));
-    const size_t total = off_o + align256(sizeof(float) * (size_t)(max_jobs * H_q * ps.D));
+    const int64_t segs = B * ps.H_kv;
+    const size_t off_binfo = sizeof(WorkspaceHeader);
+    const size_t off_wstart = off_binfo + align256(sizeof(int4) * (size_t)B);
+    const size_t off_ml = off_wstart + align256(sizeof(int4) * (size_t)waves);
+    const size_t slots = (size_t)(segs + waves) * (size_t)G;
+    const size_t off_o = off_ml + align256(sizeof(float2) * slots);
+    const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
     char* base;
     if ((rc = ensure_workspace(dev, total, &base))) return rc;
 
@@ -422,17 +410,12 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.G = (int)G;
     a.D = ps.D;
     a.max_pages = (int)max_pages;
-    a.split_pages = split_pages;
+    a.waves = (int)waves;
     a.hdr = (WorkspaceHeader*)base;
-    a.job_start = (int32_t*)(base + off_start);
-    a.jobs = (int4*)(base + off_jobs);
+    a.b_info = (int4*)(base + off_binfo);
+    a.wave_start = (int4*)(base + off_wstart);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
-
-    int64_t grid = resident_blocks;
-    const int64_t waves_needed = (max_jobs * ps.H_kv + 3) / 4;
-    if (grid > waves_needed) grid = waves_needed;
-    if (grid < 1) grid = 1;
 
     hipStream_t s = (hipStream_t)stream;
     hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;

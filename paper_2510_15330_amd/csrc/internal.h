@@ -17,10 +17,9 @@ constexpr int kErrPage = 4;
 
 // Header of the per-device workspace; the variable-size regions follow it.
 struct WorkspaceHeader {
-    int32_t err_flags;   // sticky error bits, cleared by the host
-    int32_t counter;     // work-stealing cursor of the attention kernel
-    int32_t njobs;       // number of (request, split) jobs of the current call
-    int32_t pad[61];
+    int32_t err_flags;    // sticky error bits, cleared by the host
+    int32_t total_pages;  // flattened (request, KV head, page) units of the current call
+    int32_t pad[62];
 };
 static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte aligned");
 
@@ -53,13 +52,14 @@ struct AttnArgs {
     int64_t o_sb, o_sh;
     int64_t num_pages;
     float scale_log2;    // softmax scale * log2(e)
-    int B, H_q, H_kv, G, D, max_pages, split_pages;
+    int B, H_q, H_kv, G, D, max_pages;
+    int waves;           // waves sharing the flattened page stream (the grid's waves)
     // workspace
     WorkspaceHeader* hdr;
-    int32_t* job_start;  // [B + 1]
-    int4* jobs;          // [max_jobs] (request, split, clamped length, 0)
-    float2* part_ml;     // [max_jobs * H_q] (running max in log2 units, sum)
-    float* part_o;       // [max_jobs * H_q * D]
+    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, 0)
+    int4* wave_start;    // [waves]: (request, KV head, page) of the wave's first unit
+    float2* part_ml;     // [(B*H_kv + waves) * G]: (running max in log2 units, sum)
+    float* part_o;       // [(B*H_kv + waves) * G * D]
 };
 
 // Launchers (kernels.hip).  They only enqueue; errors come back through

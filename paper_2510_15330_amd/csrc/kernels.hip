@@ -82,49 +82,75 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 }
 
 // -------------------------------------------------------------- planner ---
-// One workgroup: split each request into chunks of split_pages pages, lay
-// the (request, split, clamped length) jobs out request-major with an
-// exclusive scan, and reset the work-stealing cursor.
-__global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
-    __shared__ int scan[1024];
+// One workgroup.  The work of a call is the flattened sequence of units
+// (request b, KV head g, page p), request-major, then head, then page.  The
+// planner clamps each length to the block-table width, scans the pages per
+// request into each request's first unit, and gives every one of the W waves
+// the contiguous range [floor(w*P/W), floor((w+1)*P/W)) of the P units,
+// recording the (b, g, p) where that range starts.  Requests are split only
+// where a wave boundary falls inside them.
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanMaxBatch = 8192;   // request starts kept in LDS for the search
+
+__global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
+    __shared__ int first[kPlanMaxBatch + 1];
+    __shared__ int scan[kPlanThreads];
     __shared__ int carry;
     const int tid = threadIdx.x;
     const int maxL = a.max_pages * kPage;
     if (tid == 0) carry = 0;
     __syncthreads();
-    for (int base = 0; base < a.B; base += 1024) {
+    for (int base = 0; base < a.B; base += kPlanThreads) {
         const int b = base + tid;
-        int ns = 0, L = 0;
+        int units = 0, L = 0, np = 0;
         if (b < a.B) {
             L = a.seq_lens[b];
             if (L < 0 || L > maxL) {
                 atomicOr(&a.hdr->err_flags, kErrLength);
                 L = L < 0 ? 0 : maxL;
             }
-            const int np = (L + kPage - 1) / kPage;
-            ns = (np + a.split_pages - 1) / a.split_pages;
+            np = (L + kPage - 1) / kPage;
+            units = np * a.H_kv;
         }
-        scan[tid] = ns;
+        scan[tid] = units;
         __syncthreads();
-        for (int off = 1; off < 1024; off <<= 1) {
+        for (int off = 1; off < kPlanThreads; off <<= 1) {
             const int v = tid >= off ? scan[tid - off] : 0;
             __syncthreads();
             scan[tid] += v;
             __syncthreads();
         }
-        const int excl = carry + scan[tid] - ns;
+        const int excl = carry + scan[tid] - units;
         if (b < a.B) {
-            a.job_start[b] = excl;
-            for (int s = 0; s < ns; ++s) a.jobs[excl + s] = make_int4(b, s, L, 0);
+            first[b] = excl;
+            a.b_info[b] = make_int4(excl, np, L, 0);
         }
         __syncthreads();
-        if (tid == 1023) carry += scan[1023];
+        if (tid == kPlanThreads - 1) carry += scan[kPlanThreads - 1];
         __syncthreads();
     }
+    const int P = carry;
     if (tid == 0) {
-        a.job_start[a.B] = carry;
-        a.hdr->njobs = carry;
-        a.hdr->counter = 0;
+        first[a.B] = P;
+        a.hdr->total_pages = P;
+    }
+    __syncthreads();
+    for (int w = tid; w < a.waves; w += kPlanThreads) {
+        const int x = (int)((int64_t)w * P / a.waves);
+        const int x1 = (int)((int64_t)(w + 1) * P / a.waves);
+        int4 ws = make_int4(-1, 0, 0, 0);
+        if (x < x1) {
+            // last request whose first unit is <= x (it has pages, since x < P)
+            int lo = 0, hi = a.B - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (first[mid] <= x) lo = mid; else hi = mid - 1;
+            }
+            const int np = (first[lo + 1] - first[lo]) / a.H_kv;
+            const int off = x - first[lo];
+            ws = make_int4(lo, off / np, off % np, 0);
+        }
+        a.wave_start[w] = ws;
     }
 }
 
@@ -145,13 +171,15 @@ __global__ void __launch_bounds__(1024) plan_kernel(AttnArgs a) {
 // request's length are excluded: their scores become -inf and their V
 // elements are replaced by zeros.  O is rescaled only when a running max
 // grows (exact: otherwise the factor is 1).
+// One page of one KV head as this lane holds it.
 template <int D, bool FP8>
-struct PageRegs {
-    static constexpr int NT = D / 16;
-    static constexpr int KS = D / 32;
-    static constexpr int KC = FP8 ? D / 64 : KS;  // 16-byte K loads per lane
+struct PageK {
+    static constexpr int KC = FP8 ? D / 64 : D / 32;  // 16-byte K loads per lane
     u32x4 k[KC];
-    typename std::conditional<FP8, uint32_t, u32x2>::type v[NT];
+};
+template <int D, bool FP8>
+struct PageV {
+    typename std::conditional<FP8, uint32_t, u32x2>::type v[D / 16];
 };
 
 // K/V pages are read exactly once per step: non-temporal loads keep them from
@@ -163,33 +191,35 @@ __device__ __forceinline__ T ld_stream(const char* p) {
 }
 
 template <int D, bool FP8>
-__device__ __forceinline__ void load_page(PageRegs<D, FP8>& r, const char* kbase, const char* vbase,
-                                          int qg, int n) {
-    constexpr int NT = D / 16;
+__device__ __forceinline__ void load_k(PageK<D, FP8>& r, const char* kbase, int qg, int n) {
     if constexpr (!FP8) {
-        // K chunk c = 4j + qg (8 dims), slot n: 16 bytes; one load instruction
-        // covers 1 KiB contiguous.
+        // chunk c = 4j + qg (8 dims), slot n: 16 bytes; one instruction covers 1 KiB
 #pragma unroll
-        for (int j = 0; j < PageRegs<D, FP8>::KC; ++j)
+        for (int j = 0; j < PageK<D, FP8>::KC; ++j)
             r.k[j] = ld_stream<u32x4>(kbase + ((size_t)((4 * j + qg) * kPage + n)) * 16);
-        // V dims 16t + n, slots 4qg..4qg+3: 8 bytes; 512 bytes contiguous per instruction.
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-            r.v[t] = ld_stream<u32x2>(vbase + ((size_t)((16 * t + n) * kPage + 4 * qg)) * 2);
     } else {
-        // K chunk c = qg + 4i (16 dims), slot n: 16 bytes.
+        // chunk c = qg + 4i (16 dims), slot n: 16 bytes
 #pragma unroll
-        for (int i = 0; i < PageRegs<D, FP8>::KC; ++i)
+        for (int i = 0; i < PageK<D, FP8>::KC; ++i)
             r.k[i] = ld_stream<u32x4>(kbase + ((size_t)((qg + 4 * i) * kPage + n)) * 16);
+    }
+}
+
+template <int D, bool FP8>
+__device__ __forceinline__ void load_v(PageV<D, FP8>& r, const char* vbase, int qg, int n) {
+    // dims 16t + n, slots 4qg..4qg+3; an instruction covers 512 (bf16) or 256 (fp8) bytes
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+    for (int t = 0; t < D / 16; ++t) {
+        if constexpr (!FP8)
+            r.v[t] = ld_stream<u32x2>(vbase + ((size_t)((16 * t + n) * kPage + 4 * qg)) * 2);
+        else
             r.v[t] = ld_stream<uint32_t>(vbase + (size_t)((16 * t + n) * kPage + 4 * qg));
     }
 }
 
 // Scores of one page: lane (qg, n) gets head n at slots 4qg..4qg+3.
 template <int D, bool FP8>
-__device__ __forceinline__ f32x4 page_scores(const PageRegs<D, FP8>& r, const bf16x8 (&bq)[D / 32]) {
+__device__ __forceinline__ f32x4 page_scores(const PageK<D, FP8>& r, const bf16x8 (&bq)[D / 32]) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < D / 32; ++j) {
@@ -213,7 +243,7 @@ __device__ __forceinline__ f32x4 page_scores(const PageRegs<D, FP8>& r, const bf
 // Four bf16 V elements (slots 4qg..4qg+3 of dim 16t + n) as the lane's half
 // of a PV A operand, zeroed at slots >= nv.
 template <int D, bool FP8>
-__device__ __forceinline__ u32x2 v_quad(const PageRegs<D, FP8>& r, int t, int nv, int qg) {
+__device__ __forceinline__ u32x2 v_quad(const PageV<D, FP8>& r, int t, int nv, int qg) {
     u32x2 vv;
     if constexpr (!FP8) {
         vv = r.v[t];
@@ -241,21 +271,17 @@ __device__ __forceinline__ uint32_t pack_hi16(uint32_t lo, uint32_t hi) {
     return __builtin_amdgcn_perm(hi, lo, 0x07060302u);
 }
 
+// Online softmax over one page's scores, then O += V^T P^T for the page.
 template <int D, bool FP8>
-__device__ __forceinline__ void attend_pair(AttnState<D>& st, const PageRegs<D, FP8>& ra, const PageRegs<D, FP8>& rb,
-                                            const bf16x8 (&bq)[D / 32], float sl, int nva, int nvb, int qg) {
+__device__ __forceinline__ void page_pv(AttnState<D>& st, f32x4 sc, const PageV<D, FP8>& pv, float sl, int nv,
+                                        int qg) {
     constexpr int NT = D / 16;
-    const f32x4 sa = page_scores<D, FP8>(ra, bq);
-    f32x4 sb = {0.f, 0.f, 0.f, 0.f};
-    if (nvb > 0) sb = page_scores<D, FP8>(rb, bq);
-
-    float x[8];
+    float x[4];
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        x[i] = (4 * qg + i < nva) ? sa[i] * sl : -INFINITY;
-        x[4 + i] = (4 * qg + i < nvb) ? sb[i] * sl : -INFINITY;
-        mx = fmaxf(mx, fmaxf(x[i], x[4 + i]));
+        x[i] = (4 * qg + i < nv) ? sc[i] * sl : -INFINITY;
+        mx = fmaxf(mx, x[i]);
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -267,31 +293,55 @@ __device__ __forceinline__ void attend_pair(AttnState<D>& st, const PageRegs<D, 
         for (int t = 0; t < NT; ++t) st.o[t] *= alpha;
         st.m = m_new;
     }
-
-    uint32_t ph[4], pl[4];
-    float psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) {
-        const float p0 = fast_exp2(x[i] - st.m);
-        const float p1 = fast_exp2(x[i + 1] - st.m);
-        psum += p0 + p1;
-        const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
-        const float r0 = p0 - __uint_as_float(u0 & 0xffff0000u);
-        const float r1 = p1 - __uint_as_float(u1 & 0xffff0000u);
-        ph[i / 2] = pack_hi16(u0, u1);
-        pl[i / 2] = pack_hi16(__float_as_uint(r0), __float_as_uint(r1));
-    }
-    st.l += psum;
-    const bf16x8 bph = __builtin_bit_cast(bf16x8, u32x4{ph[0], ph[1], ph[2], ph[3]});
-    const bf16x8 bpl = __builtin_bit_cast(bf16x8, u32x4{pl[0], pl[1], pl[2], pl[3]});
-
+    const float p0 = fast_exp2(x[0] - st.m), p1 = fast_exp2(x[1] - st.m);
+    const float p2 = fast_exp2(x[2] - st.m), p3 = fast_exp2(x[3] - st.m);
+    st.l += (p0 + p1) + (p2 + p3);
+    const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
+    const uint32_t u2 = __float_as_uint(p2), u3 = __float_as_uint(p3);
+    const uint32_t r0 = __float_as_uint(p0 - __uint_as_float(u0 & 0xffff0000u));
+    const uint32_t r1 = __float_as_uint(p1 - __uint_as_float(u1 & 0xffff0000u));
+    const uint32_t r2 = __float_as_uint(p2 - __uint_as_float(u2 & 0xffff0000u));
+    const uint32_t r3 = __float_as_uint(p3 - __uint_as_float(u3 & 0xffff0000u));
+    const s16x4 bph = __builtin_bit_cast(s16x4, u32x2{pack_hi16(u0, u1), pack_hi16(u2, u3)});
+    const s16x4 bpl = __builtin_bit_cast(s16x4, u32x2{pack_hi16(r0, r1), pack_hi16(r2, r3)});
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        const u32x2 va = v_quad<D, FP8>(ra, t, nva, qg);
-        const u32x2 vb = v_quad<D, FP8>(rb, t, nvb, qg);
-        const bf16x8 av = __builtin_bit_cast(bf16x8, u32x4{va.x, va.y, vb.x, vb.y});
-        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bph, st.o[t], 0, 0, 0);
-        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bpl, st.o[t], 0, 0, 0);
+        const s16x4 av = __builtin_bit_cast(s16x4, v_quad<D, FP8>(pv, t, nv, qg));
+        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bph, st.o[t], 0, 0, 0);
+        st.o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bpl, st.o[t], 0, 0, 0);
+    }
+}
+
+// A position in a wave's stream: unit x, which is page p of request b, KV
+// head g.  All fields are wave-uniform.
+struct Cursor {
+    int b, g, p;   // request, KV head, page within the request
+    int np, L;     // the request's pages and clamped length
+    int x;         // flattened unit
+    bool live;     // false once past the wave's range
+};
+
+// Step to the next unit.  A cursor that would leave the range keeps its last
+// position (so loads issued for it stay in bounds) and stops being live.
+__device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1) {
+    if (!c.live) return;
+    if (c.x + 1 >= r1) {
+        c.live = false;
+        return;
+    }
+    ++c.x;
+    if (++c.p >= c.np) {
+        c.p = 0;
+        if (++c.g >= a.H_kv) {
+            c.g = 0;
+            // units remain, so a later request with pages exists
+            do {
+                ++c.b;
+                const int4 bi = a.b_info[c.b];
+                c.np = bi.y;
+                c.L = bi.z;
+            } while (c.np == 0 && c.b + 1 < a.B);
+        }
     }
 }
 
@@ -303,91 +353,98 @@ __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu
     const int lane = threadIdx.x & (kWaveSize - 1);
     const int qg = lane >> 4;
     const int n = lane & 15;
-    const int total = a.hdr->njobs * a.H_kv;
+    // wave index, made provably uniform so that all stream bookkeeping is scalar
+    const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6));
+    if (w >= a.waves) return;
+    const int P = a.hdr->total_pages;
+    const int r0 = (int)((int64_t)w * P / a.waves);
+    const int r1 = (int)((int64_t)(w + 1) * P / a.waves);
+    if (r0 >= r1) return;
+
     const size_t tile_bytes = (size_t)D * kPage * EB;
     const size_t page_stride = (size_t)a.H_kv * tile_bytes;
+    const bool hv = n < a.G;
 
-    // Items are dealt round-robin over all resident waves: wave w takes items
-    // w, w + W, w + 2W, ...  Consecutive items are the KV heads of one
-    // (request, split) job, so neighbouring waves get equal-sized items and
-    // every wave's share averages over many jobs.
-    const int waves = gridDim.x * (kAttnBlock / kWaveSize);
-    for (int item = blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6); item < total; item += waves) {
+    // Three cursors walk the wave's stream: C is computed, I has its page
+    // (and query rows) in flight, T has its block-table entry in flight.
+    Cursor C;
+    {
+        const int4 ws = a.wave_start[w];
+        const int4 bi = a.b_info[ws.x];
+        C.b = ws.x;
+        C.g = ws.y;
+        C.p = ws.z;
+        C.np = bi.y;
+        C.L = bi.z;
+        C.x = r0;
+        C.live = true;
+    }
+    Cursor I = C;
+    cursor_next(I, a, r1);
+    Cursor T = I;
+    cursor_next(T, a, r1);
 
-        const int job = item / a.H_kv;
-        const int g = item - job * a.H_kv;
-        const int4 js = a.jobs[job];
-        const int b = js.x, s = js.y, L = js.z;
-        const int np_total = (L + kPage - 1) / kPage;
-        const int nsplit = (np_total + a.split_pages - 1) / a.split_pages;
-        const int p_begin = s * a.split_pages;
-        const int np = min(a.split_pages, np_total - p_begin);
-
-        // this split's block-table entries, one per lane
-        int my_pg = 0;
-        if (lane < np) my_pg = a.block_table[(int64_t)b * a.bt_stride + p_begin + lane];
-        const bool lane_bad = lane < np && (my_pg < 0 || (int64_t)my_pg >= a.num_pages);
-        const bool bad = __any(lane_bad);
-        if (bad && lane == 0) atomicOr(&a.hdr->err_flags, kErrPage);
-
-        // query operand: lane (qg, n) holds head g*G+n (zeros past the group)
-        const int h = g * a.G + n;
-        const bool hv = n < a.G;
-        bf16x8 bq[KS];
-        {
-            const uint16_t* qrow = a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh;
+    // Block-table entry of a unit.  Lane 1 reads the following entry (unused)
+    // so that the address is lane-dependent: this keeps the load a vector
+    // load, ordered with the page loads, instead of a scalar one.
+    auto bt_load = [&](const Cursor& c) -> int {
+        const int idx = min(c.p + (lane & 1), c.np - 1);
+        return a.block_table[(int64_t)c.b * a.bt_stride + idx];
+    };
+    // Query rows of a unit's group as the QK B operand: lane (qg, n) holds
+    // head g*G + n.  Lanes n >= G hold a copy of the group's last head; their
+    // columns of S and O are computed and discarded, which keeps this load
+    // free of lane masks.
+    auto q_load = [&](const Cursor& c, bf16x8 (&bq)[KS]) {
+        const uint16_t* qrow = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + min(n, a.G - 1)) * a.q_sh;
 #pragma unroll
-            for (int j = 0; j < KS; ++j) {
-                const int dim0 = FP8 ? 16 * (qg + 4 * (j >> 1)) + 8 * (j & 1) : 8 * (4 * j + qg);
-                u32x4 w = {0u, 0u, 0u, 0u};
-                if (hv) w = *(const u32x4*)(qrow + dim0);
-                bq[j] = __builtin_bit_cast(bf16x8, w);
-            }
+        for (int j = 0; j < KS; ++j) {
+            const int dim0 = FP8 ? 16 * (qg + 4 * (j >> 1)) + 8 * (j & 1) : 8 * (4 * j + qg);
+            bq[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qrow + dim0));
         }
-        const float sl = FP8 ? a.scale_log2 * a.k_scale[(int64_t)b * a.H_kv + g] : a.scale_log2;
+    };
+    // fp8 only: lanes 0..31 read the K scale, lanes 32..63 the V scale.
+    auto scale_load = [&](const Cursor& c) -> float {
+        const float* src = lane < 32 ? a.k_scale : a.v_scale;
+        return src[(int64_t)c.b * a.H_kv + c.g];
+    };
+    int bad_pages = 0;  // wave-uniform: set when a block-table entry is outside the pool
+    // K and V of a unit.  An entry outside the pool is never dereferenced:
+    // page 0 is read instead and the piece's output is poisoned.
+    auto kv_load = [&](const Cursor& c, int btv, PageK<D, FP8>& rk, PageV<D, FP8>& rv, bool& bad) {
+        int pg = __builtin_amdgcn_readlane(btv, 0);
+        bad = (unsigned)pg >= (unsigned)a.num_pages;
+        if (bad) {
+            pg = 0;
+            bad_pages = 1;
+        }
+        const size_t off = (size_t)pg * page_stride + (size_t)c.g * tile_bytes;
+        load_k<D, FP8>(rk, (const char*)a.k_pages + off, qg, n);
+        load_v<D, FP8>(rv, (const char*)a.v_pages + off, qg, n);
+    };
 
-        AttnState<D> st;
+    AttnState<D> st;
+    auto reset = [&]() {
 #pragma unroll
         for (int t = 0; t < NT; ++t) st.o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
         st.m = -INFINITY;
         st.l = 0.f;
+    };
+    reset();
+    bool seg_bad = false;
 
-        if (!bad) {
-            const char* kpool = (const char*)a.k_pages + (size_t)g * tile_bytes;
-            const char* vpool = (const char*)a.v_pages + (size_t)g * tile_bytes;
-            const int tok0 = p_begin * kPage;
-            const int npairs = (np + 1) >> 1;
-            // Every iteration issues the same 24 loads (two pages of K and V)
-            // so that the wait before each pair covers only that pair's loads;
-            // indices are clamped, so the odd tail page and the prefetch past
-            // the last pair re-read an in-bounds page of this split (cache
-            // hits) whose slots are masked or never used.
-            PageRegs<D, FP8> r0a, r0b, r1a, r1b;
-            auto load_pair = [&](PageRegs<D, FP8>& ra, PageRegs<D, FP8>& rb, int pair) {
-                const int pa = __builtin_amdgcn_readlane(my_pg, min(2 * pair, np - 1));
-                const int pb = __builtin_amdgcn_readlane(my_pg, min(2 * pair + 1, np - 1));
-                load_page<D, FP8>(ra, kpool + pa * page_stride, vpool + pa * page_stride, qg, n);
-                load_page<D, FP8>(rb, kpool + pb * page_stride, vpool + pb * page_stride, qg, n);
-            };
-            auto live = [&](int page) { return page < np ? min(kPage, L - tok0 - page * kPage) : 0; };
-            load_pair(r0a, r0b, 0);
-            for (int pr = 0;;) {
-                load_pair(r1a, r1b, pr + 1);
-                attend_pair<D, FP8>(st, r0a, r0b, bq, sl, live(2 * pr), live(2 * pr + 1), qg);
-                if (++pr >= npairs) break;
-                load_pair(r0a, r0b, pr + 1);
-                attend_pair<D, FP8>(st, r1a, r1b, bq, sl, live(2 * pr), live(2 * pr + 1), qg);
-                if (++pr >= npairs) break;
-            }
-        }
-
+    // Write the finished piece of C's (request, head): the whole output if the
+    // request's head lies entirely in this wave's range, else a partial.
+    auto finish = [&](const Cursor& c, float vs) {
         float l_tot = st.l + __shfl_xor(st.l, 16);
         l_tot += __shfl_xor(l_tot, 32);
-        const float vs = FP8 ? a.v_scale[(int64_t)b * a.H_kv + g] : 1.f;
+        const int seg_x0 = c.x - c.p;
+        const bool whole = seg_x0 >= r0 && seg_x0 + c.np <= r1;
         if (hv) {
-            if (nsplit == 1) {
-                const float f = bad ? NAN : vs / l_tot;
-                uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
+            const int h = c.g * a.G + n;
+            if (whole) {
+                const float f = seg_bad ? NAN : vs / l_tot;
+                uint16_t* orow = a.out + (int64_t)c.b * a.o_sb + (int64_t)h * a.o_sh;
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
                     u32x2 pk;
@@ -396,53 +453,120 @@ __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu
                     *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
                 }
             } else {
-                const int64_t pidx = (int64_t)job * a.H_q + h;
-                float* po = a.part_o + pidx * D;
-                const float f = bad ? NAN : vs;
+                const int64_t slot = ((int64_t)c.b * a.H_kv + c.g + w) * a.G + n;
+                float* po = a.part_o + slot * D;
+                const float f = seg_bad ? NAN : vs;
 #pragma unroll
                 for (int t = 0; t < NT; ++t) *(f32x4*)(po + 16 * t + 4 * qg) = st.o[t] * f;
-                if (qg == 0) a.part_ml[pidx] = make_float2(bad ? NAN : st.m, l_tot);
+                if (qg == 0) a.part_ml[slot] = make_float2(seg_bad ? NAN : st.m, l_tot);
             }
         }
+        reset();
+        seg_bad = false;
+    };
+
+    // Operands: pages of C (X) and I (Y), query rows of C and of I.  Each step
+    // issues T's block-table entry, I's query rows and I's page, then
+    // computes C.  Every step issues the same loads, in the same order, so
+    // each wait covers exactly the data it needs and one page stays in flight.
+    PageK<D, FP8> kA, kB;
+    PageV<D, FP8> vA, vB;
+    bf16x8 q[KS], qn[KS];
+    float sc = 0.f, scn = 0.f;
+    bool badA = false, badB = false;
+    {
+        const int btC = bt_load(C);
+        q_load(C, q);
+        if constexpr (FP8) sc = scale_load(C);
+        kv_load(C, btC, kA, vA, badA);
     }
+    int btI = bt_load(I);
+
+    auto step = [&](PageK<D, FP8>& kx, PageV<D, FP8>& vx, bool badx, PageK<D, FP8>& ky, PageV<D, FP8>& vy,
+                    bool& bady) -> bool {
+        const int btT = bt_load(T);
+        q_load(I, qn);
+        if constexpr (FP8) scn = scale_load(I);
+        kv_load(I, btI, ky, vy, bady);
+        btI = btT;
+
+        float sl = a.scale_log2, vs = 1.f;
+        if constexpr (FP8) {
+            sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), 0));
+            vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), 32));
+        }
+        seg_bad = seg_bad || badx;
+        const f32x4 s4 = page_scores<D, FP8>(kx, q);
+        page_pv<D, FP8>(st, s4, vx, sl, min(kPage, C.L - C.p * kPage), qg);
+        if (C.p + 1 >= C.np || C.x + 1 >= r1) finish(C, vs);
+#pragma unroll
+        for (int j = 0; j < KS; ++j) q[j] = qn[j];
+        sc = scn;
+        C = I;
+        I = T;
+        cursor_next(T, a, r1);
+        return C.live;
+    };
+
+    for (;;) {
+        if (!step(kA, vA, badA, kB, vB, badB)) break;
+        if (!step(kB, vB, badB, kA, vA, badA)) break;
+    }
+    if (bad_pages) atomicOr(&a.hdr->err_flags, kErrPage);
 }
 
 // ----------------------------------------------------------------- merge ---
-// One wave per (request, query head): combine the splits' partial results
-//   M = max_s m_s,  l = sum_s 2^(m_s - M) l_s,  out = sum_s 2^(m_s - M) o_s / l
-// in split order (deterministic).  Requests with a single split were written
-// by the partial kernel; requests of length 0 get zeros.
+// One wave per (request, query head) whose KV head was cut by a wave boundary:
+// combine the pieces of the waves that covered it, in wave order
+// (deterministic):
+//   M = max_i m_i,  l = sum_i 2^(m_i - M) l_i,  out = sum_i 2^(m_i - M) o_i / l
+// A request's head that one wave covered whole was written by that wave;
+// requests of length 0 get zeros.
+__device__ __forceinline__ int wave_of(int x, int P, int W) {
+    // the wave w with floor(w P / W) <= x < floor((w + 1) P / W)
+    return (int)(((int64_t)(x + 1) * W - 1) / P);
+}
+
 template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int wid = blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6);
     const int lane = threadIdx.x & (kWaveSize - 1);
     if (wid >= a.B * a.H_q) return;
     const int b = wid / a.H_q, h = wid - b * a.H_q;
-    const int maxL = a.max_pages * kPage;
-    const int L = min(max(a.seq_lens[b], 0), maxL);
-    const int np_total = (L + kPage - 1) / kPage;
-    const int nsplit = (np_total + a.split_pages - 1) / a.split_pages;
+    const int g = h / a.G, n = h - g * a.G;
+    const int4 bi = a.b_info[b];
+    const int np = bi.y;
     uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
-    if (nsplit == 1) return;
-    if (nsplit == 0) {
+    if (np == 0) {
         for (int d = lane; d < D; d += kWaveSize) orow[d] = 0;
         return;
     }
-    const int j0 = a.job_start[b];
+    const int P = a.hdr->total_pages;
+    const int W = a.waves;
+    const int x0 = bi.x + g * np;
+    const int wf = wave_of(x0, P, W);
+    const int wl = wave_of(x0 + np - 1, P, W);
+    if (wf == wl) return;
+    const int64_t seg = (int64_t)b * a.H_kv + g;
+    auto has_units = [&](int v) {
+        return (int64_t)v * P / W < (int64_t)(v + 1) * P / W;
+    };
     float M = -INFINITY;
-    for (int s = 0; s < nsplit; ++s) M = fmaxf(M, a.part_ml[(int64_t)(j0 + s) * a.H_q + h].x);
+    for (int v = wf; v <= wl; ++v)
+        if (has_units(v)) M = fmaxf(M, a.part_ml[(seg + v) * a.G + n].x);
     float l = 0.f;
     float acc[D / kWaveSize];
 #pragma unroll
     for (int k = 0; k < D / kWaveSize; ++k) acc[k] = 0.f;
-    for (int s = 0; s < nsplit; ++s) {
-        const int64_t pidx = (int64_t)(j0 + s) * a.H_q + h;
-        const float2 ml = a.part_ml[pidx];
-        const float w = fast_exp2(ml.x - M);
-        l += w * ml.y;
-        const float* po = a.part_o + pidx * D;
+    for (int v = wf; v <= wl; ++v) {
+        if (!has_units(v)) continue;
+        const int64_t slot = (seg + v) * a.G + n;
+        const float2 ml = a.part_ml[slot];
+        const float wt = fast_exp2(ml.x - M);
+        l += wt * ml.y;
+        const float* po = a.part_o + slot * D;
 #pragma unroll
-        for (int k = 0; k < D / kWaveSize; ++k) acc[k] += w * po[lane + kWaveSize * k];
+        for (int k = 0; k < D / kWaveSize; ++k) acc[k] += wt * po[lane + kWaveSize * k];
     }
     const float inv = 1.f / l;
 #pragma unroll

@@ -97,6 +97,9 @@ ATTN_CASES = [
     ("k/v dtype mismatch", lambda B_, g: g.update(v=t(B_.FP8_E4M3FN, [100, 8, 128, 16])), ERR_INVALID, "differs"),
     ("non-contiguous pool", lambda B_, g: g.update(k=t(B_.BF16, [100, 8, 16, 16, 8], [16384 * 2, 2048, 128, 8, 1])),
      ERR_UNSUPPORTED, "contiguous"),
+    ("batch too large", lambda B_, g: g.update(q=t(B_.BF16, [9000, 32, 128]), out=t(B_.BF16, [9000, 32, 128]),
+                                               bt=t(B_.INT32, [9000, 10]), sl=t(B_.INT32, [9000])),
+     ERR_UNSUPPORTED, "batch 9000"),
     ("block table rows", lambda B_, g: g.update(bt=t(B_.INT32, [3, 10])), ERR_INVALID, "block_table"),
     ("block table dtype", lambda B_, g: g.update(bt=t(B_.FP32, [4, 10])), ERR_INVALID, "block_table: dtype"),
     ("seq_lens size", lambda B_, g: g.update(sl=t(B_.INT32, [5])), ERR_INVALID, "seq_lens"),
@@ -139,13 +142,13 @@ def test_append_rejects(B, name, mut, code, msg):
     assert msg in B.last_error()
 
 
-def test_split_option_range(B):
+def test_option_ranges(B):
     g = good(B)
     lib = B.library()
-    opts = B.AttnOpts(65, 0)
+    opts = B.AttnOpts(-1, 0)
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
-    assert rc == ERR_UNSUPPORTED and "split_pages" in B.last_error()
+    assert rc == ERR_INVALID and "max_waves" in B.last_error()
     opts = B.AttnOpts(0, 7)
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
