@@ -40,7 +40,7 @@ def kernel_sha():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measure(name, steps, warmup, impl, max_waves, seed=0):
+def measure(name, steps, warmup, impl, max_waves, pps=0, depth=0, seed=0):
     import torch
 
     import paper_2510_15330_amd as bl
@@ -55,7 +55,8 @@ def measure(name, steps, warmup, impl, max_waves, seed=0):
         bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
         bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
                             stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, impl=impl,
-                            max_waves=max_waves, events=events)
+                            max_waves=max_waves, events=events, pages_per_step=pps,
+                            pipeline_depth=depth)
 
     for i in range(warmup):
         step(i)
@@ -190,6 +191,8 @@ def main():
                     choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8"])
     ap.add_argument("--impl", default="auto", choices=["auto", "mfma", "valu"])
     ap.add_argument("--max-waves", type=int, default=0, help="cap on waves sharing the work (0 = all resident)")
+    ap.add_argument("--pages-per-step", type=int, default=0, help="1, 2 (or 4 for fp8); 0 = library default")
+    ap.add_argument("--pipeline-depth", type=int, default=0, help="1 or 2; 0 = library default")
     ap.add_argument("--no-capped", action="store_true", help="skip the capped companion run")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -212,7 +215,7 @@ def main():
     steps = args.steps if args.steps is not None else wl.CONFIGS[args.workload]["steps"]
 
     log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
-    r = measure(args.workload, steps, args.warmup, impl, args.max_waves)
+    r = measure(args.workload, steps, args.warmup, impl, args.max_waves, args.pages_per_step, args.pipeline_depth)
     w = r["w"]
     log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['steps_per_s']:.1f} steps/s, step traffic {r['gbs']:.1f} GB/s, "
         f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_gbs']:.1f} GB/s")
@@ -234,7 +237,9 @@ def main():
             "workload": args.workload,
             "batch": w.B, "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
             "kv_dtype": w.kv, "mean_kv_len": round(float(w.lens_at(0).mean()), 1),
-            "impl": args.impl, "max_waves": args.max_waves or "all resident", "seed": 0,
+            "impl": args.impl, "max_waves": args.max_waves or "all resident",
+            "pages_per_step": args.pages_per_step or "default",
+            "pipeline_depth": args.pipeline_depth or "default", "seed": 0,
         },
         "steps_per_s": round(r["steps_per_s"], 2),
         "pct_of_peak": round(100.0 * r["gbs"] / PEAK_HBM_GBS, 2),
@@ -257,7 +262,8 @@ def main():
     }
 
     if args.workload == "summarization" and not args.no_capped:
-        c = measure("summarization_capped", steps, args.warmup, impl, args.max_waves)
+        c = measure("summarization_capped", steps, args.warmup, impl, args.max_waves, args.pages_per_step,
+                    args.pipeline_depth)
         lens_u, info_u = wl.sample_lengths("summarization", 0)
         lens_c, info_c = wl.sample_lengths("summarization_capped", 0)
         p, gu, gc = info_u["prompt"], info_u["generated"], info_c["generated_capped"]

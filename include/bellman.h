@@ -142,6 +142,13 @@ typedef struct bellman_attn_opts {
                              GPU can keep resident.  Fewer waves split fewer
                              requests (results agree within rounding). */
     int32_t impl;         /* bellman_attn_impl_t */
+    int32_t pages_per_step; /* 16-token pages per softmax update: 1 or 2 (bf16),
+                               1, 2 or 4 (fp8); 0 = the library's choice
+                               (2 for bf16, 4 for fp8 pools) */
+    int32_t pipeline_depth; /* steps of pages in flight per wavefront while it
+                               computes one: 1 (two wavefronts per SIMD) or 2 (one
+                               per SIMD); 0 = the library's choice (2 for bf16,
+                               1 for fp8 pools) */
     void *event_begin;    /* optional hipEvent_t recorded on the stream right before
                              the main attention kernel (profiling); NULL = none */
     void *event_end;      /* optional hipEvent_t recorded right after it */

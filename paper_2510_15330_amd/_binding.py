@@ -34,6 +34,7 @@ class Tensor(ctypes.Structure):
 
 class AttnOpts(ctypes.Structure):
     _fields_ = [("max_waves", ctypes.c_int32), ("impl", ctypes.c_int32),
+                ("pages_per_step", ctypes.c_int32), ("pipeline_depth", ctypes.c_int32),
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
@@ -159,7 +160,8 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None
 
 
 def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
-                     k_scale=None, v_scale=None, max_waves=0, impl=IMPL_AUTO, events=None):
+                     k_scale=None, v_scale=None, max_waves=0, impl=IMPL_AUTO, events=None,
+                     pages_per_step=0, pipeline_depth=0):
     """bellman_decode_attention(_opts): one decode step over the paged cache.
 
     ``events`` is an optional pair of recorded-once torch.cuda.Event objects
@@ -168,7 +170,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
     lib = library()
     args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
             desc(seq_lens), ctypes.c_float(scale), desc(out))
-    if max_waves == 0 and impl == IMPL_AUTO and events is None:
+    if max_waves == 0 and impl == IMPL_AUTO and events is None and pages_per_step == 0 and pipeline_depth == 0:
         _check(lib.bellman_decode_attention(*args, _stream(stream)))
     else:
         ev0 = ev1 = None
@@ -176,7 +178,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
             ev0, ev1 = events[0].cuda_event, events[1].cuda_event
             if not ev0 or not ev1:
                 raise ValueError("record each event once before passing it")
-        opts = AttnOpts(int(max_waves), int(impl), ev0, ev1)
+        opts = AttnOpts(int(max_waves), int(impl), int(pages_per_step), int(pipeline_depth), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 

@@ -40,7 +40,7 @@ struct Workspace {
 std::mutex g_ws_mutex;
 Workspace g_ws[kMaxDevices];
 int g_cu_count[kMaxDevices];
-int g_blocks_per_cu[kMaxDevices][2][2][3];  // [dev][fp8][D==128][impl], 0 = unknown
+int g_blocks_per_cu[kMaxDevices][2][2][5][3];  // [dev][fp8][D==128][pages per step][depth], 0 = unknown
 
 int current_device(int* dev) {
     hipError_t e = hipGetDevice(dev);
@@ -351,16 +351,24 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     const int64_t max_pages = block_table->shape[1];
     if ((double)B * ps.H_kv * (double)max_pages >= 2147483647.0)
         return fail(BELLMAN_ERR_UNSUPPORTED, "batch x KV heads x block-table width must stay below 2^31 pages");
-    int max_waves = 0, impl = BELLMAN_IMPL_AUTO;
+    int max_waves = 0, impl = BELLMAN_IMPL_AUTO, pps = 0, depth = 0;
     if (opts) {
         max_waves = opts->max_waves;
         impl = opts->impl;
+        pps = opts->pages_per_step;
+        depth = opts->pipeline_depth;
+        if (depth < 0 || depth > 2) return fail(BELLMAN_ERR_UNSUPPORTED, "pipeline_depth %d not in {0, 1, 2}", depth);
         if (max_waves < 0) return fail(BELLMAN_ERR_INVALID_ARG, "max_waves %d < 0", max_waves);
+        if (pps != 0 && pps != 1 && pps != 2 && pps != 4)
+            return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step %d not in {0, 1, 2, 4}", pps);
         if (impl != BELLMAN_IMPL_AUTO && impl != BELLMAN_IMPL_MFMA && impl != BELLMAN_IMPL_VALU)
             return fail(BELLMAN_ERR_INVALID_ARG, "unknown impl %d", impl);
     }
     if (impl == BELLMAN_IMPL_VALU) return fail(BELLMAN_ERR_UNSUPPORTED, "VALU kernel not built");
     impl = BELLMAN_IMPL_MFMA;
+    if (pps == 4 && !ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step 4 is built for fp8 pools only");
+    if (pps == 0) pps = ps.fp8 ? 4 : 2;
+    if (depth == 0) depth = ps.fp8 ? 1 : 2;  // measured: fp8 steps compute more per byte
     if (B == 0) return BELLMAN_OK;
 
     int dev;
@@ -371,8 +379,11 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
         g_cu_count[dev] = cu;
     }
-    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][impl];
-    if (bpc == 0) bpc = attention_blocks_per_cu(impl, ps.fp8, ps.D);
+    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][pps][depth];
+    if (bpc == 0) {
+        bpc = attention_blocks_per_cu(pps, depth, ps.fp8, ps.D);
+        if (depth == 2) bpc = 1;  // one wavefront per SIMD
+    }
     // Every resident wave takes an equal share of the flattened page stream.
     int64_t waves = (int64_t)g_cu_count[dev] * bpc * (kAttnBlock / kWaveSize);
     if (max_waves > 0 && waves > max_waves) waves = max_waves;
@@ -426,7 +437,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         hipError_t e = hipEventRecord(ev0, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    launch_attention(a, impl, ps.fp8, (int)grid, s);
+    launch_attention(a, pps, depth, ps.fp8, (int)grid, s);
     if ((rc = launch_status("attention"))) return rc;
     if (ev1) {
         hipError_t e = hipEventRecord(ev1, s);

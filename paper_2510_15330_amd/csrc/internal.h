@@ -66,9 +66,9 @@ struct AttnArgs {
 // hipGetLastError in the caller.
 void launch_kv_append(const AppendArgs& a, hipStream_t s);
 void launch_plan(const AttnArgs& a, hipStream_t s);
-void launch_attention(const AttnArgs& a, int impl, bool fp8, int grid, hipStream_t s);
+void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s);
 void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
-int attention_blocks_per_cu(int impl, bool fp8, int D);
+int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 
 }  // namespace bellman

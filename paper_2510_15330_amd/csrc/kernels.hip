@@ -312,25 +312,91 @@ __device__ __forceinline__ void page_pv(AttnState<D>& st, f32x4 sc, const PageV<
     }
 }
 
-// A position in a wave's stream: unit x, which is page p of request b, KV
-// head g.  All fields are wave-uniform.
+// Online softmax over the scores of PP consecutive pages (PP = 2 or 4), then
+// O += V^T P^T with 16x16x32 products over page pairs: in the A operand a
+// lane's elements 0..3 are its four slots of the pair's first page and 4..7
+// its four slots of the second, the same tokens its eight P elements (B
+// operand) carry.
+template <int D, bool FP8, int PP>
+__device__ __forceinline__ void group_pv(AttnState<D>& st, const f32x4 (&sc)[PP], const PageV<D, FP8> (&pv)[PP],
+                                         float sl, const int (&nv)[PP], int qg) {
+    constexpr int NT = D / 16;
+    float x[4 * PP];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < PP; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            x[4 * i + r] = (4 * qg + r < nv[i]) ? sc[i][r] * sl : -INFINITY;
+            mx = fmaxf(mx, x[4 * i + r]);
+        }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(st.m, mx);
+    if (__any(m_new > st.m)) {
+        const float alpha = fast_exp2(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) st.o[t] *= alpha;
+        st.m = m_new;
+    }
+    uint32_t ph[2 * PP], pl[2 * PP];
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4 * PP; i += 2) {
+        const float p0 = fast_exp2(x[i] - st.m);
+        const float p1 = fast_exp2(x[i + 1] - st.m);
+        psum += p0 + p1;
+        const uint32_t u0 = __float_as_uint(p0), u1 = __float_as_uint(p1);
+        const float r0 = p0 - __uint_as_float(u0 & 0xffff0000u);
+        const float r1 = p1 - __uint_as_float(u1 & 0xffff0000u);
+        ph[i / 2] = pack_hi16(u0, u1);
+        pl[i / 2] = pack_hi16(__float_as_uint(r0), __float_as_uint(r1));
+    }
+    st.l += psum;
+#pragma unroll
+    for (int j = 0; j < PP / 2; ++j) {
+        const bf16x8 bph = __builtin_bit_cast(bf16x8, u32x4{ph[4 * j], ph[4 * j + 1], ph[4 * j + 2], ph[4 * j + 3]});
+        const bf16x8 bpl = __builtin_bit_cast(bf16x8, u32x4{pl[4 * j], pl[4 * j + 1], pl[4 * j + 2], pl[4 * j + 3]});
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const u32x2 a0 = v_quad<D, FP8>(pv[2 * j], t, nv[2 * j], qg);
+            const u32x2 a1 = v_quad<D, FP8>(pv[2 * j + 1], t, nv[2 * j + 1], qg);
+            const bf16x8 av = __builtin_bit_cast(bf16x8, u32x4{a0.x, a0.y, a1.x, a1.y});
+            st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bph, st.o[t], 0, 0, 0);
+            st.o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bpl, st.o[t], 0, 0, 0);
+        }
+    }
+}
+
+// A position in a wave's stream: a step of `len` consecutive pages starting
+// at unit x, which is page p of request b, KV head g.  Wave-uniform.
 struct Cursor {
-    int b, g, p;   // request, KV head, page within the request
+    int b, g, p;   // request, KV head, first page of the step within the request
     int np, L;     // the request's pages and clamped length
-    int x;         // flattened unit
+    int x;         // flattened unit of the step's first page
+    int len;       // pages in the step (1..PP; never crosses a request or the range end)
     bool live;     // false once past the wave's range
 };
 
-// Step to the next unit.  A cursor that would leave the range keeps its last
-// position (so loads issued for it stay in bounds) and stops being live.
+template <int PP>
+__device__ __forceinline__ void cursor_len(Cursor& c, int r1) {
+    c.len = min(PP, min(c.np - c.p, r1 - c.x));
+}
+
+// Step to the next group of pages.  A cursor that would leave the range
+// keeps its last position (so loads issued for it stay in bounds) and stops
+// being live.
+template <int PP>
 __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1) {
     if (!c.live) return;
-    if (c.x + 1 >= r1) {
+    if (c.x + c.len >= r1) {
         c.live = false;
         return;
     }
-    ++c.x;
-    if (++c.p >= c.np) {
+    c.x += c.len;
+    c.p += c.len;
+    if (c.p >= c.np) {
         c.p = 0;
         if (++c.g >= a.H_kv) {
             c.g = 0;
@@ -343,10 +409,16 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1
             } while (c.np == 0 && c.b + 1 < a.B);
         }
     }
+    cursor_len<PP>(c, r1);
 }
 
-template <int D, bool FP8>
-__global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu(2))) attn_mfma_kernel(AttnArgs a) {
+// DEPTH steps of PP pages are in flight per wave while it computes one.  With
+// DEPTH = 1 two waves share each SIMD; with DEPTH = 2 each SIMD runs one wave
+// (its issue is not arbitrated against a second, older wave, which otherwise
+// runs ahead and leaves the younger one to finish alone).
+template <int D, bool FP8, int PP, int DEPTH>
+__global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu(DEPTH == 1 ? 2 : 1, DEPTH == 1 ? 2 : 1)))
+attn_mfma_kernel(AttnArgs a) {
     constexpr int NT = D / 16;
     constexpr int KS = D / 32;
     constexpr int EB = FP8 ? 1 : 2;
@@ -365,30 +437,35 @@ __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu
     const size_t page_stride = (size_t)a.H_kv * tile_bytes;
     const bool hv = n < a.G;
 
-    // Three cursors walk the wave's stream: C is computed, I has its page
-    // (and query rows) in flight, T has its block-table entry in flight.
-    Cursor C;
+    // DEPTH + 2 cursors walk the wave's stream: cur[0] is computed,
+    // cur[1..DEPTH] have their pages (and query rows) in flight, and
+    // cur[DEPTH+1] has its block-table entries in flight.
+    Cursor cur[DEPTH + 2];
     {
         const int4 ws = a.wave_start[w];
         const int4 bi = a.b_info[ws.x];
-        C.b = ws.x;
-        C.g = ws.y;
-        C.p = ws.z;
-        C.np = bi.y;
-        C.L = bi.z;
-        C.x = r0;
-        C.live = true;
+        cur[0].b = ws.x;
+        cur[0].g = ws.y;
+        cur[0].p = ws.z;
+        cur[0].np = bi.y;
+        cur[0].L = bi.z;
+        cur[0].x = r0;
+        cur[0].live = true;
+        cursor_len<PP>(cur[0], r1);
     }
-    Cursor I = C;
-    cursor_next(I, a, r1);
-    Cursor T = I;
-    cursor_next(T, a, r1);
+#pragma unroll
+    for (int j = 1; j < DEPTH + 2; ++j) {
+        cur[j] = cur[j - 1];
+        cursor_next<PP>(cur[j], a, r1);
+    }
 
-    // Block-table entry of a unit.  Lane 1 reads the following entry (unused)
-    // so that the address is lane-dependent: this keeps the load a vector
+    // Block-table entries of a step: lane i < PP reads page p + i, clamped to
+    // the step's last page (for one-page steps lane 1 reads an in-row
+    // neighbour, unused).  The lane-dependent address keeps this a vector
     // load, ordered with the page loads, instead of a scalar one.
     auto bt_load = [&](const Cursor& c) -> int {
-        const int idx = min(c.p + (lane & 1), c.np - 1);
+        const int i = PP == 1 ? (lane & 1) : (lane & (PP - 1));
+        const int idx = min(c.p + i, (PP == 1 ? c.np : c.p + c.len) - 1);
         return a.block_table[(int64_t)c.b * a.bt_stride + idx];
     };
     // Query rows of a unit's group as the QK B operand: lane (qg, n) holds
@@ -409,18 +486,23 @@ __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu
         return src[(int64_t)c.b * a.H_kv + c.g];
     };
     int bad_pages = 0;  // wave-uniform: set when a block-table entry is outside the pool
-    // K and V of a unit.  An entry outside the pool is never dereferenced:
-    // page 0 is read instead and the piece's output is poisoned.
-    auto kv_load = [&](const Cursor& c, int btv, PageK<D, FP8>& rk, PageV<D, FP8>& rv, bool& bad) {
-        int pg = __builtin_amdgcn_readlane(btv, 0);
-        bad = (unsigned)pg >= (unsigned)a.num_pages;
-        if (bad) {
-            pg = 0;
-            bad_pages = 1;
+    // K and V of a step's pages.  An entry outside the pool is never
+    // dereferenced: page 0 is read instead and the piece's output is poisoned.
+    // A one-page step of a two-page stream re-reads its page (a cache hit).
+    auto kv_load = [&](const Cursor& c, int btv, PageK<D, FP8> (&rk)[PP], PageV<D, FP8> (&rv)[PP], bool& bad) {
+        bad = false;
+#pragma unroll
+        for (int i = 0; i < PP; ++i) {
+            int pg = __builtin_amdgcn_readlane(btv, i);
+            if ((unsigned)pg >= (unsigned)a.num_pages) {
+                pg = 0;
+                bad = true;
+                bad_pages = 1;
+            }
+            const size_t off = (size_t)pg * page_stride + (size_t)c.g * tile_bytes;
+            load_k<D, FP8>(rk[i], (const char*)a.k_pages + off, qg, n);
+            load_v<D, FP8>(rv[i], (const char*)a.v_pages + off, qg, n);
         }
-        const size_t off = (size_t)pg * page_stride + (size_t)c.g * tile_bytes;
-        load_k<D, FP8>(rk, (const char*)a.k_pages + off, qg, n);
-        load_v<D, FP8>(rv, (const char*)a.v_pages + off, qg, n);
     };
 
     AttnState<D> st;
@@ -465,52 +547,76 @@ __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu
         seg_bad = false;
     };
 
-    // Operands: pages of C (X) and I (Y), query rows of C and of I.  Each step
-    // issues T's block-table entry, I's query rows and I's page, then
-    // computes C.  Every step issues the same loads, in the same order, so
-    // each wait covers exactly the data it needs and one page stays in flight.
-    PageK<D, FP8> kA, kB;
-    PageV<D, FP8> vA, vB;
-    bf16x8 q[KS], qn[KS];
-    float sc = 0.f, scn = 0.f;
-    bool badA = false, badB = false;
-    {
-        const int btC = bt_load(C);
-        q_load(C, q);
-        if constexpr (FP8) sc = scale_load(C);
-        kv_load(C, btC, kA, vA, badA);
+    // Operands live in rings of DEPTH + 1 slots: pages, query rows, fp8
+    // scales.  Each step issues cur[DEPTH+1]'s block-table entries and
+    // cur[DEPTH]'s query rows and pages into the slot freed by the previous
+    // step, then computes cur[0].  Every step issues the same loads, in the
+    // same order, so each wait covers exactly the data it needs and DEPTH
+    // steps stay in flight.
+    PageK<D, FP8> kb[DEPTH + 1][PP];
+    PageV<D, FP8> vb[DEPTH + 1][PP];
+    bf16x8 qb[DEPTH + 1][KS];
+    float scb[DEPTH + 1];
+    bool badb[DEPTH + 1];
+#pragma unroll
+    for (int j = 0; j < DEPTH; ++j) {
+        const int btj = bt_load(cur[j]);
+        q_load(cur[j], qb[j]);
+        scb[j] = 0.f;
+        if constexpr (FP8) scb[j] = scale_load(cur[j]);
+        kv_load(cur[j], btj, kb[j], vb[j], badb[j]);
     }
-    int btI = bt_load(I);
+    int btn = bt_load(cur[DEPTH]);
 
-    auto step = [&](PageK<D, FP8>& kx, PageV<D, FP8>& vx, bool badx, PageK<D, FP8>& ky, PageV<D, FP8>& vy,
-                    bool& bady) -> bool {
-        const int btT = bt_load(T);
-        q_load(I, qn);
-        if constexpr (FP8) scn = scale_load(I);
-        kv_load(I, btI, ky, vy, bady);
-        btI = btT;
+    auto step = [&](auto slot) -> bool {
+        constexpr int sc_ = decltype(slot)::value;                // slot computed now
+        constexpr int ld_ = (sc_ + DEPTH) % (DEPTH + 1);          // slot loaded now
+        const int btT = bt_load(cur[DEPTH + 1]);
+        q_load(cur[DEPTH], qb[ld_]);
+        if constexpr (FP8) scb[ld_] = scale_load(cur[DEPTH]);
+        kv_load(cur[DEPTH], btn, kb[ld_], vb[ld_], badb[ld_]);
+        btn = btT;
 
+        const Cursor& C = cur[0];
         float sl = a.scale_log2, vs = 1.f;
         if constexpr (FP8) {
-            sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), 0));
-            vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sc), 32));
+            sl *= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scb[sc_]), 0));
+            vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scb[sc_]), 32));
         }
-        seg_bad = seg_bad || badx;
-        const f32x4 s4 = page_scores<D, FP8>(kx, q);
-        page_pv<D, FP8>(st, s4, vx, sl, min(kPage, C.L - C.p * kPage), qg);
-        if (C.p + 1 >= C.np || C.x + 1 >= r1) finish(C, vs);
+        seg_bad = seg_bad || badb[sc_];
+        if constexpr (PP == 1) {
+            const f32x4 s4 = page_scores<D, FP8>(kb[sc_][0], qb[sc_]);
+            page_pv<D, FP8>(st, s4, vb[sc_][0], sl, min(kPage, C.L - C.p * kPage), qg);
+        } else {
+            f32x4 sc4[PP];
+            int nv[PP];
 #pragma unroll
-        for (int j = 0; j < KS; ++j) q[j] = qn[j];
-        sc = scn;
-        C = I;
-        I = T;
-        cursor_next(T, a, r1);
-        return C.live;
+            for (int i = 0; i < PP; ++i) {
+                sc4[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+                nv[i] = 0;
+                if (i == 0 || C.len > i) {
+                    sc4[i] = page_scores<D, FP8>(kb[sc_][i], qb[sc_]);
+                    nv[i] = min(kPage, C.L - (C.p + i) * kPage);
+                }
+            }
+            group_pv<D, FP8, PP>(st, sc4, vb[sc_], sl, nv, qg);
+        }
+        if (C.p + C.len >= C.np || C.x + C.len >= r1) finish(C, vs);
+#pragma unroll
+        for (int j = 0; j < DEPTH + 1; ++j) cur[j] = cur[j + 1];
+        cursor_next<PP>(cur[DEPTH + 1], a, r1);
+        return cur[0].live;
     };
 
     for (;;) {
-        if (!step(kA, vA, badA, kB, vB, badB)) break;
-        if (!step(kB, vB, badB, kA, vA, badA)) break;
+        if (!step(std::integral_constant<int, 0>{})) break;
+        if (!step(std::integral_constant<int, 1>{})) break;
+        if constexpr (DEPTH >= 2) {
+            if (!step(std::integral_constant<int, 2>{})) break;
+        }
+        if constexpr (DEPTH >= 3) {
+            if (!step(std::integral_constant<int, 3>{})) break;
+        }
     }
     if (bad_pages) atomicOr(&a.hdr->err_flags, kErrPage);
 }
@@ -586,35 +692,57 @@ void launch_plan(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, a);
 }
 
-void launch_attention(const AttnArgs& a, int impl, bool fp8, int grid, hipStream_t s) {
-    (void)impl;
-    if (a.B == 0 || a.H_q == 0) return;
-    const dim3 g(grid), blk(kAttnBlock);
-    if (a.D == 128) {
-        if (fp8)
-            hipLaunchKernelGGL((attn_mfma_kernel<128, true>), g, blk, 0, s, a);
-        else
-            hipLaunchKernelGGL((attn_mfma_kernel<128, false>), g, blk, 0, s, a);
-    } else {
-        if (fp8)
-            hipLaunchKernelGGL((attn_mfma_kernel<64, true>), g, blk, 0, s, a);
-        else
-            hipLaunchKernelGGL((attn_mfma_kernel<64, false>), g, blk, 0, s, a);
+template <int D, bool FP8, int PP, int DEPTH>
+struct Variant {
+    static void launch(const AttnArgs& a, int grid, hipStream_t s) {
+        hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH>), dim3(grid), dim3(kAttnBlock), 0, s, a);
     }
+    static int occupancy() {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<D, FP8, PP, DEPTH>, kAttnBlock, 0) !=
+                hipSuccess ||
+            nb < 1)
+            nb = 1;
+        return nb;
+    }
+};
+
+// Dispatch on (head_dim, fp8, pages per step, depth): 1 or 2 pages for bf16
+// pools, 1, 2 or 4 for fp8 pools; depth 1 or 2.
+template <int D, bool FP8, int PP>
+static int dispatch_depth(int depth, bool occ, const AttnArgs* a, int grid, hipStream_t s) {
+    if (depth == 2) {
+        if (occ) return Variant<D, FP8, PP, 2>::occupancy();
+        Variant<D, FP8, PP, 2>::launch(*a, grid, s);
+    } else {
+        if (occ) return Variant<D, FP8, PP, 1>::occupancy();
+        Variant<D, FP8, PP, 1>::launch(*a, grid, s);
+    }
+    return 0;
 }
 
-int attention_blocks_per_cu(int impl, bool fp8, int D) {
-    (void)impl;
-    int nb = 0;
-    hipError_t e;
-    if (D == 128)
-        e = fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<128, true>, kAttnBlock, 0)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<128, false>, kAttnBlock, 0);
-    else
-        e = fp8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<64, true>, kAttnBlock, 0)
-                : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<64, false>, kAttnBlock, 0);
-    if (e != hipSuccess || nb < 1) nb = 1;
-    return nb;
+template <int D, bool FP8>
+static int dispatch_pp(int pp, int depth, bool occ, const AttnArgs* a, int grid, hipStream_t s) {
+    if constexpr (FP8) {
+        if (pp == 4) return dispatch_depth<D, FP8, 4>(depth, occ, a, grid, s);
+    }
+    if (pp == 2) return dispatch_depth<D, FP8, 2>(depth, occ, a, grid, s);
+    return dispatch_depth<D, FP8, 1>(depth, occ, a, grid, s);
+}
+
+static int dispatch(int D, bool fp8, int pp, int depth, bool occ, const AttnArgs* a, int grid, hipStream_t s) {
+    if (D == 128) return fp8 ? dispatch_pp<128, true>(pp, depth, occ, a, grid, s)
+                             : dispatch_pp<128, false>(pp, depth, occ, a, grid, s);
+    return fp8 ? dispatch_pp<64, true>(pp, depth, occ, a, grid, s) : dispatch_pp<64, false>(pp, depth, occ, a, grid, s);
+}
+
+void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s) {
+    if (a.B == 0 || a.H_q == 0) return;
+    dispatch(a.D, fp8, pages_per_step, depth, false, &a, grid, s);
+}
+
+int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D) {
+    return dispatch(D, fp8, pages_per_step, depth, true, nullptr, 0, nullptr);
 }
 
 void launch_merge(const AttnArgs& a, hipStream_t s) {

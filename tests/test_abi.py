@@ -145,14 +145,23 @@ def test_append_rejects(B, name, mut, code, msg):
 def test_option_ranges(B):
     g = good(B)
     lib = B.library()
-    opts = B.AttnOpts(-1, 0)
+    opts = B.AttnOpts(-1, 0, 0, 0)
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
     assert rc == ERR_INVALID and "max_waves" in B.last_error()
-    opts = B.AttnOpts(0, 7)
+    opts = B.AttnOpts(0, 7, 0, 0)
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
     assert rc == ERR_INVALID and "impl" in B.last_error()
+    for bad_pps in (3, 4):   # 4 is built for fp8 pools only; these are bf16
+        opts = B.AttnOpts(0, 0, bad_pps, 0)
+        rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
+                                               ctypes.byref(opts), None)
+        assert rc == ERR_UNSUPPORTED and "pages_per_step" in B.last_error()
+    opts = B.AttnOpts(0, 0, 0, 3)
+    rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
+                                           ctypes.byref(opts), None)
+    assert rc == ERR_UNSUPPORTED and "pipeline_depth" in B.last_error()
 
 
 def test_controller_rejects(B):

@@ -87,17 +87,19 @@ def test_tiny_append_bitexact_and_attention(reading):
         assert np.array_equal(G.out_f64(out)[0], v_row)
 
 
+@pytest.mark.parametrize("depth", [1, 2])
+@pytest.mark.parametrize("pps", [1, 2])
 @pytest.mark.parametrize("waves", [1, 2, 3, 7, 64, 5000])
-def test_tiny_wave_counts(waves):
+def test_tiny_wave_counts(waves, pps, depth):
     """Different wave counts cut the requests at different pages (the 16+17+
     200-token batch has 32 (page, head) units, so 64 and 5000 waves leave
     most waves without work); every cut must merge back to the oracle."""
     w = G.to_device(wl.build("tiny", seed=1))
     out = torch.full((w.B, w.H_q, w.D), float("nan"), dtype=torch.bfloat16, device="cuda")
-    G.gpu_step(w, 0, out, max_waves=waves)
+    G.gpu_step(w, 0, out, max_waves=waves, pages_per_step=pps, pipeline_depth=depth)
     torch.cuda.synchronize()
     ref = G.oracle_full(w, 0)
-    G.assert_close(G.out_f64(out), ref, "bf16", f"waves={waves}")
+    G.assert_close(G.out_f64(out), ref, "bf16", f"waves={waves} pages/step={pps}")
 
 
 # ------------------------------------------------------ llama3-8b config ---
@@ -198,8 +200,8 @@ def test_closed_forms_exact():
     kp, vp = dn.write_pools(case["dense_k"], case["dense_v"], lens, case["page_lists"], case["num_pages"],
                             2, 128, 8, np.uint16(0x7FC0))
     case.update(k_pages=kp, v_pages=vp)
-    for waves in (1, 8, 0):
-        got = run_case(dev_case(case), 0.088, max_waves=waves)
+    for waves, pps in ((1, 1), (8, 1), (0, 1), (1, 2), (8, 2), (0, 2)):
+        got = run_case(dev_case(case), 0.088, max_waves=waves, pages_per_step=pps)
         for b in range(3):
             for h in range(8):
                 ref = dn.bits_to_f64_bf16(cv[b][h // 4]).copy()
@@ -221,8 +223,11 @@ def test_edge_shapes(B, Hq, Hkv, D, lens, kv):
     scale = float(np.float32(1.0 / np.sqrt(D)))
     ref = oracle_case(case, scale, kv)
     for waves in (0, 1, 5, 13):
-        got = run_case(dev_case(case, kv), scale, max_waves=waves)
-        G.assert_close(got, ref, kv, f"edge {B},{Hq},{Hkv},{D},{lens},{kv} waves={waves}")
+        for pps in ((1, 2, 4) if kv == "fp8" else (1, 2)):
+            for depth in (1, 2):
+                got = run_case(dev_case(case, kv), scale, max_waves=waves, pages_per_step=pps, pipeline_depth=depth)
+                G.assert_close(got, ref, kv, f"edge {B},{Hq},{Hkv},{D},{lens},{kv} waves={waves} "
+                                             f"pages/step={pps} depth={depth}")
         for b, L in enumerate(lens):
             if L == 0:
                 assert np.all(got[b] == 0.0)
@@ -243,11 +248,12 @@ def test_fp8_every_code_through_single_token_rows():
     kp, vp = dn.write_pools(case["dense_k"], case["dense_v"], [1, 1], case["page_lists"], case["num_pages"],
                             Hkv, D, 16, np.uint8(0x7F))
     case.update(k_pages=kp, v_pages=vp)
-    got = run_case(dev_case(case, "fp8"), 0.1)
     ref = dn.codes_to_f64_fp8(allc).reshape(2, 128)
-    for b in range(2):
-        for h in range(Hq):
-            assert np.array_equal(got[b, h], ref[b]), f"fp8 code decode b={b} h={h}"
+    for pps in (1, 2, 4):
+        got = run_case(dev_case(case, "fp8"), 0.1, pages_per_step=pps)
+        for b in range(2):
+            for h in range(Hq):
+                assert np.array_equal(got[b, h], ref[b]), f"fp8 code decode b={b} h={h} pages/step={pps}"
 
 
 def test_bad_block_table_entry_is_flagged_not_read():
