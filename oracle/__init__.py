@@ -62,8 +62,10 @@ def _bind(lib):
     lib.oracle_decode_attention.argtypes = [
         i32, i32, i32, i32, i32, P, P, P, i64, P, P, P, i32, P, ctypes.c_float, P]
     lib.oracle_decode_attention.restype = i32
-    lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, P, P, P, P, i64, P, i32, P]
+    lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, i64, P, P, P, i32, P]
     lib.oracle_kv_append.restype = i32
+    lib.oracle_quantize_e4m3fn.argtypes = [ctypes.c_float, ctypes.c_float]
+    lib.oracle_quantize_e4m3fn.restype = ctypes.c_uint8
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = i32
     return lib
@@ -123,21 +125,36 @@ def decode_attention(q_bits, k_pages, v_pages, block_table, seq_lens, scale,
     return out
 
 
+def quantize_e4m3fn(x: float, scale: float, lib=None) -> int:
+    return (lib or load()).oracle_quantize_e4m3fn(float(x), float(scale))
+
+
 def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens,
-              kv_dtype=BF16, lib=None):
-    """Byte-exact append on host copies; mutates k_pages, v_pages, seq_lens."""
+              kv_dtype=BF16, k_scale=None, v_scale=None, lib=None):
+    """Append on host copies; mutates k_pages, v_pages, seq_lens.
+
+    Rows of the pool's element type are copied byte for byte; bf16 rows
+    (uint16 bit patterns) into fp8 pools are quantised with the per-(request,
+    KV head) scales k_scale / v_scale (float32 [B, H_kv])."""
     lib = lib or load()
     code = np.uint16 if kv_dtype == BF16 else np.uint8
     for a in (k_pages, v_pages, seq_lens):
         assert a.flags.c_contiguous
-    k_new = _c(k_new, code)
-    v_new = _c(v_new, code)
+    new_dtype = BF16 if np.asarray(k_new).dtype == np.uint16 else FP8_E4M3FN
+    ncode = np.uint16 if new_dtype == BF16 else np.uint8
+    k_new = _c(k_new, ncode)
+    v_new = _c(v_new, ncode)
     assert k_pages.dtype == code and v_pages.dtype == code
     assert seq_lens.dtype == np.int32
+    if new_dtype != kv_dtype:
+        assert kv_dtype == FP8_E4M3FN and new_dtype == BF16
+        k_scale = _c(k_scale, np.float32)
+        v_scale = _c(v_scale, np.float32)
     block_table = _c(block_table, np.int32)
     B, H_kv, D = k_new.shape
-    rc = lib.oracle_kv_append(B, H_kv, D, kv_dtype, _ptr(k_new), _ptr(v_new),
+    rc = lib.oracle_kv_append(B, H_kv, D, kv_dtype, new_dtype, _ptr(k_new), _ptr(v_new),
                               _ptr(k_pages), _ptr(v_pages), k_pages.shape[0],
+                              _ptr(k_scale), _ptr(v_scale),
                               _ptr(block_table), block_table.shape[1], _ptr(seq_lens))
     if rc != 0:
         raise ValueError(f"oracle_kv_append failed: {rc}")

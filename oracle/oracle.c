@@ -191,21 +191,68 @@ int oracle_decode_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
     return bad ? -2 : 0;
 }
 
+/* Quantise one value to OCP e4m3fn: v = x / scale in binary32 (one correctly
+ * rounded division), then round to the nearest e4m3fn value, ties to the
+ * even mantissa, saturating to +-448; NaN stays NaN.  Written from the format
+ * definition: normal values are (1 + m/8) 2^(e-7) for e in 1..15, m in 0..7
+ * except e = 15, m = 7 (NaN); subnormals are (m/8) 2^-6. */
+uint8_t oracle_quantize_e4m3fn(float x, float scale)
+{
+    float v = x / scale;
+    int sign = signbit(v) ? 0x80 : 0;
+    double a = fabs((double)v);
+    double step, scaled, r, fl;
+    int e, code;
+    if (isnan(v))
+        return (uint8_t)(sign | 0x7F);
+    if (a >= 448.0)
+        return (uint8_t)(sign | 0x7E);
+    if (a < ldexp(1.0, -6)) {
+        step = ldexp(1.0, -9);                         /* subnormal spacing */
+    } else {
+        e = (int)floor(log2(a));
+        if (ldexp(1.0, e) > a) e -= 1;                 /* guard log2 rounding */
+        if (ldexp(1.0, e + 1) <= a) e += 1;
+        step = ldexp(1.0, e - 3);                      /* 3 mantissa bits */
+    }
+    scaled = a / step;                                 /* exact: power-of-two step */
+    fl = floor(scaled);
+    r = scaled - fl;
+    if (r > 0.5 || (r == 0.5 && fmod(fl, 2.0) != 0.0))
+        fl += 1.0;
+    a = fl * step;                                     /* rounded magnitude */
+    if (a >= 448.0)
+        return (uint8_t)(sign | 0x7E);
+    if (a < ldexp(1.0, -6)) {
+        code = (int)(a / ldexp(1.0, -9));              /* 0..7 */
+    } else {
+        e = (int)floor(log2(a));
+        if (ldexp(1.0, e) > a) e -= 1;
+        if (ldexp(1.0, e + 1) <= a) e += 1;
+        code = ((e + 7) << 3) | (int)(a / ldexp(1.0, e - 3) - 8.0);
+    }
+    return (uint8_t)(sign | code);
+}
+
 /*
  * KV append, on host copies of the pools: for each request b the new token's
- * K and V rows ([B, H_kv, D] codes of the pool's element type) are copied
- * byte for byte into page block_table[b][L/16], slot L%16, with L =
- * seq_lens[b]; then seq_lens[b] becomes L + 1.  Nothing else is written.
- * Returns 0, or -1 (and writes nothing) when a slot falls outside the block
- * table or the page pool.
+ * K and V rows ([B, H_kv, D]) are written into page block_table[b][L/16],
+ * slot L%16, with L = seq_lens[b]; then seq_lens[b] becomes L + 1.  Nothing
+ * else is written.  new_dtype == pool dtype: the rows are codes of that type,
+ * copied byte for byte.  bf16 rows into fp8 pools: each value x of head g is
+ * stored as oracle_quantize_e4m3fn(x, scale[b, g]) with that request's K or
+ * V scale.  Returns 0, or -1 (and writes nothing) when a slot falls outside
+ * the block table or the page pool.
  */
-int oracle_kv_append(int B, int H_kv, int D, int kv_dtype,
+int oracle_kv_append(int B, int H_kv, int D, int kv_dtype, int new_dtype,
                      const void *k_new, const void *v_new,
                      void *k_pages, void *v_pages, int64_t num_pages,
+                     const float *k_scale, const float *v_scale,
                      const int32_t *block_table, int max_pages, int32_t *seq_lens)
 {
     const int eb = elem_bytes(kv_dtype);
     const int x = 16 / eb;
+    const int quant = kv_dtype == ORACLE_FP8_E4M3FN && new_dtype == ORACLE_BF16;
 
     for (int b = 0; b < B; ++b) {
         int L = seq_lens[b];
@@ -224,10 +271,17 @@ int oracle_kv_append(int B, int H_kv, int D, int kv_dtype,
         for (int g = 0; g < H_kv; ++g) {
             for (int d = 0; d < D; ++d) {
                 int64_t src = ((int64_t)b * H_kv + g) * D + d;
-                memcpy((char *)k_pages + k_offset(pg, g, slot, d, H_kv, D, x) * eb,
-                       (const char *)k_new + src * eb, (size_t)eb);
-                memcpy((char *)v_pages + v_offset(pg, g, slot, d, H_kv, D) * eb,
-                       (const char *)v_new + src * eb, (size_t)eb);
+                char *kdst = (char *)k_pages + k_offset(pg, g, slot, d, H_kv, D, x) * eb;
+                char *vdst = (char *)v_pages + v_offset(pg, g, slot, d, H_kv, D) * eb;
+                if (quant) {
+                    float kx = (float)oracle_bf16_to_f64(((const uint16_t *)k_new)[src]);
+                    float vx = (float)oracle_bf16_to_f64(((const uint16_t *)v_new)[src]);
+                    *(uint8_t *)kdst = oracle_quantize_e4m3fn(kx, k_scale[(int64_t)b * H_kv + g]);
+                    *(uint8_t *)vdst = oracle_quantize_e4m3fn(vx, v_scale[(int64_t)b * H_kv + g]);
+                } else {
+                    memcpy(kdst, (const char *)k_new + src * eb, (size_t)eb);
+                    memcpy(vdst, (const char *)v_new + src * eb, (size_t)eb);
+                }
             }
         }
         seq_lens[b] = L + 1;
