@@ -82,9 +82,14 @@ typedef struct bellman_tensor {
 /*
  * Append one token per request to the paged KV cache (the step that grows
  * each request's KV length by one token per decode step, Sec. 3).
- *   k_new, v_new  [B, H_kv, D], same element type as the pools (fp8 codes
- *                 are copied as they are, already quantised with the
- *                 request's scale); innermost dim contiguous.
+ *   k_new, v_new  [B, H_kv, D], innermost dim contiguous.  Either the
+ *                 pools' element type (codes copied as they are), or bf16
+ *                 rows for fp8 pools: then each value x of KV head g is
+ *                 stored as e4m3fn(x / scale[b, g]) with the pool's
+ *                 dequant_scale (K's for k_new, V's for v_new), the quotient
+ *                 one correctly rounded binary32 division, rounded to
+ *                 nearest with ties to the even mantissa, saturating at
+ *                 +-448, NaN kept.
  *   k_pages       [NP, H_kv, D/x, 16, x] contiguous (written).
  *   v_pages       [NP, H_kv, D, 16] contiguous (written).
  *   block_table   int32 [B, maxP], innermost contiguous; the page that will
@@ -93,7 +98,8 @@ typedef struct bellman_tensor {
  *                 request b goes to position L = seq_lens[b]
  *                 (page block_table[b][L/16], slot L%16), then seq_lens[b]
  *                 becomes L + 1.
- * The copy is bit-exact and writes nothing else.  A request whose slot lies
+ * The write is bit-exact (a byte copy, or the quantisation above) and
+ * touches nothing else.  A request whose slot lies
  * outside the block table or the pool is skipped (no byte written, length
  * unchanged) and flagged in the device error word.
  */

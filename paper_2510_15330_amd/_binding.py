@@ -151,11 +151,15 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
-def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None):
-    """bellman_kv_append: write one token per request, then seq_lens += 1."""
-    _device_tensors(k_new, v_new, k_pages, v_pages, block_table, seq_lens)
+def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None,
+              k_scale=None, v_scale=None):
+    """bellman_kv_append: write one token per request, then seq_lens += 1.
+
+    bf16 rows into fp8 pools are quantised with k_scale / v_scale (the
+    pools' per-(request, KV head) dequantisation scales)."""
+    _device_tensors(k_new, v_new, k_pages, v_pages, block_table, seq_lens, k_scale, v_scale)
     lib = library()
-    _check(lib.bellman_kv_append(desc(k_new), desc(v_new), desc(k_pages), desc(v_pages),
+    _check(lib.bellman_kv_append(desc(k_new), desc(v_new), desc(k_pages, k_scale), desc(v_pages, v_scale),
                                  desc(block_table), desc(seq_lens), _stream(stream)))
 
 

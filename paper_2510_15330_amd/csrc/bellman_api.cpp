@@ -291,11 +291,16 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     if ((rc = check_pools(k_pages, v_pages, &ps, false))) return rc;
     if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
     const int64_t B = k_new->shape[0];
-    const size_t eb = ps.fp8 ? 1 : 2;
-    if ((rc = check_rows(k_new, "k_new", k_pages->dtype, B, ps.H_kv, ps.D, 16))) return rc;
-    if ((rc = check_rows(v_new, "v_new", k_pages->dtype, B, ps.H_kv, ps.D, eb))) return rc;
+    // bf16 rows into fp8 pools are quantised with the pools' dequant scales
+    const bool quant = ps.fp8 && k_new->dtype == BELLMAN_BF16;
+    const int32_t row_dtype = quant ? (int32_t)BELLMAN_BF16 : k_pages->dtype;
+    const size_t row_eb = (size_t)elem_size(row_dtype);
+    if ((rc = check_rows(k_new, "k_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
+    if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, row_eb))) return rc;
     if ((rc = check_block_table(block_table, B))) return rc;
     if ((rc = check_seq_lens(seq_lens, B))) return rc;
+    if (quant && (!k_pages->dequant_scale || !v_pages->dequant_scale))
+        return fail(BELLMAN_ERR_INVALID_ARG, "quantising bf16 rows into fp8 pools needs dequant_scale on both pools");
     if (B > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "batch too large");
     if (B == 0) return BELLMAN_OK;
 
@@ -318,11 +323,14 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     a.seq_lens = (int32_t*)seq_lens->data;
     a.err = &((WorkspaceHeader*)base)->err_flags;
     a.num_pages = ps.num_pages;
+    a.k_scale = k_pages->dequant_scale;
+    a.v_scale = v_pages->dequant_scale;
     a.B = (int)B;
     a.H_kv = ps.H_kv;
     a.D = ps.D;
     a.max_pages = (int)block_table->shape[1];
-    a.elem_bytes = (int)eb;
+    a.elem_bytes = ps.fp8 ? 1 : 2;
+    a.quant = quant ? 1 : 0;
     launch_kv_append(a, (hipStream_t)stream);
     return launch_status("kv_append");
 }

@@ -35,7 +35,10 @@ struct AppendArgs {
     int32_t* seq_lens;
     int32_t* err;
     int64_t num_pages;
+    const float* k_scale;  // quantising append only: fp32 [B, H_kv]
+    const float* v_scale;
     int B, H_kv, D, max_pages, elem_bytes;
+    int quant;             // 1: bf16 rows quantised into fp8 pools
 };
 
 struct AttnArgs {

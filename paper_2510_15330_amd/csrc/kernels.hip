@@ -39,8 +39,32 @@ __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w, bool high) {
 }
 
 // ------------------------------------------------------------- KV append ---
-// One workgroup per request: copy the new K row into its 16-byte chunks and
-// the new V row into its slot column, then advance the request's length.
+// x / scale rounded to OCP e4m3fn: nearest, ties to the even mantissa,
+// saturating at +-448, NaN kept.  The quotient is one correctly rounded
+// binary32 division.
+__device__ __forceinline__ uint32_t quantize_e4m3fn(float x, float scale) {
+    const float v = __fdiv_rn(x, scale);
+    const uint32_t u = __float_as_uint(v);
+    const uint32_t sign = (u >> 24) & 0x80u;
+    const uint32_t a = u & 0x7fffffffu;
+    if (a > 0x7f800000u) return sign | 0x7fu;          // NaN
+    if (a >= 0x43e00000u) return sign | 0x7eu;         // |v| >= 448 (and inf)
+    if (a < 0x3c800000u)                                // |v| < 2^-6: multiples of 2^-9
+        return sign | (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    uint32_t e = (a >> 23) - 120u;                      // e4m3 biased exponent, 1..15
+    uint32_t q = (a >> 20) & 7u;                        // top three mantissa bits
+    const uint32_t rem = a & 0xfffffu;
+    if (rem > 0x80000u || (rem == 0x80000u && (q & 1u))) ++q;
+    if (q == 8u) {
+        q = 0u;
+        ++e;
+    }
+    return sign | (e << 3) | q;                         // below 448 nothing rounds past 448
+}
+
+// One workgroup per request: write the new K row into its 16-byte chunks and
+// the new V row into its slot column (copying codes, or quantising bf16 rows
+// into fp8 pools), then advance the request's length.
 __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
     const int b = blockIdx.x;
     const int L = a.seq_lens[b];
@@ -59,23 +83,55 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
     const int64_t tile_elems = (int64_t)a.D * kPage;
 
     char* kp = (char*)a.k_pages;
-    const char* kn = (const char*)a.k_new;
-    for (int i = threadIdx.x; i < a.H_kv * chunks; i += blockDim.x) {
-        const int g = i / chunks, c = i - g * chunks;
-        const int64_t src = (int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * x;
-        const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;  // 16-byte units
-        *(u32x4*)(kp + dst * 16) = *(const u32x4*)(kn + src * eb);
-    }
     char* vp = (char*)a.v_pages;
-    const char* vn = (const char*)a.v_new;
-    for (int i = threadIdx.x; i < a.H_kv * a.D; i += blockDim.x) {
-        const int g = i / a.D, d = i - g * a.D;
-        const int64_t src = (int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d;
-        const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d * kPage + slot;
-        if (eb == 2)
-            *(uint16_t*)(vp + dst * 2) = *(const uint16_t*)(vn + src * 2);
-        else
-            *(uint8_t*)(vp + dst) = *(const uint8_t*)(vn + src);
+    if (!a.quant) {
+        const char* kn = (const char*)a.k_new;
+        for (int i = threadIdx.x; i < a.H_kv * chunks; i += blockDim.x) {
+            const int g = i / chunks, c = i - g * chunks;
+            const int64_t src = (int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * x;
+            const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;  // 16-byte units
+            *(u32x4*)(kp + dst * 16) = *(const u32x4*)(kn + src * eb);
+        }
+        const char* vn = (const char*)a.v_new;
+        for (int i = threadIdx.x; i < a.H_kv * a.D; i += blockDim.x) {
+            const int g = i / a.D, d = i - g * a.D;
+            const int64_t src = (int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d;
+            const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d * kPage + slot;
+            if (eb == 2)
+                *(uint16_t*)(vp + dst * 2) = *(const uint16_t*)(vn + src * 2);
+            else
+                *(uint8_t*)(vp + dst) = *(const uint8_t*)(vn + src);
+        }
+    } else {
+        // bf16 rows -> e4m3fn codes; fp8 pools hold 16 dims per 16-byte chunk
+        const uint16_t* kn = (const uint16_t*)a.k_new;
+        for (int i = threadIdx.x; i < a.H_kv * chunks; i += blockDim.x) {
+            const int g = i / chunks, c = i - g * chunks;
+            const float ks = a.k_scale[(int64_t)b * a.H_kv + g];
+            const uint16_t* src = kn + (int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * 16;
+            const u32x4 w0 = *(const u32x4*)src;
+            const u32x4 w1 = *(const u32x4*)(src + 8);
+            const uint32_t in[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            uint32_t outw[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint32_t lo = in[2 * k], hi = in[2 * k + 1];
+                outw[k] = quantize_e4m3fn(__uint_as_float(lo << 16), ks) |
+                          (quantize_e4m3fn(__uint_as_float(lo & 0xffff0000u), ks) << 8) |
+                          (quantize_e4m3fn(__uint_as_float(hi << 16), ks) << 16) |
+                          (quantize_e4m3fn(__uint_as_float(hi & 0xffff0000u), ks) << 24);
+            }
+            const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;
+            *(u32x4*)(kp + dst * 16) = u32x4{outw[0], outw[1], outw[2], outw[3]};
+        }
+        const uint16_t* vn = (const uint16_t*)a.v_new;
+        for (int i = threadIdx.x; i < a.H_kv * a.D; i += blockDim.x) {
+            const int g = i / a.D, d = i - g * a.D;
+            const float vs = a.v_scale[(int64_t)b * a.H_kv + g];
+            const uint32_t bits = vn[(int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d];
+            const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d * kPage + slot;
+            *(uint8_t*)(vp + dst) = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), vs);
+        }
     }
     __syncthreads();  // every thread has read seq_lens[b]
     if (threadIdx.x == 0) a.seq_lens[b] = L + 1;

@@ -295,3 +295,67 @@ def test_empty_batch_is_noop():
     out = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
     bl.decode_attention(q, k, v, bt, sl, 0.125, out)
     torch.cuda.synchronize()
+
+
+# ------------------------------------------------------ quantising append ---
+
+def test_quantising_append_every_bf16_pattern():
+    """bf16 rows into fp8 pools: all 65536 bf16 bit patterns go through the
+    quantiser (K in order, V permuted) under mixed scales; the whole pools
+    must equal the oracle's byte for byte."""
+    rng = np.random.default_rng(41)
+    B, H_kv, D, NP = 64, 8, 128, 80
+    maxP = 1
+    lens = rng.integers(0, 16, size=B).astype(np.int32)
+    bt = rng.permutation(NP)[:B].astype(np.int32).reshape(B, maxP)
+    kp = rng.integers(0, 256, size=(NP, H_kv, D // 16, 16, 16)).astype(np.uint8)
+    vp = rng.integers(0, 256, size=(NP, H_kv, D, 16)).astype(np.uint8)
+    allbits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    kn = allbits.reshape(B, H_kv, D)
+    vn = rng.permutation(allbits).reshape(B, H_kv, D)
+    ks = np.float32(2.0) ** rng.integers(-12, 12, size=(B, H_kv)).astype(np.float32) * \
+        rng.uniform(0.5, 1.0, size=(B, H_kv)).astype(np.float32)
+    vs = rng.uniform(1e-3, 10.0, size=(B, H_kv)).astype(np.float32)
+    ref_k, ref_v, ref_sl = kp.copy(), vp.copy(), lens.copy()
+    oracle.kv_append(kn, vn, ref_k, ref_v, bt, ref_sl, oracle.FP8_E4M3FN, ks, vs)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    dk, dv, dsl = t(kp), t(vp), t(lens)
+    bl.kv_append(t(kn.view(np.int16)).view(torch.bfloat16), t(vn.view(np.int16)).view(torch.bfloat16),
+                 dk, dv, t(bt), dsl, k_scale=t(ks), v_scale=t(vs))
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    assert np.array_equal(dsl.cpu().numpy(), ref_sl)
+    gk, gv = dk.cpu().numpy(), dv.cpu().numpy()
+    bad_k = np.argwhere(gk != ref_k)
+    assert len(bad_k) == 0, f"K pool differs at {len(bad_k)} bytes, first {bad_k[:3]}"
+    assert np.array_equal(gv, ref_v), f"V pool differs at {int((gv != ref_v).sum())} bytes"
+
+
+def test_quantising_append_then_attention():
+    """A decode run of a shrunk fp8 workload whose new rows arrive as bf16 and
+    are quantised by the append; appends bit-exact, attention within the fp8
+    bounds at every step."""
+    rng = np.random.default_rng(42)
+    B, H_q, H_kv, D, steps = 6, 64, 8, 128, 4
+    lens = [1, 15, 16, 100, 333, 1000]
+    case = dn.random_case(rng, B, H_q, H_kv, D, [L + steps for L in lens], "fp8")
+    # values of the size the workloads have (code 448 <-> about 4 sigma of N(0, 1))
+    case["k_scale"][:] = np.float32(4.0 / 448.0)
+    case["v_scale"][:] = np.float32(4.0 / 448.0)
+    sl0 = np.asarray(lens, dtype=np.int32)
+    d = dev_case(dict(case, seq_lens=sl0), "fp8")
+    kp, vp = case["k_pages"].copy(), case["v_pages"].copy()
+    sl = sl0.copy()
+    for s in range(steps):
+        kn = torch.from_numpy(rng.standard_normal((B, H_kv, D)).astype(np.float32)).to(torch.bfloat16)
+        vn = torch.from_numpy(rng.standard_normal((B, H_kv, D)).astype(np.float32)).to(torch.bfloat16)
+        kb = kn.view(torch.int16).numpy().view(np.uint16)
+        vb = vn.view(torch.int16).numpy().view(np.uint16)
+        oracle.kv_append(kb, vb, kp, vp, case["block_table"], sl, oracle.FP8_E4M3FN, case["k_scale"], case["v_scale"])
+        bl.kv_append(kn.cuda(), vn.cuda(), d["k"], d["v"], d["bt"], d["sl"], k_scale=d["ks"], v_scale=d["vs"])
+        got = run_case(d, float(np.float32(1 / np.sqrt(D))))
+        assert np.array_equal(d["k"].cpu().numpy(), kp) and np.array_equal(d["v"].cpu().numpy(), vp), f"step {s}"
+        ref = oracle.decode_attention(case["q_bits"], kp, vp, case["block_table"], sl,
+                                      float(np.float32(1 / np.sqrt(D))), oracle.FP8_E4M3FN,
+                                      case["k_scale"], case["v_scale"])
+        G.assert_close(got, ref, "fp8", f"quantising append step {s}")
