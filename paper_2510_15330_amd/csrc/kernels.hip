@@ -20,6 +20,8 @@ typedef short s16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     uint32_t u = __float_as_uint(f);
@@ -273,6 +275,22 @@ __device__ __forceinline__ void load_v(PageV<D, FP8>& r, const char* vbase, int 
     }
 }
 
+// Four-page fp8 steps hold V by page: lane (qg, n) reads the whole 16-slot
+// row of dim 16t + n of page qg (16 bytes), so one instruction covers all four
+// pages' 256-byte row blocks of tile t.  rv[j].v[t] is the row's dword j
+// (slots 4j..4j+3).
+template <int D>
+__device__ __forceinline__ void load_v_rows(PageV<D, true> (&rv)[4], const char* vbase, int n) {
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) {
+        const u32x4 w = ld_stream<u32x4>(vbase + (size_t)(16 * t + n) * kPage);
+        rv[0].v[t] = w.x;
+        rv[1].v[t] = w.y;
+        rv[2].v[t] = w.z;
+        rv[3].v[t] = w.w;
+    }
+}
+
 // Scores of one page: lane (qg, n) gets head n at slots 4qg..4qg+3.
 template <int D, bool FP8>
 __device__ __forceinline__ f32x4 page_scores(const PageK<D, FP8>& r, const bf16x8 (&bq)[D / 32]) {
@@ -425,6 +443,211 @@ __device__ __forceinline__ void group_pv(AttnState<D>& st, const f32x4 (&sc)[PP]
     }
 }
 
+// ------------------------------------------------- fp8 pages on fp8 MFMA ---
+// v_mfma_scale_f32_16x16x128_f8f6f4 multiplies e4m3 operands directly; each
+// lane supplies 32 elements of its 16-lane group's k-block and an E8M0 scale
+// (2^(s-127)) for them.  K and V codes enter as loaded.  Q and P are split
+// into e4m3 hi + lo terms (residual scaled by 16), about 2^-8 relative, and
+// the power-of-two factors of the split ride in the scale operands.
+constexpr int kE8M0One = 127;
+
+__device__ __forceinline__ f32x4 mfma_f8(const i32x8& a, const i32x8& b, f32x4 c, int scale_b) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, kE8M0One, 0, scale_b);
+}
+
+// Codes of two floats into the low (hi = false) or high half of w.
+__device__ __forceinline__ uint32_t f32x2_to_fp8(float a, float b, uint32_t w, bool hi) {
+    return hi ? (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, true)
+              : (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(a, b, (int)w, false);
+}
+__device__ __forceinline__ f32x2 fp8x2_to_f32(uint32_t w, bool hi) {
+    return hi ? __builtin_amdgcn_cvt_pk_f32_fp8(w, true) : __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+}
+
+// Split four values v (already scaled into the e4m3 range) into hi and lo
+// code words: hi = e4m3(v), lo = e4m3(16 (v - hi)).
+__device__ __forceinline__ void split4(const float (&v)[4], uint32_t& hi, uint32_t& lo) {
+    hi = f32x2_to_fp8(v[0], v[1], 0u, false);
+    hi = f32x2_to_fp8(v[2], v[3], hi, true);
+    const f32x2 h01 = fp8x2_to_f32(hi, false), h23 = fp8x2_to_f32(hi, true);
+    lo = f32x2_to_fp8(16.f * (v[0] - h01.x), 16.f * (v[1] - h01.y), 0u, false);
+    lo = f32x2_to_fp8(16.f * (v[2] - h23.x), 16.f * (v[3] - h23.y), lo, true);
+}
+
+// Query rows of a (request, head) group as fp8 B operands of the QK product.
+// Lane (qg, n) holds head n's dims of chunks qg and qg+4 (the K operand's
+// order), scaled by 2^k with k chosen per head so the row's largest
+// magnitude lands in [128, 256); 2^-k and 2^-(k+4) go into the E8M0 scales.
+struct Q8 {
+    i32x8 hi, lo;
+    int s_hi, s_lo;
+};
+
+template <int D>
+__device__ __forceinline__ void q_to_fp8(const bf16x8 (&bq)[D / 32], Q8& q8) {
+    constexpr int NV = D / 4;          // values this lane holds: 32 (D = 128) or 16 (D = 64)
+    float v[NV];
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) {
+        const u32x4 w = __builtin_bit_cast(u32x4, bq[j]);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[8 * j + 2 * i] = __uint_as_float(ws[i] << 16);
+            v[8 * j + 2 * i + 1] = __uint_as_float(ws[i] & 0xffff0000u);
+        }
+    }
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) amax = fmaxf(amax, fabsf(v[i]));
+    amax = fmaxf(amax, __shfl_xor(amax, 16));
+    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    // 2^e <= amax < 2^(e+1); scale by 2^(7-e); keep the E8M0 exponents in range
+    int e = amax > 0.f ? (int)((__float_as_uint(amax) >> 23) & 0xffu) - 127 : 0;
+    int k = 7 - e;
+    k = max(-120, min(k, 120));
+    const float sq = __uint_as_float((uint32_t)(k + 127) << 23);
+    uint32_t hw[8], lw[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        hw[i] = 0u;
+        lw[i] = 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < NV / 4; ++i) {
+        const float t[4] = {v[4 * i] * sq, v[4 * i + 1] * sq, v[4 * i + 2] * sq, v[4 * i + 3] * sq};
+        split4(t, hw[i], lw[i]);
+    }
+    q8.hi = i32x8{(int)hw[0], (int)hw[1], (int)hw[2], (int)hw[3], (int)hw[4], (int)hw[5], (int)hw[6], (int)hw[7]};
+    q8.lo = i32x8{(int)lw[0], (int)lw[1], (int)lw[2], (int)lw[3], (int)lw[4], (int)lw[5], (int)lw[6], (int)lw[7]};
+    q8.s_hi = kE8M0One - k;
+    q8.s_lo = kE8M0One - k - 4;
+}
+
+// 4x4 transpose of dwords over the four 16-lane groups: afterwards register j
+// of lane group g holds what register g of lane group j held.  A 32-lane swap
+// exchanges the off-diagonal 2x2 blocks, a 16-lane swap transposes within them.
+__device__ __forceinline__ void transpose4(int (&r)[8]) {
+    auto a = __builtin_amdgcn_permlane32_swap((unsigned)r[0], (unsigned)r[2], false, false);
+    auto b = __builtin_amdgcn_permlane32_swap((unsigned)r[1], (unsigned)r[3], false, false);
+    auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+    auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+    r[0] = (int)c[0];
+    r[1] = (int)c[1];
+    r[2] = (int)d[0];
+    r[3] = (int)d[1];
+}
+
+// One step of PP fp8 pages: scores on fp8 MFMA, online softmax, then
+// O += V^T P^T with the step's 4*PP tokens per lane group (zero-padded to the
+// instruction's 32-element blocks).  V codes of slots >= nv are zeroed.
+template <int D, int PP>
+__device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> (&kx)[PP],
+                                         const PageV<D, true> (&vx)[PP], const Q8& q8, float sl,
+                                         const int (&nv)[PP], int qg) {
+    constexpr int NT = D / 16;
+    float x[4 * PP];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < PP; ++i) {
+        // pages past the step's end were loaded from a valid page; their
+        // scores are masked below, so the products run unconditionally
+        i32x8 ka;
+        if constexpr (D == 128)
+            ka = i32x8{(int)kx[i].k[0].x, (int)kx[i].k[0].y, (int)kx[i].k[0].z, (int)kx[i].k[0].w,
+                       (int)kx[i].k[1].x, (int)kx[i].k[1].y, (int)kx[i].k[1].z, (int)kx[i].k[1].w};
+        else  // upper half meets the zero half of the query operand; a copy of
+              // the lower half keeps the register file free of a wide memory view
+            ka = i32x8{(int)kx[i].k[0].x, (int)kx[i].k[0].y, (int)kx[i].k[0].z, (int)kx[i].k[0].w,
+                       (int)kx[i].k[0].x, (int)kx[i].k[0].y, (int)kx[i].k[0].z, (int)kx[i].k[0].w};
+        f32x4 s4 = {0.f, 0.f, 0.f, 0.f};
+        s4 = mfma_f8(ka, q8.hi, s4, q8.s_hi);
+        s4 = mfma_f8(ka, q8.lo, s4, q8.s_lo);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            x[4 * i + r] = (4 * qg + r < nv[i]) ? s4[r] * sl : -INFINITY;
+            mx = fmaxf(mx, x[4 * i + r]);
+        }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(st.m, mx);
+    if (__any(m_new > st.m)) {
+        const float alpha = fast_exp2(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) st.o[t] *= alpha;
+        st.m = m_new;
+    }
+    // P in [0, 1] scaled by 2^8: hi carries 2^-8, lo 2^-12 in the scale operand
+    int ph[8], pl[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        ph[i] = 0;
+        pl[i] = 0;
+    }
+    float psum = 0.f;
+#pragma unroll
+    for (int i = 0; i < PP; ++i) {
+        float p[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            p[r] = fast_exp2(x[4 * i + r] - st.m);
+            psum += p[r];
+            p[r] *= 256.f;
+        }
+        uint32_t h, l;
+        split4(p, h, l);
+        ph[i] = (int)h;
+        pl[i] = (int)l;
+    }
+    st.l += psum;
+    if constexpr (PP == 4) {
+        // Lane group qg holds dword i = slots 4qg..4qg+3 of page i; V rows are
+        // held by page (lane group qg: page qg, dword j = slots 4j..4j+3), so P
+        // is transposed over the four lane groups: two 32-lane and two 16-lane
+        // swaps per operand.
+        transpose4(ph);
+        transpose4(pl);
+        const i32x8 bph = {ph[0], ph[1], ph[2], ph[3], 0, 0, 0, 0};
+        const i32x8 bpl = {pl[0], pl[1], pl[2], pl[3], 0, 0, 0, 0};
+        // codes of slots >= nv are zeroed (a tail slot may hold any byte)
+        const int nvl = qg == 0 ? nv[0] : qg == 1 ? nv[1] : qg == 2 ? nv[2] : nv[3];
+        uint32_t mk[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k = nvl - 4 * j;
+            mk[j] = k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const i32x8 av = {(int)(vx[0].v[t] & mk[0]), (int)(vx[1].v[t] & mk[1]),
+                              (int)(vx[2].v[t] & mk[2]), (int)(vx[3].v[t] & mk[3]), 0, 0, 0, 0};
+            st.o[t] = mfma_f8(av, bph, st.o[t], kE8M0One - 8);
+            st.o[t] = mfma_f8(av, bpl, st.o[t], kE8M0One - 12);
+        }
+        return;
+    }
+    const i32x8 bph = {ph[0], ph[1], ph[2], ph[3], ph[4], ph[5], ph[6], ph[7]};
+    const i32x8 bpl = {pl[0], pl[1], pl[2], pl[3], pl[4], pl[5], pl[6], pl[7]};
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        int va[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) va[i] = 0;
+#pragma unroll
+        for (int i = 0; i < PP; ++i) {
+            uint32_t w = vx[i].v[t];
+            const int k = nv[i] - 4 * qg;  // live codes among this lane's four
+            w &= k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+            va[i] = (int)w;
+        }
+        const i32x8 av = {va[0], va[1], va[2], va[3], va[4], va[5], va[6], va[7]};
+        st.o[t] = mfma_f8(av, bph, st.o[t], kE8M0One - 8);
+        st.o[t] = mfma_f8(av, bpl, st.o[t], kE8M0One - 12);
+    }
+}
+
 // A position in a wave's stream: a step of `len` consecutive pages starting
 // at unit x, which is page p of request b, KV head g.  Wave-uniform.
 struct Cursor {
@@ -520,7 +743,10 @@ attn_mfma_kernel(AttnArgs a) {
     // neighbour, unused).  The lane-dependent address keeps this a vector
     // load, ordered with the page loads, instead of a scalar one.
     auto bt_load = [&](const Cursor& c) -> int {
-        const int i = PP == 1 ? (lane & 1) : (lane & (PP - 1));
+        // page i of the step sits in lane i, or in lane group i when fp8 V
+        // rows are read by page (each lane then addresses its own page)
+        constexpr bool kRows = FP8 && PP == 4;
+        const int i = kRows ? (lane >> 4) : PP == 1 ? (lane & 1) : (lane & (PP - 1));
         const int idx = min(c.p + i, (PP == 1 ? c.np : c.p + c.len) - 1);
         return a.block_table[(int64_t)c.b * a.bt_stride + idx];
     };
@@ -547,9 +773,10 @@ attn_mfma_kernel(AttnArgs a) {
     // A one-page step of a two-page stream re-reads its page (a cache hit).
     auto kv_load = [&](const Cursor& c, int btv, PageK<D, FP8> (&rk)[PP], PageV<D, FP8> (&rv)[PP], bool& bad) {
         bad = false;
+        constexpr bool kRows = FP8 && PP == 4;
 #pragma unroll
         for (int i = 0; i < PP; ++i) {
-            int pg = __builtin_amdgcn_readlane(btv, i);
+            int pg = __builtin_amdgcn_readlane(btv, kRows ? 16 * i : i);
             if ((unsigned)pg >= (unsigned)a.num_pages) {
                 pg = 0;
                 bad = true;
@@ -557,7 +784,12 @@ attn_mfma_kernel(AttnArgs a) {
             }
             const size_t off = (size_t)pg * page_stride + (size_t)c.g * tile_bytes;
             load_k<D, FP8>(rk[i], (const char*)a.k_pages + off, qg, n);
-            load_v<D, FP8>(rv[i], (const char*)a.v_pages + off, qg, n);
+            if constexpr (!kRows) load_v<D, FP8>(rv[i], (const char*)a.v_pages + off, qg, n);
+        }
+        if constexpr (kRows) {
+            // this lane's page (lane group qg), invalid entries read page 0 as above
+            const int pl = (unsigned)btv < (unsigned)a.num_pages ? btv : 0;
+            load_v_rows<D>(rv, (const char*)a.v_pages + (size_t)pl * page_stride + (size_t)c.g * tile_bytes, n);
         }
     };
 
@@ -614,15 +846,23 @@ attn_mfma_kernel(AttnArgs a) {
     bf16x8 qb[DEPTH + 1][KS];
     float scb[DEPTH + 1];
     bool badb[DEPTH + 1];
+    // All block-table entries of the prologue go out before its pages: the
+    // loop's first wait for btn then leaves as many loads in flight as every
+    // later one (the counter is in order, and the wait is shared by all
+    // iterations of the loop).
+    int bts[DEPTH + 1];
+#pragma unroll
+    for (int j = 0; j <= DEPTH; ++j) bts[j] = bt_load(cur[j]);
 #pragma unroll
     for (int j = 0; j < DEPTH; ++j) {
-        const int btj = bt_load(cur[j]);
         q_load(cur[j], qb[j]);
         scb[j] = 0.f;
         if constexpr (FP8) scb[j] = scale_load(cur[j]);
-        kv_load(cur[j], btj, kb[j], vb[j], badb[j]);
+        kv_load(cur[j], bts[j], kb[j], vb[j], badb[j]);
     }
-    int btn = bt_load(cur[DEPTH]);
+    int btn = bts[DEPTH];
+    Q8 q8;                 // fp8 only: query rows of (q8_b, q8_g) as fp8 operands
+    int q8_b = -1, q8_g = -1;
 
     auto step = [&](auto slot) -> bool {
         constexpr int sc_ = decltype(slot)::value;                // slot computed now
@@ -640,7 +880,17 @@ attn_mfma_kernel(AttnArgs a) {
             vs = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(scb[sc_]), 32));
         }
         seg_bad = seg_bad || badb[sc_];
-        if constexpr (PP == 1) {
+        if constexpr (FP8) {
+            if (C.b != q8_b || C.g != q8_g) {  // new (request, head): convert its query rows
+                q_to_fp8<D>(qb[sc_], q8);
+                q8_b = C.b;
+                q8_g = C.g;
+            }
+            int nv[PP];
+#pragma unroll
+            for (int i = 0; i < PP; ++i) nv[i] = (i == 0 || C.len > i) ? min(kPage, C.L - (C.p + i) * kPage) : 0;
+            fp8_step<D, PP>(st, kb[sc_], vb[sc_], q8, sl, nv, qg);
+        } else if constexpr (PP == 1) {
             const f32x4 s4 = page_scores<D, FP8>(kb[sc_][0], qb[sc_]);
             page_pv<D, FP8>(st, s4, vb[sc_][0], sl, min(kPage, C.L - C.p * kPage), qg);
         } else {
