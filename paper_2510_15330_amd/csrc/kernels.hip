@@ -333,6 +333,27 @@ __device__ __forceinline__ u32x2 v_quad(const PageV<D, FP8>& r, int t, int nv, i
     return vv;
 }
 
+// Reductions over the four 16-lane groups (lanes n, n+16, n+32, n+48): a
+// 16-lane swap pairs groups 0/1 and 2/3, a 32-lane swap pairs the halves.
+// Both are plain VALU permutes, off the LDS path a lane shuffle would take;
+// every lane of a column ends with the same bits.
+__device__ __forceinline__ float group_max4(float x) {
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const unsigned v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group_sum4(float x) {
+    const unsigned u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const unsigned v = __float_as_uint(y);
+    const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 template <int D>
 struct AttnState {
     f32x4 o[D / 16];
@@ -357,8 +378,7 @@ __device__ __forceinline__ void page_pv(AttnState<D>& st, f32x4 sc, const PageV<
         x[i] = (4 * qg + i < nv) ? sc[i] * sl : -INFINITY;
         mx = fmaxf(mx, x[i]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = group_max4(mx);
     const float m_new = fmaxf(st.m, mx);
     if (__any(m_new > st.m)) {
         const float alpha = fast_exp2(st.m - m_new);
@@ -404,8 +424,7 @@ __device__ __forceinline__ void group_pv(AttnState<D>& st, const f32x4 (&sc)[PP]
             x[4 * i + r] = (4 * qg + r < nv[i]) ? sc[i][r] * sl : -INFINITY;
             mx = fmaxf(mx, x[4 * i + r]);
         }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = group_max4(mx);
     const float m_new = fmaxf(st.m, mx);
     if (__any(m_new > st.m)) {
         const float alpha = fast_exp2(st.m - m_new);
@@ -500,8 +519,7 @@ __device__ __forceinline__ void q_to_fp8(const bf16x8 (&bq)[D / 32], Q8& q8) {
     float amax = 0.f;
 #pragma unroll
     for (int i = 0; i < NV; ++i) amax = fmaxf(amax, fabsf(v[i]));
-    amax = fmaxf(amax, __shfl_xor(amax, 16));
-    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    amax = group_max4(amax);
     // 2^e <= amax < 2^(e+1); scale by 2^(7-e); keep the E8M0 exponents in range
     int e = amax > 0.f ? (int)((__float_as_uint(amax) >> 23) & 0xffu) - 127 : 0;
     int k = 7 - e;
@@ -569,8 +587,7 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
             mx = fmaxf(mx, x[4 * i + r]);
         }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    mx = group_max4(mx);
     const float m_new = fmaxf(st.m, mx);
     if (__any(m_new > st.m)) {
         const float alpha = fast_exp2(st.m - m_new);
@@ -647,6 +664,28 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
         st.o[t] = mfma_f8(av, bpl, st.o[t], kE8M0One - 12);
     }
 }
+
+// Mark loaded registers as read.  A step reads some of its loads only on some
+// paths (the query only at a segment change, the second page only when the
+// step has one); a register whose load was never waited for on the path taken
+// counts as still in flight when a later step reuses it, and the vector-memory
+// counter is in order, so that later wait would drain every load issued
+// before it.  Reading the whole slot once, after the next slot's loads are
+// out, settles all of them together.
+__device__ __forceinline__ void consume(const u32x4& x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void consume(const u32x2& x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void consume(uint32_t x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void consume(float x) { asm volatile("" ::"v"(x)); }
+__device__ __forceinline__ void consume(const bf16x8& x) { consume(__builtin_bit_cast(u32x4, x)); }
+template <typename T, int N>
+__device__ __forceinline__ void consume(const T (&x)[N]) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) consume(x[i]);
+}
+template <int D, bool FP8>
+__device__ __forceinline__ void consume(const PageK<D, FP8>& r) { consume(r.k); }
+template <int D, bool FP8>
+__device__ __forceinline__ void consume(const PageV<D, FP8>& r) { consume(r.v); }
 
 // A position in a wave's stream: a step of `len` consecutive pages starting
 // at unit x, which is page p of request b, KV head g.  Wave-uniform.
@@ -806,8 +845,7 @@ attn_mfma_kernel(AttnArgs a) {
     // Write the finished piece of C's (request, head): the whole output if the
     // request's head lies entirely in this wave's range, else a partial.
     auto finish = [&](const Cursor& c, float vs) {
-        float l_tot = st.l + __shfl_xor(st.l, 16);
-        l_tot += __shfl_xor(l_tot, 32);
+        const float l_tot = group_sum4(st.l);
         const int seg_x0 = c.x - c.p;
         const bool whole = seg_x0 >= r0 && seg_x0 + c.np <= r1;
         if (hv) {
@@ -864,7 +902,7 @@ attn_mfma_kernel(AttnArgs a) {
     Q8 q8;                 // fp8 only: query rows of (q8_b, q8_g) as fp8 operands
     int q8_b = -1, q8_g = -1;
 
-    auto step = [&](auto slot) -> bool {
+    auto step = [&](auto slot) {
         constexpr int sc_ = decltype(slot)::value;                // slot computed now
         constexpr int ld_ = (sc_ + DEPTH) % (DEPTH + 1);          // slot loaded now
         const int btT = bt_load(cur[DEPTH + 1]);
@@ -872,6 +910,7 @@ attn_mfma_kernel(AttnArgs a) {
         if constexpr (FP8) scb[ld_] = scale_load(cur[DEPTH]);
         kv_load(cur[DEPTH], btn, kb[ld_], vb[ld_], badb[ld_]);
         btn = btT;
+        if constexpr (FP8 && DEPTH > 1) consume(qb[sc_]);
 
         const Cursor& C = cur[0];
         float sl = a.scale_log2, vs = 1.f;
@@ -898,31 +937,31 @@ attn_mfma_kernel(AttnArgs a) {
             int nv[PP];
 #pragma unroll
             for (int i = 0; i < PP; ++i) {
-                sc4[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-                nv[i] = 0;
-                if (i == 0 || C.len > i) {
-                    sc4[i] = page_scores<D, FP8>(kb[sc_][i], qb[sc_]);
-                    nv[i] = min(kPage, C.L - (C.p + i) * kPage);
-                }
+                // pages past the step's end hold a valid page of the request
+                // (the block-table read is clamped); all their slots are masked
+                sc4[i] = page_scores<D, FP8>(kb[sc_][i], qb[sc_]);
+                nv[i] = (i == 0 || C.len > i) ? min(kPage, C.L - (C.p + i) * kPage) : 0;
             }
             group_pv<D, FP8, PP>(st, sc4, vb[sc_], sl, nv, qg);
         }
-        if (C.p + C.len >= C.np || C.x + C.len >= r1) finish(C, vs);
+        if (C.live && (C.p + C.len >= C.np || C.x + C.len >= r1)) finish(C, vs);
 #pragma unroll
         for (int j = 0; j < DEPTH + 1; ++j) cur[j] = cur[j + 1];
         cursor_next<PP>(cur[DEPTH + 1], a, r1);
-        return cur[0].live;
     };
 
+    // One exit, after a whole round of DEPTH + 1 steps.  An exit between
+    // steps would leave that step's prefetches in flight on an edge that the
+    // compiler joins with the continuing edge ahead of the loop header, and
+    // the header would then wait for every load in flight on each iteration.
+    // The last round may run up to DEPTH steps past the range: their cursors
+    // are dead (re-reading the last pages of the range, writing nothing).
     for (;;) {
-        if (!step(std::integral_constant<int, 0>{})) break;
-        if (!step(std::integral_constant<int, 1>{})) break;
-        if constexpr (DEPTH >= 2) {
-            if (!step(std::integral_constant<int, 2>{})) break;
-        }
-        if constexpr (DEPTH >= 3) {
-            if (!step(std::integral_constant<int, 3>{})) break;
-        }
+        step(std::integral_constant<int, 0>{});
+        step(std::integral_constant<int, 1>{});
+        if constexpr (DEPTH >= 2) step(std::integral_constant<int, 2>{});
+        if constexpr (DEPTH >= 3) step(std::integral_constant<int, 3>{});
+        if (!cur[0].live) break;
     }
     if (bad_pages) atomicOr(&a.hdr->err_flags, kErrPage);
 }
