@@ -213,6 +213,124 @@ int32_t bellman_length_cap(const bellman_load_signal_t *load_signal);
  * (fractional rank p/100 * (n - 1)).  Host arrays; n >= 1. */
 int bellman_calibrate_thresholds(const double *tbt, int64_t n, double *t1, double *t2);
 
+/* ------------------------------------------- closed-loop serving model --
+ * A discrete-event model of the paper's evaluation (Sec. 4, "Setup and
+ * trace", "Default unbounded run", "beLLMan in action"): requests arrive
+ * (caller-supplied times and sizes), wait in a FIFO queue, are admitted into a
+ * continuously batched server with paged KV memory, chunked prefill and
+ * preemption by recomputation (the behaviour of the vLLM scheduler the paper
+ * serves with), decode one token per iteration until they reach their target
+ * length, and the controller above sees the per-second average time between
+ * tokens (TBT) and caps the targets of newly queued requests.  Host
+ * arithmetic in integer nanoseconds; each iteration, in this order:
+ *  1. Ticks (k * tick_ns) and arrivals up to the current time, in time order,
+ *     a tick first on ties.  A tick averages the TBT samples of the tokens
+ *     decoded in ((k-1) tick_ns, k tick_ns] and pushes the average to the
+ *     controller (nothing for a second without samples).  An arrival is
+ *     queued with target N = bellman_length_cap(L) under the current rate
+ *     (N = L without a controller).
+ *  2. First-come first-served admission while fewer than max_running run: the
+ *     queue head must prefill P = prompt + generated tokens (generated > 0
+ *     after a preemption) and is admitted if ceil(P / 16) pages can be taken
+ *     leaving watermark_pages free.
+ *  3. With nothing running, time jumps to the next arrival.
+ *  4. In running order, a decoding request whose next KV position
+ *     (prompt + generated - 1) lies past its pages takes one more page; with
+ *     none free, the most recently admitted running requests are preempted
+ *     (pages returned, prefill progress dropped, back at the queue head,
+ *     earlier-admitted first) until one is, or the request itself was.
+ *  5. In running order, prefilling requests take up to the remaining
+ *     prefill_chunk_tokens of this iteration (no limit when 0).
+ *  6. Duration = fixed_ns + attention time + prefill time: the model takes
+ *     (attn_ps_per_token * KV + prefill_ps_per_token * chunk) / 1000 with KV
+ *     the decoding requests' summed prompt + generated tokens; live mode
+ *     replaces the attention term by the measured time of the real
+ *     bellman_kv_append + bellman_decode_attention on the decoding requests
+ *     times live_layers (and adds prefill_ps_per_token * chunk / 1000).
+ *  7. Decoding requests gain a token and one TBT sample each (the duration);
+ *     a request that completed its prefill gains a token (the first one fixes
+ *     its TTFT) and starts decoding; one that reaches N finishes and frees
+ *     its pages.  Running order is kept.
+ */
+typedef enum bellman_sim_controller_kind {
+    BELLMAN_SIM_NO_CONTROL = 0,   /* targets = predicted lengths */
+    BELLMAN_SIM_LINEAR = 1        /* the paper's linear controller (t1, t2, window, r_min, r_max) */
+} bellman_sim_controller_kind_t;
+
+typedef struct bellman_sim_config {
+    int32_t max_running;          /* >= 1 requests in the running batch (prefilling or decoding) */
+    int32_t controller;           /* bellman_sim_controller_kind_t */
+    int64_t kv_capacity_pages;    /* KV budget in 16-token pages */
+    int64_t watermark_pages;      /* pages admission leaves free (>= 0) */
+    int64_t fixed_ns;             /* per-iteration time of everything but attention and prefill */
+    int64_t attn_ps_per_token;    /* model mode: attention picoseconds per attended KV token */
+    int64_t prefill_ps_per_token; /* picoseconds per prefilled token */
+    int64_t tick_ns;              /* controller period (paper: 1 s) */
+    double t1, t2;                /* controller thresholds, nanoseconds of TBT */
+    int32_t window;               /* controller moving-average length (paper: 5) */
+    int32_t prefill_chunk_tokens; /* prefill tokens per iteration, 0 = unlimited */
+    double r_min, r_max;          /* controller rate range (paper: 0.05, 0.20) */
+    int32_t live;                 /* 0: model; 1: time the real kernels on the current device */
+    int32_t live_layers;          /* live: model layers one measured attention layer stands for */
+    int32_t live_q_heads;         /* live: per-GPU query heads of the measured layer */
+    int32_t live_kv_heads;        /* live: per-GPU KV heads (bf16 pools, 16-token pages) */
+    int32_t live_head_dim;        /* live: 64 or 128 */
+    int32_t reserved;             /* 0 */
+    void *stream;                 /* live: hipStream_t for the kernels (NULL = null stream) */
+} bellman_sim_config_t;
+
+typedef struct bellman_sim_request {
+    int64_t admit_ns;             /* first admission (prefill start) */
+    int64_t first_ns;             /* first token */
+    int64_t finish_ns;            /* last token */
+    int32_t target;               /* N, tokens */
+    int32_t preemptions;          /* times the request was preempted */
+    double r_at_queue;            /* controller rate when the request arrived */
+} bellman_sim_request_t;
+
+typedef struct bellman_sim_tick {
+    int64_t t_ns;                 /* tick time */
+    int64_t tokens;               /* TBT samples in the tick's second */
+    int64_t tbt_sum_ns;           /* their sum */
+    double r;                     /* controller rate after the tick */
+    int32_t queued;               /* queue length when the tick was taken */
+    int32_t running;              /* running requests when the tick was taken */
+} bellman_sim_tick_t;
+
+typedef struct bellman_sim_iteration {
+    int64_t end_ns;               /* iteration end */
+    int64_t dt_ns;                /* its duration */
+    int32_t decoding;             /* requests that decoded a token (TBT samples) */
+    int32_t chunk;                /* prefill tokens processed */
+    int32_t running;              /* running requests at the start of step 4 */
+    int32_t queued;               /* queue length at the start of step 4 */
+} bellman_sim_iteration_t;
+
+typedef struct bellman_sim_stats {
+    int64_t iterations;
+    int64_t ticks;                /* ticks taken (only the first max_ticks are stored) */
+    int64_t end_ns;               /* time the last request finished */
+    int64_t preemptions;          /* total preemptions */
+    double live_gpu_ms;           /* live: summed measured append + attention time */
+    int64_t live_kv_bytes;        /* live: K/V bytes the measured attention launches read */
+} bellman_sim_stats_t;
+
+/* Run the model over n requests (host arrays: arrival_ns non-decreasing and
+ * >= 0, prompt >= 1 and length >= 1 tokens, ceil((prompt + length) / 16) +
+ * watermark_pages <= kv_capacity_pages).  Writes requests[n], the first
+ * max_ticks ticks, the first max_iterations iteration records (iterations may
+ * be NULL when max_iterations is 0) and *stats (host memory, caller-owned).  Live mode
+ * allocates its own device buffers (KV pools of kv_capacity_pages pages,
+ * block table, lengths, query and new-token rows), synchronises the stream
+ * once per iteration to read the kernel time, and frees them before
+ * returning.  Returns 0 or a negative status (bad configuration or arrays,
+ * HIP failure, device error flags raised by the live kernels). */
+int bellman_sim_run(const bellman_sim_config_t *cfg, int64_t n, const int64_t *arrival_ns,
+                    const int32_t *prompt, const int32_t *length,
+                    bellman_sim_request_t *requests, bellman_sim_tick_t *ticks,
+                    int64_t max_ticks, bellman_sim_iteration_t *iterations,
+                    int64_t max_iterations, bellman_sim_stats_t *stats);
+
 /* ----------------------------------------------------------------- misc -- */
 
 /* Text of the last error raised on the calling thread ("" if none). */

@@ -8,6 +8,8 @@ the GPU library (``paper_2510_15330_amd``) and never imports it.
   built by gcc into ``liboracle.so`` and called through ctypes.
 * ``controller.py`` — the paper's linear length controller (Sec. 3,
   "Placeholder for congestion control", "beLLMan in action"), in plain Python.
+* ``serve_sim.py`` — the closed-loop serving model (Sec. 4), an event loop in
+  plain Python.
 """
 from __future__ import annotations
 

@@ -231,6 +231,16 @@ int launch_status(const char* what) {
 
 }  // namespace
 
+namespace bellman {
+int set_error(int code, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+}  // namespace bellman
+
 // ================================================================== ABI ====
 
 extern "C" {

@@ -74,4 +74,8 @@ void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 
+// Record the calling thread's last-error text (bellman_last_error) and
+// return `code`; shared by the host-side parts of the library.
+int set_error(int code, const char* fmt, ...);
+
 }  // namespace bellman
