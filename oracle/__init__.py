@@ -4,8 +4,9 @@ TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
 benchmark's CPU-baseline leg may import this package.  It shares no code with
 the GPU library (``paper_2510_15330_amd``) and never imports it.
 
-* ``oracle.c`` — binary64 paged decode attention and the byte-exact KV append,
-  built by gcc into ``liboracle.so`` and called through ctypes.
+* ``oracle.c`` — binary64 paged decode and prompt (prefill) attention, the
+  byte-exact KV append and prompt write, built by gcc into ``liboracle.so``
+  and called through ctypes.
 * ``controller.py`` — the paper's linear length controller (Sec. 3,
   "Placeholder for congestion control", "beLLMan in action"), in plain Python.
 * ``serve_sim.py`` — the closed-loop serving model (Sec. 4), an event loop in
@@ -66,6 +67,11 @@ def _bind(lib):
     lib.oracle_decode_attention.restype = i32
     lib.oracle_kv_append.argtypes = [i32, i32, i32, i32, i32, P, P, P, P, i64, P, P, P, i32, P]
     lib.oracle_kv_append.restype = i32
+    lib.oracle_prefill_attention.argtypes = [
+        i32, i32, i32, i32, i32, P, P, P, i64, P, P, P, i32, P, P, ctypes.c_float, P]
+    lib.oracle_prefill_attention.restype = i32
+    lib.oracle_kv_write.argtypes = [i32, i32, i32, i32, P, P, P, P, i64, P, i32, P, P]
+    lib.oracle_kv_write.restype = i32
     lib.oracle_quantize_e4m3fn.argtypes = [ctypes.c_float, ctypes.c_float]
     lib.oracle_quantize_e4m3fn.restype = ctypes.c_uint8
     lib.oracle_num_threads.argtypes = []
@@ -160,3 +166,57 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens,
                               _ptr(block_table), block_table.shape[1], _ptr(seq_lens))
     if rc != 0:
         raise ValueError(f"oracle_kv_append failed: {rc}")
+
+
+def prefill_attention(q_bits, k_pages, v_pages, block_table, seq_lens, q_start, scale,
+                      kv_dtype=BF16, k_scale=None, v_scale=None, lib=None):
+    """Binary64 causal prompt attention over the paged layout.
+
+    q_bits   uint16 [T, H_q, D]; q_start int32 [B + 1] (q_start[0] = 0,
+    q_start[B] = T): request b's query tokens are the last
+    n_b = q_start[b+1] - q_start[b] of its seq_lens[b] cached tokens, and
+    each attends every cached token up to its own position.
+    Returns float64 [T, H_q, D].
+    """
+    lib = lib or load()
+    q_bits = _c(q_bits, np.uint16)
+    code = np.uint16 if kv_dtype == BF16 else np.uint8
+    k_pages = _c(k_pages, code)
+    v_pages = _c(v_pages, code)
+    block_table = _c(block_table, np.int32)
+    seq_lens = _c(seq_lens, np.int32)
+    q_start = _c(q_start, np.int32)
+    T, H_q, D = q_bits.shape
+    B = len(seq_lens)
+    NP, H_kv = k_pages.shape[0], k_pages.shape[1]
+    if kv_dtype == FP8_E4M3FN:
+        k_scale = _c(k_scale, np.float32)
+        v_scale = _c(v_scale, np.float32)
+    out = np.empty((T, H_q, D), dtype=np.float64)
+    rc = lib.oracle_prefill_attention(
+        B, H_q, H_kv, D, kv_dtype, _ptr(q_bits), _ptr(k_pages), _ptr(v_pages), NP,
+        _ptr(k_scale), _ptr(v_scale), _ptr(block_table), block_table.shape[1],
+        _ptr(seq_lens), _ptr(q_start), float(scale), _ptr(out))
+    if rc != 0:
+        raise ValueError(f"oracle_prefill_attention failed: {rc}")
+    return out
+
+
+def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, kv_dtype=BF16, lib=None):
+    """Prompt write on host copies; mutates k_pages, v_pages, seq_lens.
+    k_new / v_new [T, H_kv, D] in the pools' element type (uint16 / uint8)."""
+    lib = lib or load()
+    code = np.uint16 if kv_dtype == BF16 else np.uint8
+    for a in (k_pages, v_pages, seq_lens):
+        assert a.flags.c_contiguous
+    k_new = _c(k_new, code)
+    v_new = _c(v_new, code)
+    assert k_pages.dtype == code and v_pages.dtype == code and seq_lens.dtype == np.int32
+    block_table = _c(block_table, np.int32)
+    q_start = _c(q_start, np.int32)
+    T, H_kv, D = k_new.shape
+    rc = lib.oracle_kv_write(len(seq_lens), H_kv, D, kv_dtype, _ptr(k_new), _ptr(v_new), _ptr(k_pages),
+                             _ptr(v_pages), k_pages.shape[0], _ptr(block_table), block_table.shape[1],
+                             _ptr(seq_lens), _ptr(q_start))
+    if rc != 0:
+        raise ValueError(f"oracle_kv_write failed: {rc}")

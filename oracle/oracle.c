@@ -105,17 +105,66 @@ static int64_t v_offset(int64_t page, int g, int slot, int d, int H_kv, int D)
  * A request with length 0 gets an all-zero output row.
  * Returns 0, or -1 when a used block-table entry or a length is out of range.
  */
-int oracle_decode_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
-                            const uint16_t *q,
-                            const void *k_pages, const void *v_pages, int64_t num_pages,
-                            const float *k_scale, const float *v_scale,
-                            const int32_t *block_table, int max_pages,
-                            const int32_t *seq_lens, float scale, double *out)
+/* One query row against the first L tokens of request b's KV head g: the
+ * definition above, into o[0..D).  Returns 0, or -2 if out of memory. */
+static int attend(const uint16_t *qrow, int b, int g, int L, int H_kv, int D, int kv_dtype,
+                  const void *k_pages, const void *v_pages, double ks, double vs,
+                  const int32_t *block_table, int max_pages, float scale, double *o)
 {
-    const int G = H_q / H_kv;
     const int x = 16 / elem_bytes(kv_dtype);
-    int bad = 0;
+    double *s;
+    double m, Z;
 
+    for (int d = 0; d < D; ++d)
+        o[d] = 0.0;
+    if (L == 0)
+        return 0;
+    s = (double *)malloc(sizeof(double) * (size_t)L);
+    if (!s)
+        return -2;
+
+    /* scores */
+    for (int t = 0; t < L; ++t) {
+        int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
+        int slot = t % ORACLE_PAGE;
+        double dot = 0.0;
+        for (int d = 0; d < D; ++d) {
+            double kv = load_code(k_pages, k_offset(pg, g, slot, d, H_kv, D, x), kv_dtype) * ks;
+            dot += oracle_bf16_to_f64(qrow[d]) * kv;
+        }
+        s[t] = (double)scale * dot;
+    }
+
+    /* softmax weights */
+    m = s[0];
+    for (int t = 1; t < L; ++t)
+        if (s[t] > m)
+            m = s[t];
+    Z = 0.0;
+    for (int t = 0; t < L; ++t) {
+        s[t] = exp(s[t] - m);
+        Z += s[t];
+    }
+
+    /* weighted sum of values */
+    for (int t = 0; t < L; ++t) {
+        int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
+        int slot = t % ORACLE_PAGE;
+        double w = s[t] / Z;
+        for (int d = 0; d < D; ++d) {
+            double vv = load_code(v_pages, v_offset(pg, g, slot, d, H_kv, D), kv_dtype) * vs;
+            o[d] += w * vv;
+        }
+    }
+    free(s);
+    return 0;
+}
+
+/* Every used block-table entry of every request lies in the pool, and the
+ * lengths fit the table. */
+static int check_table(int B, const int32_t *seq_lens, const int32_t *block_table, int max_pages,
+                       int64_t num_pages)
+{
     for (int b = 0; b < B; ++b) {
         int L = seq_lens[b];
         if (L < 0 || L > max_pages * ORACLE_PAGE)
@@ -126,76 +175,91 @@ int oracle_decode_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
                 return -1;
         }
     }
+    return 0;
+}
+
+int oracle_decode_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
+                            const uint16_t *q,
+                            const void *k_pages, const void *v_pages, int64_t num_pages,
+                            const float *k_scale, const float *v_scale,
+                            const int32_t *block_table, int max_pages,
+                            const int32_t *seq_lens, float scale, double *out)
+{
+    const int G = H_q / H_kv;
+    int bad = 0;
+
+    if (check_table(B, seq_lens, block_table, max_pages, num_pages))
+        return -1;
 
 #pragma omp parallel for collapse(2) schedule(dynamic)
     for (int b = 0; b < B; ++b) {
         for (int h = 0; h < H_q; ++h) {
             const int g = h / G;
-            const int L = seq_lens[b];
-            double *o = out + ((int64_t)b * H_q + h) * D;
-            const uint16_t *qrow = q + ((int64_t)b * H_q + h) * D;
             double ks = 1.0, vs = 1.0;
-            double *s;
-            double m, Z;
-
-            for (int d = 0; d < D; ++d)
-                o[d] = 0.0;
-            if (L == 0)
-                continue;
             if (kv_dtype == ORACLE_FP8_E4M3FN) {
                 ks = (double)k_scale[(int64_t)b * H_kv + g];
                 vs = (double)v_scale[(int64_t)b * H_kv + g];
             }
-            s = (double *)malloc(sizeof(double) * (size_t)L);
-            if (!s) {
+            if (attend(q + ((int64_t)b * H_q + h) * D, b, g, seq_lens[b], H_kv, D, kv_dtype, k_pages, v_pages,
+                       ks, vs, block_table, max_pages, scale, out + ((int64_t)b * H_q + h) * D))
                 bad = 1;
-                continue;
-            }
-
-            /* scores */
-            for (int t = 0; t < L; ++t) {
-                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
-                int slot = t % ORACLE_PAGE;
-                double dot = 0.0;
-                for (int d = 0; d < D; ++d) {
-                    double kv = load_code(k_pages, k_offset(pg, g, slot, d, H_kv, D, x), kv_dtype) * ks;
-                    dot += oracle_bf16_to_f64(qrow[d]) * kv;
-                }
-                s[t] = (double)scale * dot;
-            }
-
-            /* softmax weights */
-            m = s[0];
-            for (int t = 1; t < L; ++t)
-                if (s[t] > m)
-                    m = s[t];
-            Z = 0.0;
-            for (int t = 0; t < L; ++t) {
-                s[t] = exp(s[t] - m);
-                Z += s[t];
-            }
-
-            /* weighted sum of values */
-            for (int t = 0; t < L; ++t) {
-                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];
-                int slot = t % ORACLE_PAGE;
-                double w = s[t] / Z;
-                for (int d = 0; d < D; ++d) {
-                    double vv = load_code(v_pages, v_offset(pg, g, slot, d, H_kv, D), kv_dtype) * vs;
-                    o[d] += w * vv;
-                }
-            }
-            free(s);
         }
     }
     return bad ? -2 : 0;
 }
 
-/* Quantise one value to OCP e4m3fn: v = x / scale in binary32 (one correctly
- * rounded division), then round to the nearest e4m3fn value, ties to the
- * even mantissa, saturating to +-448; NaN stays NaN.  Written from the format
- * definition: normal values are (1 + m/8) 2^(e-7) for e in 1..15, m in 0..7
- * except e = 15, m = 7 (NaN); subnormals are (m/8) 2^-6. */
+/*
+ * Prefill (prompt) attention over the paged cache: request b contributes the
+ * query tokens q_start[b] .. q_start[b+1]-1, the last n_b of its L_b =
+ * seq_lens[b] tokens (their keys and values are already in the cache), and
+ * query token i, at position p = L_b - n_b + (i - q_start[b]), attends the
+ * tokens 0..p (causal self-attention, the prefill that produces a request's
+ * first output token).  That is the decode definition above applied to each
+ * query token with length p + 1.  q and out are [T, H_q, D] with T =
+ * q_start[B].  Returns 0, -1 for a malformed table, -2 if out of memory.
+ */
+int oracle_prefill_attention(int B, int H_q, int H_kv, int D, int kv_dtype,
+                             const uint16_t *q,
+                             const void *k_pages, const void *v_pages, int64_t num_pages,
+                             const float *k_scale, const float *v_scale,
+                             const int32_t *block_table, int max_pages,
+                             const int32_t *seq_lens, const int32_t *q_start, float scale, double *out)
+{
+    const int G = H_q / H_kv;
+    int bad = 0;
+    int64_t T;
+
+    if (check_table(B, seq_lens, block_table, max_pages, num_pages))
+        return -1;
+    if (q_start[0] != 0)
+        return -1;
+    for (int b = 0; b < B; ++b)
+        if (q_start[b + 1] < q_start[b] || q_start[b + 1] - q_start[b] > seq_lens[b])
+            return -1;
+    T = q_start[B];
+
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t i = 0; i < T; ++i) {
+        for (int h = 0; h < H_q; ++h) {
+            int b = 0;
+            while (q_start[b + 1] <= i)
+                ++b;
+            const int n = q_start[b + 1] - q_start[b];
+            const int p = seq_lens[b] - n + (int)(i - q_start[b]);
+            const int g = h / G;
+            double ks = 1.0, vs = 1.0;
+            if (kv_dtype == ORACLE_FP8_E4M3FN) {
+                ks = (double)k_scale[(int64_t)b * H_kv + g];
+                vs = (double)v_scale[(int64_t)b * H_kv + g];
+            }
+            if (attend(q + (i * H_q + h) * D, b, g, p + 1, H_kv, D, kv_dtype, k_pages, v_pages, ks, vs,
+                       block_table, max_pages, scale, out + (i * H_q + h) * D))
+                bad = 1;
+        }
+    }
+    return bad ? -2 : 0;
+}
+
 uint8_t oracle_quantize_e4m3fn(float x, float scale)
 {
     float v = x / scale;
@@ -285,6 +349,53 @@ int oracle_kv_append(int B, int H_kv, int D, int kv_dtype, int new_dtype,
             }
         }
         seq_lens[b] = L + 1;
+    }
+    return 0;
+}
+
+/*
+ * Write a prompt's keys and values into the paged cache: request b's tokens
+ * q_start[b] .. q_start[b+1]-1 of k_new / v_new ([T, H_kv, D], the pool's
+ * element type) go to positions seq_lens[b], seq_lens[b] + 1, ... (page
+ * block_table[b][pos / 16], slot pos % 16), byte for byte, and seq_lens[b]
+ * grows by their count.  Nothing else is written.  Returns 0 or -1.
+ */
+int oracle_kv_write(int B, int H_kv, int D, int kv_dtype, const void *k_new, const void *v_new,
+                    void *k_pages, void *v_pages, int64_t num_pages,
+                    const int32_t *block_table, int max_pages, int32_t *seq_lens, const int32_t *q_start)
+{
+    const int eb = elem_bytes(kv_dtype);
+    const int x = 16 / eb;
+
+    if (q_start[0] != 0)
+        return -1;
+    for (int b = 0; b < B; ++b) {
+        int L = seq_lens[b], n = q_start[b + 1] - q_start[b];
+        if (n < 0 || L < 0 || (n > 0 && (L + n - 1) / ORACLE_PAGE >= max_pages))
+            return -1;
+        for (int pos = L; pos < L + n; ++pos) {
+            int32_t pg = block_table[(int64_t)b * max_pages + pos / ORACLE_PAGE];
+            if (pg < 0 || pg >= num_pages)
+                return -1;
+        }
+    }
+    for (int b = 0; b < B; ++b) {
+        int L = seq_lens[b];
+        for (int64_t i = q_start[b]; i < q_start[b + 1]; ++i) {
+            int pos = L + (int)(i - q_start[b]);
+            int64_t pg = block_table[(int64_t)b * max_pages + pos / ORACLE_PAGE];
+            int slot = pos % ORACLE_PAGE;
+            for (int g = 0; g < H_kv; ++g) {
+                for (int d = 0; d < D; ++d) {
+                    int64_t src = (i * H_kv + g) * D + d;
+                    memcpy((char *)k_pages + k_offset(pg, g, slot, d, H_kv, D, x) * eb,
+                           (const char *)k_new + src * eb, (size_t)eb);
+                    memcpy((char *)v_pages + v_offset(pg, g, slot, d, H_kv, D) * eb,
+                           (const char *)v_new + src * eb, (size_t)eb);
+                }
+            }
+        }
+        seq_lens[b] = L + (q_start[b + 1] - q_start[b]);
     }
     return 0;
 }

@@ -348,11 +348,11 @@ def test_out_of_range_inputs_rejected(oracle_lib):
 
 MUTANTS = {
     "gqa head modulo": ("const int g = h / G;", "const int g = h % H_kv;"),
-    "drops last token": ("for (int t = 0; t < L; ++t) {\n                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];\n                int slot = t % ORACLE_PAGE;\n                double w",
-                         "for (int t = 0; t < L - 1; ++t) {\n                int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];\n                int slot = t % ORACLE_PAGE;\n                double w"),
+    "drops last token": ("for (int t = 0; t < L; ++t) {\n        int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];\n        int slot = t % ORACLE_PAGE;\n        double w",
+                         "for (int t = 0; t < L - 1; ++t) {\n        int64_t pg = block_table[(int64_t)b * max_pages + t / ORACLE_PAGE];\n        int slot = t % ORACLE_PAGE;\n        double w"),
     "scale ignored": ("s[t] = (double)scale * dot;", "s[t] = dot;"),
     "normalised by length": ("double w = s[t] / Z;", "double w = s[t] / L;"),
-    "max taken from first score": ("if (s[t] > m)\n                    m = s[t];", "if (s[t] > m)\n                    m = m;"),
+    "max taken from first score": ("if (s[t] > m)\n            m = s[t];", "if (s[t] > m)\n            m = m;"),
     "k chunk index transposed": ("return (chunk * ORACLE_PAGE + slot) * x + d % x;",
                                  "return (chunk * ORACLE_PAGE + (d % x) % ORACLE_PAGE) * x + slot % x;"),
     "v slot/dim swapped": ("return (tile * D + d) * ORACLE_PAGE + slot;",
@@ -382,7 +382,8 @@ def _all_pins(lib):
 def test_mutants_are_caught(name):
     src = open(ORACLE_C).read()
     old, new = MUTANTS[name]
-    assert src.count(old) == 1, f"mutation site for {name!r} not found exactly once"
+    # a site shared by the decode and prefill entry points is mutated in both
+    assert src.count(old) >= 1, f"mutation site for {name!r} not found"
     d = tempfile.mkdtemp()
     try:
         c = os.path.join(d, "m.c")
