@@ -8,6 +8,11 @@ U{6000..12000} + generated lognormal(median 500, sigma 0.5) clipped to 1500,
 50 steps); the same batch with beLLMan's per-request caps {100, 200, 400} is
 measured beside it.  Inputs are synthetic and resident in HBM before timing.
 
+``--workload prefill_summarization`` (or ``prefill_chunked``) measures the
+prompt path instead: the prompt write and causal prompt attention of four
+6-12k-token prompts (or their last 2048-token chunks), priced against the
+bf16 matrix-core peak.
+
 Prints one JSON line.  ``value`` is the algorithmic HBM traffic of the timed
 steps divided by their wall time (GB/s); ``roofline`` prices the attention
 kernel alone, timed with HIP events the library records around it;
@@ -28,6 +33,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
 METRIC = "decode-attention HBM GB/s (% of MI355X peak) + decode steps/sec at batch 256"
 KERNEL_SRC = os.path.join(ROOT, "paper_2510_15330_amd", "csrc", "kernels.hip")
 
@@ -163,6 +169,137 @@ def cpu_baseline(w, target_s=12.0, min_s=10.0):
     }
 
 
+def measure_prefill(name, steps, warmup, split_p=True, seed=0):
+    """Prompt path: a step restores the cached lengths (one small copy), writes
+    the batch's keys and values into their pages and runs causal prompt
+    attention over the cache."""
+    import torch
+
+    import paper_2510_15330_amd as bl
+    from paper_2510_15330_amd import workloads as wl
+
+    w = wl.build_prefill(name, seed=seed, device="cuda")
+    out = torch.empty((w.T, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    lens0 = w.seq_lens.clone()
+    stream = torch.cuda.current_stream()
+
+    def step(events=None):
+        w.seq_lens.copy_(lens0)
+        bl.kv_write(w.k_new, w.v_new, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, stream=stream)
+        bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
+                             stream=stream, split_p=split_p, events=events)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if bl.device_errors() != 0:
+        raise RuntimeError("device error flags set during warmup")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if bl.device_errors() != 0:
+        raise RuntimeError("device error flags set during the timed steps")
+    if not torch.isfinite(out.float()).all():
+        raise RuntimeError("non-finite prompt attention output")
+    kt = np.array([a.elapsed_time(b) for a, b in evs]) * 1e-3
+    wall = t1 - t0
+    return dict(w=w, wall=wall, kt=kt, flops=w.flops(), tflops=w.flops() * steps / wall / 1e12,
+                kernel_tflops=w.flops() / kt.mean() / 1e12)
+
+
+def cpu_baseline_prefill(w, target_s=12.0):
+    """The binary64 oracle on sampled query rows of the batch's first request
+    (each row as a one-token request ending at its position), timed on this
+    host; pools are copied to host memory first (not timed)."""
+    import torch
+
+    import oracle
+
+    lib = oracle.load()
+    kp = w.k_pages.cpu().view(torch.int16).numpy().view(np.uint16)
+    vp = w.v_pages.cpu().view(torch.int16).numpy().view(np.uint16)
+    bt0 = w.block_table[:1].cpu().numpy()
+    rng = np.random.default_rng(0)
+    n0 = int(w.new[0])
+
+    def run(k):
+        rows = np.sort(rng.integers(0, n0, size=k))
+        lens = (w.cached[0] + rows + 1).astype(np.int32)
+        qb = w.q[torch.from_numpy(rows).cuda()].cpu().view(torch.int16).numpy().view(np.uint16)
+        bt = np.repeat(bt0, k, axis=0)
+        t = time.perf_counter()
+        oracle.prefill_attention(qb, kp, vp, bt, lens, np.arange(k + 1, dtype=np.int32), w.scale, lib=lib)
+        return time.perf_counter() - t, int(lens.sum())
+
+    dt, _ = run(8)
+    k = int(max(8, 8 * target_s / max(dt, 1e-4)))
+    dt, keys = run(k)
+    flops = 4.0 * w.D * w.H_q * keys
+    return {
+        "value": round(flops / dt / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(oracle.num_threads(lib)),
+        "kind": "oracle",
+        "sample": f"binary64 oracle on {k} random query rows of request 0 ({n0} prompt tokens, all {w.H_q} "
+                  f"query heads; {keys} visible keys in all) in {dt:.1f} s",
+        "host_cpu": _cpu_model(),
+    }
+
+
+def main_prefill(args):
+    steps = args.steps if args.steps is not None else 20
+    log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
+    r = measure_prefill(args.workload, steps, args.warmup, split_p=not args.p_bf16)
+    w = r["w"]
+    log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['tflops']:.1f} TFLOP/s per step, "
+        f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_tflops']:.1f} TFLOP/s")
+    result = {
+        "metric": "prompt-attention TFLOP/s (causal prefill over the paged cache)",
+        "value": round(r["tflops"], 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(r["wall"] / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload, "requests": w.B, "tokens": w.T,
+            "cached": [int(x) for x in w.cached], "new": [int(x) for x in w.new],
+            "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
+            "p_precision": "bf16" if args.p_bf16 else "bf16 hi+lo", "seed": 0,
+        },
+        "attention_kernel_us": {
+            "mean": round(r["kt"].mean() * 1e6, 2),
+            "p50": round(float(np.percentile(r["kt"], 50)) * 1e6, 2),
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(r["kernel_tflops"], 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(r["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
+            "traffic": None,
+            "kernel": "prefill_attn_kernel (causal prompt attention, bf16 matrix cores)",
+            "flops_per_launch": int(r["flops"]),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline_prefill(w)
+    print(json.dumps(result), flush=True)
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -193,7 +330,10 @@ def main():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="summarization",
-                    choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8"])
+                    choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8",
+                             "prefill_summarization", "prefill_chunked"],
+                    help="decode batches, or prompt batches (prefill_*: the prompt write + prompt attention)")
+    ap.add_argument("--p-bf16", action="store_true", help="prompt attention: P rounded to bf16 once")
     ap.add_argument("--impl", default="auto", choices=["auto", "mfma", "valu"])
     ap.add_argument("--max-waves", type=int, default=0, help="cap on waves sharing the work (0 = all resident)")
     ap.add_argument("--pages-per-step", type=int, default=0, help="1, 2 (or 4 for fp8); 0 = library default")
@@ -229,6 +369,9 @@ def main():
         log(f"[bench] copied {n} bytes x3")
         return
     bl.library()
+    if args.workload.startswith("prefill_"):
+        main_prefill(args)
+        return
     impl = {"auto": bl.IMPL_AUTO, "mfma": bl.IMPL_MFMA, "valu": bl.IMPL_VALU}[args.impl]
     steps = args.steps if args.steps is not None else wl.CONFIGS[args.workload]["steps"]
 

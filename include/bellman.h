@@ -169,6 +169,69 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
                                   bellman_tensor_t *out, const bellman_attn_opts_t *opts,
                                   void *stream);
 
+/* ----------------------------------------------------------- prompt path --
+ * Before a request decodes, its prompt is prefilled (the step that sets the
+ * time to first token, Sec. 3 "Our key proposal"; Sec. 4 "Setup and trace"):
+ * the prompt's keys and values are written into its pages and every prompt
+ * token attends causally over the cache.  Both calls take a batch of
+ * requests whose new tokens are concatenated: q_start int32 [B + 1] (device,
+ * contiguous) with q_start[0] = 0 gives request b the token rows
+ * q_start[b] .. q_start[b+1]-1 (n_b = q_start[b+1] - q_start[b] >= 0).
+ * Requests may already hold cached tokens (chunked prefill).
+ */
+
+/* Write n_b new tokens per request at positions seq_lens[b] .. seq_lens[b] +
+ * n_b - 1 (page block_table[b][pos / 16], slot pos % 16), then set
+ * seq_lens[b] += n_b.
+ *   k_new, v_new  [T, H_kv, D] in the pools' element type, innermost
+ *                 contiguous (k_new rows 16-byte aligned); T = q_start[B].
+ *   k_pages, v_pages, block_table: as for bellman_kv_append; the pages of
+ *                 every new position must already be assigned.
+ *   seq_lens      int32 [B] contiguous (read, then advanced).
+ * Byte-exact copies; nothing else is written.  A token outside its
+ * request's table or the pool is skipped and flagged (flag 1), and that
+ * request's length is left unchanged when its last position does not fit. */
+int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_new,
+                     bellman_tensor_t *k_pages, bellman_tensor_t *v_pages,
+                     const bellman_tensor_t *block_table, bellman_tensor_t *seq_lens,
+                     const bellman_tensor_t *q_start, void *stream);
+
+/* Causal prompt attention over the paged cache: request b's query rows are
+ * its last n_b of L_b = seq_lens[b] cached tokens, and the row of token
+ * q_start[b] + i, at position p = L_b - n_b + i, gets
+ *   out[., h, :] = sum_{t <= p} softmax_t(scale * <q[., h, :], k_t>) * v_t
+ * (query head h reads KV head h / G).
+ *   q            bf16 [T, H_q, D], innermost contiguous, rows 16-byte aligned.
+ *   k_pages, v_pages  bf16 pools as for bellman_decode_attention (fp8 pools:
+ *                BELLMAN_ERR_UNSUPPORTED); D in {64, 128}; H_q a multiple of
+ *                H_kv.
+ *   block_table  int32 [B, maxP]; seq_lens int32 [B] (after the write).
+ *   out          bf16 [T, H_q, D] (written, rounded to nearest even); rows of
+ *                a malformed request (n_b > L_b, rows past T, L_b past the
+ *                table: flag 2) are not written; a q_start that decreases, starts below
+ *                0 or ends past T writes no row at all (flag 2).
+ * Each workgroup takes 128 query rows of one request and one query head;
+ * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo.  Scratch:
+ * B + 1 integers of the per-device workspace. */
+int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
+                              const bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
+                              const bellman_tensor_t *seq_lens, const bellman_tensor_t *q_start,
+                              float scale, bellman_tensor_t *out, void *stream);
+
+typedef struct bellman_prefill_opts {
+    int32_t split_p;      /* 1 (default): P as bf16 hi + lo; 0: P rounded to bf16 once */
+    int32_t reserved;     /* 0 */
+    void *event_begin;    /* optional hipEvent_t recorded before the attention kernels */
+    void *event_end;      /* optional hipEvent_t recorded after them */
+} bellman_prefill_opts_t;
+
+/* bellman_prefill_attention with options (NULL = defaults). */
+int bellman_prefill_attention_opts(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
+                                   const bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
+                                   const bellman_tensor_t *seq_lens, const bellman_tensor_t *q_start,
+                                   float scale, bellman_tensor_t *out,
+                                   const bellman_prefill_opts_t *opts, void *stream);
+
 /* ------------------------------------------------ output-length control --
  * The paper's linear congestion controller (Sec. 3: "Our key proposal",
  * "Placeholder for congestion control", "Default unbounded run", "beLLMan in
@@ -342,7 +405,8 @@ int bellman_reserve_workspace(int64_t bytes);
 
 /* Synchronise `stream`, copy the current device's error word to *flags and
  * clear it.  Bits: 1 = an append slot outside the block table or pool,
- * 2 = an attention length above maxP*16 (clamped), 4 = a block-table entry
+ * 2 = an attention length above maxP*16 (clamped) or a malformed prompt
+ * range, 4 = a block-table entry
  * outside the pool (page skipped). */
 int bellman_device_errors(void *stream, int32_t *flags);
 

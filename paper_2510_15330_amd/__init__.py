@@ -1,4 +1,5 @@
-"""MI355X (gfx950) paged decode attention with beLLMan's length controller.
+"""MI355X (gfx950) paged decode attention with beLLMan's length controller,
+and the prompt (prefill) path that fills the cache before decoding.
 
 The numerical work runs in ``libbellman.so`` (HIP kernels behind a C ABI,
 declared in ``include/bellman.h``); this package marshals torch tensors into
@@ -15,10 +16,12 @@ from ._binding import (  # noqa: F401
     decode_attention,
     device_errors,
     kv_append,
+    kv_write,
     last_error,
     length_cap,
     library,
     library_path,
+    prefill_attention,
     reserve_workspace,
     shutdown,
     version,

@@ -38,6 +38,11 @@ class AttnOpts(ctypes.Structure):
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
+class PrefillOpts(ctypes.Structure):
+    _fields_ = [("split_p", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
+
+
 class LoadSignal(ctypes.Structure):
     _fields_ = [
         ("controller", ctypes.c_void_p),
@@ -71,6 +76,13 @@ def library():
     lib.bellman_decode_attention_opts.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                   ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_opts.restype = ctypes.c_int
+    lib.bellman_kv_write.argtypes = [T, T, T, T, T, T, T, P]
+    lib.bellman_kv_write.restype = ctypes.c_int
+    lib.bellman_prefill_attention.argtypes = [T, T, T, T, T, T, ctypes.c_float, T, P]
+    lib.bellman_prefill_attention.restype = ctypes.c_int
+    lib.bellman_prefill_attention_opts.argtypes = [T, T, T, T, T, T, ctypes.c_float, T,
+                                                   ctypes.POINTER(PrefillOpts), P]
+    lib.bellman_prefill_attention_opts.restype = ctypes.c_int
     lib.bellman_controller_create.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_int32,
                                               ctypes.c_double, ctypes.c_double]
     lib.bellman_controller_create.restype = P
@@ -184,6 +196,34 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
                 raise ValueError("record each event once before passing it")
         opts = AttnOpts(int(max_waves), int(impl), int(pages_per_step), int(pipeline_depth), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
+
+
+def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, stream=None):
+    """bellman_kv_write: write each request's new prompt tokens after its
+    cached ones, then seq_lens += tokens written."""
+    _device_tensors(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start)
+    _check(library().bellman_kv_write(desc(k_new), desc(v_new), desc(k_pages), desc(v_pages), desc(block_table),
+                                      desc(seq_lens), desc(q_start), _stream(stream)))
+
+
+def prefill_attention(q, k_pages, v_pages, block_table, seq_lens, q_start, scale, out, stream=None,
+                      split_p=True, events=None):
+    """bellman_prefill_attention(_opts): causal attention of each request's
+    new (last) tokens over its cached ones."""
+    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, q_start, out)
+    lib = library()
+    args = (desc(q), desc(k_pages), desc(v_pages), desc(block_table), desc(seq_lens), desc(q_start),
+            ctypes.c_float(scale), desc(out))
+    if split_p and events is None:
+        _check(lib.bellman_prefill_attention(*args, _stream(stream)))
+        return
+    ev0 = ev1 = None
+    if events is not None:
+        ev0, ev1 = events[0].cuda_event, events[1].cuda_event
+        if not ev0 or not ev1:
+            raise ValueError("record each event once before passing it")
+    opts = PrefillOpts(int(bool(split_p)), 0, ev0, ev1)
+    _check(lib.bellman_prefill_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 
 def reserve_workspace(nbytes: int):

@@ -471,4 +471,143 @@ int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* 
     return bellman_decode_attention_opts(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream);
 }
 
+
+// ------------------------------------------------------------ prompt path --
+
+namespace {
+int check_q_start(const bellman_tensor_t* qs, int64_t B) {
+    int rc;
+    if ((rc = check_tensor(qs, "q_start", 1))) return rc;
+    if ((rc = check_dtype(qs, "q_start", BELLMAN_INT32))) return rc;
+    if (qs->shape[0] != B + 1)
+        return fail(BELLMAN_ERR_INVALID_ARG, "q_start: %lld entries for batch %lld (need B + 1)", (long long)qs->shape[0],
+                    (long long)B);
+    if (qs->shape[0] > 1 && qs->stride[0] != 1) return fail(BELLMAN_ERR_UNSUPPORTED, "q_start: must be contiguous");
+    return BELLMAN_OK;
+}
+}  // namespace
+
+int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_new, bellman_tensor_t* k_pages,
+                     bellman_tensor_t* v_pages, const bellman_tensor_t* block_table, bellman_tensor_t* seq_lens,
+                     const bellman_tensor_t* q_start, void* stream) {
+    g_last_error[0] = 0;
+    int rc;
+    PoolShape ps;
+    if ((rc = check_pools(k_pages, v_pages, &ps, false))) return rc;
+    if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
+    const int64_t T = k_new->shape[0];
+    const size_t eb = ps.fp8 ? 1 : 2;
+    if ((rc = check_rows(k_new, "k_new", k_pages->dtype, T, ps.H_kv, ps.D, 16))) return rc;
+    if ((rc = check_rows(v_new, "v_new", k_pages->dtype, T, ps.H_kv, ps.D, eb))) return rc;
+    if ((rc = check_seq_lens(seq_lens, seq_lens ? seq_lens->shape[0] : 0))) return rc;
+    const int64_t B = seq_lens->shape[0];
+    if ((rc = check_block_table(block_table, B))) return rc;
+    if ((rc = check_q_start(q_start, B))) return rc;
+    if (T > INT32_MAX || B > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "too many tokens or requests");
+    if (T == 0 || B == 0) return BELLMAN_OK;
+
+    int dev;
+    if ((rc = current_device(&dev))) return rc;
+    char* base;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+    WriteArgs a;
+    a.k_new = k_new->data;
+    a.v_new = v_new->data;
+    a.k_st = k_new->stride[0];
+    a.k_sh = k_new->stride[1];
+    a.v_st = v_new->stride[0];
+    a.v_sh = v_new->stride[1];
+    a.k_pages = k_pages->data;
+    a.v_pages = v_pages->data;
+    a.block_table = (const int32_t*)block_table->data;
+    a.bt_stride = block_table->shape[0] > 1 ? block_table->stride[0] : block_table->shape[1];
+    a.seq_lens = (int32_t*)seq_lens->data;
+    a.q_start = (const int32_t*)q_start->data;
+    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.num_pages = ps.num_pages;
+    a.B = (int)B;
+    a.T = (int)T;
+    a.H_kv = ps.H_kv;
+    a.D = ps.D;
+    a.max_pages = (int)block_table->shape[1];
+    a.elem_bytes = (int)eb;
+    launch_kv_write(a, (hipStream_t)stream);
+    return launch_status("kv_write");
+}
+
+int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
+                                   const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                                   const bellman_tensor_t* seq_lens, const bellman_tensor_t* q_start, float scale,
+                                   bellman_tensor_t* out, const bellman_prefill_opts_t* opts, void* stream) {
+    g_last_error[0] = 0;
+    int rc;
+    PoolShape ps;
+    if ((rc = check_pools(k_pages, v_pages, &ps, true))) return rc;
+    if (ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "prefill attention over fp8 pools is not implemented");
+    if ((rc = check_tensor(q, "q", 3))) return rc;
+    const int64_t T = q->shape[0];
+    const int64_t H_q = q->shape[1];
+    if ((rc = check_rows(q, "q", BELLMAN_BF16, T, H_q, ps.D, 16))) return rc;
+    if ((rc = check_rows(out, "out", BELLMAN_BF16, T, H_q, ps.D, 8))) return rc;
+    if ((rc = check_seq_lens(seq_lens, seq_lens ? seq_lens->shape[0] : 0))) return rc;
+    const int64_t B = seq_lens->shape[0];
+    if ((rc = check_block_table(block_table, B))) return rc;
+    if ((rc = check_q_start(q_start, B))) return rc;
+    if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
+    if (H_q < 1 || H_q % ps.H_kv != 0)
+        return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
+    if (H_q > 65535) return fail(BELLMAN_ERR_UNSUPPORTED, "more than 65535 query heads");
+    if (T > INT32_MAX / 2 || B > INT32_MAX / 2) return fail(BELLMAN_ERR_UNSUPPORTED, "too many tokens or requests");
+    if (T == 0 || B == 0) return BELLMAN_OK;
+
+    int dev;
+    if ((rc = current_device(&dev))) return rc;
+    char* base;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), &base))) return rc;
+    PrefillArgs a;
+    a.q = (const uint16_t*)q->data;
+    a.q_st = q->stride[0];
+    a.q_sh = q->stride[1];
+    a.k_pages = k_pages->data;
+    a.v_pages = v_pages->data;
+    a.block_table = (const int32_t*)block_table->data;
+    a.bt_stride = block_table->shape[0] > 1 ? block_table->stride[0] : block_table->shape[1];
+    a.seq_lens = (const int32_t*)seq_lens->data;
+    a.q_start = (const int32_t*)q_start->data;
+    a.out = (uint16_t*)out->data;
+    a.o_st = out->stride[0];
+    a.o_sh = out->stride[1];
+    a.num_pages = ps.num_pages;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.B = (int)B;
+    a.T = (int)T;
+    a.H_q = (int)H_q;
+    a.H_kv = ps.H_kv;
+    a.G = (int)(H_q / ps.H_kv);
+    a.D = ps.D;
+    a.max_pages = (int)block_table->shape[1];
+    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.tile_start = (int32_t*)(base + sizeof(WorkspaceHeader));
+    hipStream_t s = (hipStream_t)stream;
+    if (opts && opts->event_begin) {
+        hipError_t e = hipEventRecord((hipEvent_t)opts->event_begin, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    launch_prefill(a, opts ? opts->split_p != 0 : true, s);
+    if ((rc = launch_status("prefill_attention"))) return rc;
+    if (opts && opts->event_end) {
+        hipError_t e = hipEventRecord((hipEvent_t)opts->event_end, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    return BELLMAN_OK;
+}
+
+int bellman_prefill_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
+                              const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                              const bellman_tensor_t* seq_lens, const bellman_tensor_t* q_start, float scale,
+                              bellman_tensor_t* out, void* stream) {
+    return bellman_prefill_attention_opts(q, k_pages, v_pages, block_table, seq_lens, q_start, scale, out, nullptr,
+                                          stream);
+}
+
 }  // extern "C"

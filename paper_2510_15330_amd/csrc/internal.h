@@ -65,6 +65,42 @@ struct AttnArgs {
     float* part_o;       // [(B*H_kv + waves) * G * D]
 };
 
+// Prompt KV write (prefill.hip).
+struct WriteArgs {
+    const void* k_new;   // [T, H_kv, D] pool element type
+    const void* v_new;
+    int64_t k_st, k_sh, v_st, v_sh;   // row strides (elements)
+    void* k_pages;
+    void* v_pages;
+    const int32_t* block_table;
+    int64_t bt_stride;
+    int32_t* seq_lens;
+    const int32_t* q_start;  // [B + 1]
+    int32_t* err;
+    int64_t num_pages;
+    int B, T, H_kv, D, max_pages, elem_bytes;
+};
+
+// Prompt (prefill) attention over the paged cache (prefill.hip).
+constexpr int kPrefillRows = 128;   // query rows per workgroup (4 waves x 32)
+struct PrefillArgs {
+    const uint16_t* q;   // bf16 [T, H_q, D]
+    int64_t q_st, q_sh;
+    const void* k_pages;
+    const void* v_pages;
+    const int32_t* block_table;
+    int64_t bt_stride;
+    const int32_t* seq_lens;   // [B]: cached tokens, the last n_b are the queries
+    const int32_t* q_start;    // [B + 1]
+    uint16_t* out;       // bf16 [T, H_q, D]
+    int64_t o_st, o_sh;
+    int64_t num_pages;
+    float scale_log2;
+    int B, T, H_q, H_kv, G, D, max_pages;
+    int32_t* err;
+    int32_t* tile_start;   // workspace [B + 1]: first query tile of each request
+};
+
 // Launchers (kernels.hip).  They only enqueue; errors come back through
 // hipGetLastError in the caller.
 void launch_kv_append(const AppendArgs& a, hipStream_t s);
@@ -73,6 +109,9 @@ void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8
 void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
+// Prefill launchers (prefill.hip).
+void launch_kv_write(const WriteArgs& a, hipStream_t s);
+void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s);
 
 // Record the calling thread's last-error text (bellman_last_error) and
 // return `code`; shared by the host-side parts of the library.

@@ -1,0 +1,388 @@
+// Prompt (prefill) path over the paged KV cache: the write of a prompt's
+// keys and values into its pages, and causal prompt attention (each query
+// token attends every cached token up to its own position), for gfx950.
+//
+// The paper's serving loop (Sec. 3 "Our key proposal", Sec. 4 "Setup and
+// trace") prefills each queued request's prompt before decoding; the
+// prefill's cost sets the time to first token.  The attention is a dense
+// contraction (QK^T and PV over head_dim and keys), so it runs on
+// v_mfma_f32_32x32x16_bf16, with the keys and values staged through LDS and
+// shared by the workgroup's four waves.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/bellman.h"
+#include "internal.h"
+
+namespace bellman {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint16_t to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float swap_halves(float x) {  // value of lane l ^ 32
+    const unsigned u = __float_as_uint(x);
+    // the swap exchanges the first operand's lanes 32..63 with the second
+    // operand's lanes 0..31: the upper half finds its partner in r[0], the
+    // lower half in r[1]
+    const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+    return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
+}
+
+// Request whose range [q_start[b], q_start[b+1]) holds token i (q_start
+// non-decreasing), or -1.
+__device__ __forceinline__ int find_request(const int32_t* q_start, int B, int i) {
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (q_start[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    return (q_start[lo] <= i && i < q_start[lo + 1]) ? lo : -1;
+}
+
+// ----------------------------------------------------------- prompt write --
+// One workgroup per prompt token: its K row goes in 16-byte chunks and its V
+// row element by element (V pages are dim-major) to position
+// seq_lens[b] + (i - q_start[b]).  Lengths are advanced afterwards by
+// lens_kernel, so every token sees its request's old length.
+__global__ void __launch_bounds__(256) kv_write_kernel(WriteArgs a) {
+    const int i = blockIdx.x;
+    const int b = find_request(a.q_start, a.B, i);
+    if (b < 0) {
+        if (threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
+        return;
+    }
+    const int pos = a.seq_lens[b] + (i - a.q_start[b]);
+    const int pi = pos / kPage;
+    int pg = -1;
+    if (pos >= 0 && pi < a.max_pages) pg = a.block_table[(int64_t)b * a.bt_stride + pi];
+    if (pg < 0 || pg >= a.num_pages) {
+        if (threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
+        return;
+    }
+    const int slot = pos % kPage;
+    const int eb = a.elem_bytes, x = 16 / eb, chunks = a.D / x;
+    char* kp = (char*)a.k_pages;
+    char* vp = (char*)a.v_pages;
+    const int64_t tile = (int64_t)a.D * kPage;  // elements per (page, head) tile
+    for (int j = threadIdx.x; j < a.H_kv * chunks; j += blockDim.x) {
+        const int g = j / chunks, c = j - g * chunks;
+        const char* src = (const char*)a.k_new + ((int64_t)i * a.k_st + (int64_t)g * a.k_sh + (int64_t)c * x) * eb;
+        const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;   // 16-byte units
+        *(u32x4*)(kp + dst * 16) = *(const u32x4*)src;
+    }
+    for (int j = threadIdx.x; j < a.H_kv * a.D; j += blockDim.x) {
+        const int g = j / a.D, d = j - g * a.D;
+        const int64_t src = (int64_t)i * a.v_st + (int64_t)g * a.v_sh + d;
+        const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile + (int64_t)d * kPage + slot;
+        if (eb == 2)
+            *(uint16_t*)(vp + dst * 2) = *(const uint16_t*)((const char*)a.v_new + src * 2);
+        else
+            *(uint8_t*)(vp + dst) = *(const uint8_t*)((const char*)a.v_new + src);
+    }
+}
+
+// Each request's length grows by its token count (when its last position
+// fits the table).
+__global__ void lens_kernel(WriteArgs a) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= a.B) return;
+    const int n = a.q_start[b + 1] - a.q_start[b];
+    const int L = a.seq_lens[b];
+    if (n < 0 || L < 0 || (int64_t)L + n > (int64_t)a.max_pages * kPage || a.q_start[b + 1] > a.T) {
+        atomicOr(a.err, kErrAppendSlot);
+        return;
+    }
+    a.seq_lens[b] = L + n;
+}
+
+// --------------------------------------------------------------- planning --
+// Exclusive scan of the requests' query-tile counts, ceil(n_b / 128), into
+// tile_start[0..B].  A request whose range is malformed (longer than its
+// length, or a length past the table) gets no tiles and a flag; a q_start
+// that is not non-decreasing from a non-negative start up to at most T gives
+// no request any tile (so the tiles always fit the grid of
+// ceil(T / 128) + B workgroups).
+constexpr int kPlanThreads = 1024;
+
+__device__ __forceinline__ int tiles_of(const PrefillArgs& a, int b) {
+    const int n = a.q_start[b + 1] - a.q_start[b], L = a.seq_lens[b];
+    if (n < 0 || n > L || (int64_t)L > (int64_t)a.max_pages * kPage) return -1;
+    return (n + kPrefillRows - 1) / kPrefillRows;
+}
+
+__global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs a) {
+    __shared__ int part[kPlanThreads];
+    __shared__ int malformed;
+    const int tid = threadIdx.x;
+    if (tid == 0) malformed = (a.q_start[0] < 0 || a.q_start[a.B] > a.T) ? 1 : 0;
+    __syncthreads();
+    const int per = (a.B + kPlanThreads - 1) / kPlanThreads;
+    const int b0 = tid * per;
+    int sum = 0, bad = 0;
+    for (int k = 0; k < per; ++k) {
+        const int b = b0 + k;
+        if (b >= a.B) break;
+        if (a.q_start[b + 1] < a.q_start[b]) atomicOr(&malformed, 1);
+        const int t = tiles_of(a, b);
+        if (t < 0) bad = 1;
+        else sum += t;
+    }
+    if (bad) atomicOr(a.err, kErrLength);
+    part[tid] = sum;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {  // inclusive scan
+        const int v = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    if (malformed) {
+        for (int k = 0; k < per; ++k)
+            if (b0 + k < a.B) a.tile_start[b0 + k] = 0;
+        if (tid == 0) {
+            a.tile_start[a.B] = 0;
+            atomicOr(a.err, kErrLength);
+        }
+        return;
+    }
+    int run = tid ? part[tid - 1] : 0;
+    for (int k = 0; k < per; ++k) {
+        const int b = b0 + k;
+        if (b < a.B) {
+            a.tile_start[b] = run;
+            run += max(tiles_of(a, b), 0);
+        }
+    }
+    if (tid == kPlanThreads - 1) a.tile_start[a.B] = part[tid];
+}
+
+// -------------------------------------------------------------- attention --
+// Workgroup = 128 query rows of one request and one query head; wave w owns
+// rows 32w..32w+31.  Keys go by steps of 32 (two pages): the step's K and V
+// tiles are copied from the pool into LDS as they are laid out there (K
+// [page][D/8 chunks][16 slots][8], V [page][D][16 slots]), double-buffered,
+// and read by all four waves.
+//
+// S^T = K Q^T on 32x32x16 MFMAs (A = 32 keys x 16 dims from LDS, B = the
+// wave's 32 query columns, held in registers for the whole kernel).  The
+// result leaves lane (h, c) (h = lane / 32) with query c and the 16 keys
+// 8 (j / 4) + 4 h + j % 4, so the row max needs only the partner lane c + 32,
+// and the lane's own probabilities are exactly the B operand of
+// O^T += V^T P^T for the same query column: per 16-key half u, keys
+// 16 u + {4h..4h+3, 8+4h..8+4h+3}, whose V^T elements are two 8-byte runs of
+// the dim-major V rows.  Online softmax in base 2; O is rescaled only when a
+// running max grows.  P enters as bf16 (hi), and with SPLIT also as the bf16
+// remainder (lo), carrying it to ~2^-17.
+template <int D, bool SPLIT>
+__global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
+    constexpr int KT = 2 * D * kPage;   // elements of a two-page K (or V) tile
+    constexpr int UNITS = 2 * KT / 8;   // 16-byte units of K + V per step
+    constexpr int PER = UNITS / 256;    // per thread
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2 * KT];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int c = lane & 31, hl = lane >> 5;
+    const int h = blockIdx.y, g = h / a.G;
+    const int total = a.tile_start[a.B];
+    const int x = total - 1 - (int)blockIdx.x;   // last tiles (the longest) first
+    if (x < 0) return;
+    int lo = 0, hi = a.B - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.tile_start[mid] <= x) lo = mid;
+        else hi = mid - 1;
+    }
+    const int b = lo;
+    const int t0 = a.q_start[b];
+    const int n = a.q_start[b + 1] - t0;
+    const int L = a.seq_lens[b];
+    const int p0 = L - n;                          // position of query token 0
+    const int r0 = (x - a.tile_start[b]) * kPrefillRows;
+    const int kv_end = p0 + min(r0 + kPrefillRows, n);   // keys [0, kv_end)
+    const int nsteps = (kv_end + 31) / 32;
+    const int np = (L + kPage - 1) / kPage;
+    const int32_t* bt = a.block_table + (int64_t)b * a.bt_stride;
+
+    const int rw = r0 + 32 * w;                    // this wave's first row
+    const int row = min(rw + c, n - 1);            // padding columns repeat the last row
+    const int pos = p0 + row;                      // keys 0..pos are visible to this column
+    const int wave_steps = rw < n ? (p0 + min(rw + 31, n - 1)) / 32 + 1 : 0;
+
+    bf16x8 qv[D / 16];
+    {
+        const uint16_t* qrow = a.q + (int64_t)(t0 + row) * a.q_st + (int64_t)h * a.q_sh + 8 * hl;
+#pragma unroll
+        for (int kb = 0; kb < D / 16; ++kb) qv[kb] = *(const bf16x8*)(qrow + 16 * kb);
+    }
+    f32x16 o[D / 32];
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) o[t] = f32x16{};
+    float m = -INFINITY, l = 0.f;
+    bool bad = false;
+
+    // thread tid stages units tid + 256 k: unit u < KT/8 is K, the rest V;
+    // within a tile, unit v covers elements [8v, 8v + 8) of page v / (D*2)
+    u32x4 stage[PER];
+    auto load = [&](int s) {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int u = tid + 256 * k;
+            const bool isv = u >= KT / 8;
+            const int v = isv ? u - KT / 8 : u;
+            const int pp = v / (D * 2);            // page of the step (0, 1)
+            int pg = bt[min(2 * s + pp, np - 1)];
+            if ((unsigned)pg >= (unsigned)a.num_pages) {
+                pg = 0;
+                bad = true;
+            }
+            const char* base = (const char*)(isv ? a.v_pages : a.k_pages) +
+                               ((int64_t)pg * a.H_kv + g) * (int64_t)(D * kPage * 2);
+            stage[k] = *(const u32x4*)(base + (int64_t)(v - pp * D * 2) * 16);
+        }
+    };
+    auto store = [&](int s, int buf) {
+        const bool tail = 32 * s + 32 > L;         // keys past the length in this step
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int u = tid + 256 * k;
+            u32x4 val = stage[k];
+            if (tail && u >= KT / 8) {
+                // V unit: dim row (v % (2D)) / 2 of page pp, slots 8 (v % 2) .. +7
+                const int v = u - KT / 8;
+                const int pp = v / (D * 2);
+                const int key0 = 32 * s + 16 * pp + 8 * (v & 1);
+                const int live = L - key0;         // keys < L keep their values
+                if (live <= 0) {
+                    val = u32x4{0u, 0u, 0u, 0u};
+                } else if (live < 8) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int k0 = 2 * e;
+                        const uint32_t keep = (k0 + 1 < live ? 0xffff0000u : 0u) | (k0 < live ? 0x0000ffffu : 0u);
+                        val[e] &= keep;
+                    }
+                }
+            }
+            *(u32x4*)(&lds[buf][8 * u]) = val;
+        }
+    };
+
+    load(0);
+    store(0, 0);
+    __syncthreads();
+    for (int s = 0; s < nsteps; ++s) {
+        const int cur = s & 1;
+        if (s + 1 < nsteps) load(s + 1);
+        if (s < wave_steps) {
+            const uint16_t* K = lds[cur];
+            const uint16_t* V = lds[cur] + KT;
+            // S^T = K Q^T: A lane (h, c) = key c, dims 16 kb + 8 h ..: chunk 2 kb + h
+            f32x16 sc = f32x16{};
+            const int kk = c;
+#pragma unroll
+            for (int kb = 0; kb < D / 16; ++kb) {
+                const bf16x8 ka = *(const bf16x8*)(K + (kk >> 4) * (D * kPage) + (2 * kb + hl) * (kPage * 8) +
+                                                   (kk & 15) * 8);
+                sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc, 0, 0, 0);
+            }
+            float xs[16];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int key = 32 * s + 8 * (j >> 2) + 4 * hl + (j & 3);
+                xs[j] = key <= pos ? sc[j] * a.scale_log2 : -INFINITY;
+                mx = fmaxf(mx, xs[j]);
+            }
+            mx = fmaxf(mx, swap_halves(mx));
+            const float m_new = fmaxf(m, mx);
+            if (__any(m_new > m)) {
+                const float alpha = __builtin_amdgcn_exp2f(m - m_new);
+                l *= alpha;
+#pragma unroll
+                for (int t = 0; t < D / 32; ++t) o[t] *= alpha;
+                m = m_new;
+            }
+            uint32_t ph[8], pl[8];
+            float psum = 0.f;
+#pragma unroll
+            for (int j = 0; j < 16; j += 2) {
+                const f32x2 pq = {__builtin_amdgcn_exp2f(xs[j] - m), __builtin_amdgcn_exp2f(xs[j + 1] - m)};
+                psum += pq.x + pq.y;
+                const bf16x2 hi = __builtin_convertvector(pq, bf16x2);   // round to nearest even
+                ph[j / 2] = __builtin_bit_cast(uint32_t, hi);
+                if constexpr (SPLIT)   // the remainder is exact in fp32; rounded again
+                    pl[j / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi, f32x2), bf16x2));
+            }
+            l += psum;
+            // O^T += V^T P^T, per 32-dim tile t and 16-key half u
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const bf16x8 bh = __builtin_bit_cast(bf16x8, u32x4{ph[4 * u], ph[4 * u + 1], ph[4 * u + 2], ph[4 * u + 3]});
+                bf16x8 bl;
+                if constexpr (SPLIT)
+                    bl = __builtin_bit_cast(bf16x8, u32x4{pl[4 * u], pl[4 * u + 1], pl[4 * u + 2], pl[4 * u + 3]});
+#pragma unroll
+                for (int t = 0; t < D / 32; ++t) {
+                    const uint16_t* vr = V + (u * D + 32 * t + c) * kPage + 4 * hl;
+                    const u32x2 v0 = *(const u32x2*)vr;
+                    const u32x2 v1 = *(const u32x2*)(vr + 8);
+                    const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{v0.x, v0.y, v1.x, v1.y});
+                    o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
+                    if constexpr (SPLIT) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                }
+            }
+        }
+        if (s + 1 < nsteps) store(s + 1, cur ^ 1);
+        __syncthreads();
+    }
+    if (bad && lane == 0) atomicOr(a.err, kErrPage);
+    if (rw >= n) return;
+    const float l_tot = l + swap_halves(l);
+    const float f = 1.0f / l_tot;
+    if (rw + c < n) {
+        uint16_t* orow = a.out + (int64_t)(t0 + rw + c) * a.o_st + (int64_t)h * a.o_sh;
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                u32x2 pk;
+                pk.x = (uint32_t)to_bf16_rne(o[t][4 * r4] * f) | ((uint32_t)to_bf16_rne(o[t][4 * r4 + 1] * f) << 16);
+                pk.y = (uint32_t)to_bf16_rne(o[t][4 * r4 + 2] * f) | ((uint32_t)to_bf16_rne(o[t][4 * r4 + 3] * f) << 16);
+                *(u32x2*)(orow + 32 * t + 8 * r4 + 4 * hl) = pk;
+            }
+    }
+}
+
+}  // namespace
+
+void launch_kv_write(const WriteArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(kv_write_kernel, dim3(a.T), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(lens_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
+}
+
+void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s) {
+    hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a);
+    const dim3 grid((unsigned)((a.T + kPrefillRows - 1) / kPrefillRows + a.B), (unsigned)a.H_q);
+    if (a.D == 128) {
+        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<128, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((prefill_attn_kernel<128, false>), grid, dim3(256), 0, s, a);
+    } else {
+        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<64, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((prefill_attn_kernel<64, false>), grid, dim3(256), 0, s, a);
+    }
+}
+
+}  // namespace bellman

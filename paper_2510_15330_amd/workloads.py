@@ -25,6 +25,15 @@ that setting produces:
                            fp8-e4m3fn K/V with one fp32 scale per (request, KV
                            head) for K and one for V.
 
+Prompt (prefill) batches, drawn by ``build_prefill``:
+
+* ``prefill_tiny``          4 requests, 8 query / 2 KV heads, head_dim 64,
+                           cached {0, 0, 16, 5} + new {1, 17, 200, 300} tokens.
+* ``prefill_summarization`` 4 whole prompts of U{6000..12000} tokens,
+                           32/8 heads, head_dim 128.
+* ``prefill_chunked``       the last 2048 tokens of 4 such prompts (the rest
+                           cached), the chunk size of the serving model.
+
 Values are N(0, 1) rounded to bf16.  Pages (16 tokens) are scattered over a
 randomly permuted pool, every page a request will need during the run is
 reserved up front, slots that hold no token yet and pages that belong to no
@@ -51,12 +60,18 @@ CONFIGS = {
     "stress_fp8": dict(B=512, H_q=64, H_kv=8, D=128, kv="fp8", steps=50),
 }
 
+PREFILL_CONFIGS = {
+    "prefill_tiny": dict(H_q=8, H_kv=2, D=64),
+    "prefill_summarization": dict(H_q=32, H_kv=8, D=128),
+    "prefill_chunked": dict(H_q=32, H_kv=8, D=128),
+}
+
 # Seed-stream indices under numpy's SeedSequence(seed).spawn(...)
-_S_LEN, _S_GEN, _S_CAP, _S_PAGES, _S_VALUES = range(5)
+_S_LEN, _S_GEN, _S_CAP, _S_PAGES, _S_VALUES, _S_P_LEN, _S_P_PAGES, _S_P_VALUES = range(8)
 
 
 def _streams(seed):
-    return np.random.SeedSequence(seed).spawn(5)
+    return np.random.SeedSequence(seed).spawn(8)
 
 
 def sample_lengths(name, seed=0, tiny_reading="after"):
@@ -277,3 +292,120 @@ def _fp8_pool(shape, gen, device, mask, owner, B, H_kv, red_dims, chunk_pages=40
     del vals
     codes = torch.where(mask, codes, torch.tensor(FP8_NAN_CODE, dtype=torch.uint8, device=device))
     return codes, scale.contiguous()
+
+
+# ------------------------------------------------------------ prompt batches --
+
+@dataclasses.dataclass
+class PrefillWorkload:
+    name: str
+    H_q: int
+    H_kv: int
+    D: int
+    scale: float                 # fp32 softmax scale 1/sqrt(D)
+    cached: np.ndarray           # int64 [B], tokens already in the cache
+    new: np.ndarray              # int64 [B], prompt tokens of this batch
+    num_pages: int
+    block_table: torch.Tensor    # int32 [B, maxP]
+    seq_lens: torch.Tensor       # int32 [B], initialised to ``cached``
+    q_start: torch.Tensor        # int32 [B + 1], exclusive prefix sum of ``new``
+    k_pages: torch.Tensor        # bf16 [NP, H_kv, D/8, 16, 8]
+    v_pages: torch.Tensor        # bf16 [NP, H_kv, D, 16]
+    q: torch.Tensor              # bf16 [T, H_q, D]
+    k_new: torch.Tensor          # bf16 [T, H_kv, D]
+    v_new: torch.Tensor
+
+    @property
+    def B(self):
+        return len(self.new)
+
+    @property
+    def T(self):
+        return int(self.new.sum())
+
+    def total(self):
+        return self.cached + self.new
+
+    def flops(self):
+        """Multiply-adds of QK^T and PV over the visible (causal) pairs, two
+        flops each: query i of request b sees cached_b + i + 1 keys."""
+        c, n = self.cached.astype(np.int64), self.new.astype(np.int64)
+        pairs = int((n * c + n * (n + 1) // 2).sum())
+        return 4 * self.D * self.H_q * pairs
+
+    def write_bytes(self):
+        """Bytes one prompt write moves (new rows in, pool slots out)."""
+        return 2 * 2 * self.T * self.H_kv * self.D * 2
+
+
+def prefill_lengths(name, seed=0):
+    """(cached, new) token counts, int64 [B] each."""
+    ss = _streams(seed)
+    if name == "prefill_tiny":
+        return np.array([0, 0, 16, 5], dtype=np.int64), np.array([1, 17, 200, 300], dtype=np.int64)
+    prompt = np.random.default_rng(ss[_S_P_LEN]).integers(6000, 12000, size=4, endpoint=True).astype(np.int64)
+    if name == "prefill_summarization":
+        return np.zeros(4, dtype=np.int64), prompt
+    if name == "prefill_chunked":
+        return prompt - 2048, np.full(4, 2048, dtype=np.int64)
+    raise KeyError(name)
+
+
+def build_prefill(name=None, seed=0, device="cpu", cached=None, new=None, H_q=None, H_kv=None, D=None,
+                  slack_pages=5, extra_table=1):
+    """Materialise a prompt batch on ``device``: pages for every cached and new
+    token (scattered over a permuted pool), cached tokens' K/V present, every
+    other slot NaN, unused table entries -1.  Named configurations come from
+    PREFILL_CONFIGS / prefill_lengths; explicit ``cached``/``new`` and head
+    counts override them."""
+    if name is not None:
+        cfg = PREFILL_CONFIGS[name]
+        c0, n0 = prefill_lengths(name, seed)
+        cached = c0 if cached is None else cached
+        new = n0 if new is None else new
+        H_q, H_kv, D = (cfg["H_q"] if H_q is None else H_q, cfg["H_kv"] if H_kv is None else H_kv,
+                        cfg["D"] if D is None else D)
+    cached = np.asarray(cached, dtype=np.int64)
+    new = np.asarray(new, dtype=np.int64)
+    B = len(new)
+    ss = _streams(seed)
+    final = cached + new
+    need = (final + PAGE - 1) // PAGE
+    NP = int(need.sum()) + slack_pages
+    perm = np.random.default_rng(ss[_S_P_PAGES]).permutation(NP).astype(np.int32)
+    maxP = int(need.max()) + extra_table if B else 1
+    bt = np.full((B, maxP), -1, dtype=np.int32)
+    owner = np.full(NP, -1, dtype=np.int64)
+    logical = np.zeros(NP, dtype=np.int64)
+    pos = 0
+    for b in range(B):
+        n = int(need[b])
+        pages = perm[pos:pos + n]
+        bt[b, :n] = pages
+        owner[pages] = b
+        logical[pages] = np.arange(n)
+        pos += n
+    filled = np.where(owner >= 0, np.clip(cached[np.maximum(owner, 0)] - PAGE * logical, 0, PAGE), 0)
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(ss[_S_P_VALUES].generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
+    kshape = (NP, H_kv, D // 8, PAGE, 8)
+    vshape = (NP, H_kv, D, PAGE)
+    filled_t = torch.from_numpy(filled).to(device)
+    slot = torch.arange(PAGE, device=device)
+    live = slot[None, :] < filled_t[:, None]
+    nan = torch.tensor(BF16_NAN_BITS, dtype=torch.int16, device=device).view(torch.bfloat16)
+    k_pages = torch.where(live[:, None, None, :, None], _fill_pages(kshape, gen, device), nan)
+    v_pages = torch.where(live[:, None, None, :], _fill_pages(vshape, gen, device), nan)
+    T = int(new.sum())
+    q = _bf16_normal((T, H_q, D), gen, device)
+    k_new = _bf16_normal((T, H_kv, D), gen, device)
+    v_new = _bf16_normal((T, H_kv, D), gen, device)
+    q_start = np.concatenate([[0], np.cumsum(new)]).astype(np.int32)
+    return PrefillWorkload(
+        name=name or "custom", H_q=H_q, H_kv=H_kv, D=D, scale=float(np.float32(1.0 / math.sqrt(D))),
+        cached=cached, new=new, num_pages=NP,
+        block_table=torch.from_numpy(bt).to(device),
+        seq_lens=torch.from_numpy(cached.astype(np.int32)).to(device),
+        q_start=torch.from_numpy(q_start).to(device),
+        k_pages=k_pages.contiguous(), v_pages=v_pages.contiguous(), q=q, k_new=k_new, v_new=v_new)

@@ -9,7 +9,10 @@ import oracle
 import paper_2510_15330_amd as bl
 from paper_2510_15330_amd import workloads as wl
 
-TOL = {"bf16": (1e-2, 2e-3), "fp8": (3e-2, 1e-2)}   # (max-abs, rel-L2)
+# (max-abs, rel-L2).  "bf16_p1": prompt attention with P rounded to bf16 once
+# (an opt-in mode): P's rounding adds up to 2^-9 of each weight on top of the
+# output's 2^-9 rounding, so the bounds double.
+TOL = {"bf16": (1e-2, 2e-3), "fp8": (3e-2, 1e-2), "bf16_p1": (2e-2, 4e-3)}
 
 
 def bits16(t: torch.Tensor) -> np.ndarray:

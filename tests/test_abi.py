@@ -147,6 +147,58 @@ def test_append_rejects(B, name, mut, code, msg):
     assert msg in B.last_error()
 
 
+def prompt(B_, g, T=40, Bsz=4):
+    g.update(pq=t(B_.BF16, [T, 32, 128]), pout=t(B_.BF16, [T, 32, 128]), qs=t(B_.INT32, [Bsz + 1]),
+             pkn=t(B_.BF16, [T, 8, 128]), pvn=t(B_.BF16, [T, 8, 128]))
+    return g
+
+
+PREFILL_CASES = [
+    ("q_start size", lambda B_, g: g.update(qs=t(B_.INT32, [4])), ERR_INVALID, "q_start"),
+    ("q_start dtype", lambda B_, g: g.update(qs=t(B_.FP32, [5])), ERR_INVALID, "q_start: dtype"),
+    ("q_start strided", lambda B_, g: g.update(qs=t(B_.INT32, [5], [2])), ERR_UNSUPPORTED, "contiguous"),
+    ("out rows", lambda B_, g: g.update(pout=t(B_.BF16, [39, 32, 128])), ERR_INVALID, "out: shape"),
+    ("H_q not multiple", lambda B_, g: g.update(pq=t(B_.BF16, [40, 30, 128]), pout=t(B_.BF16, [40, 30, 128])),
+     ERR_INVALID, "not a multiple"),
+    ("fp8 pools", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 8, 16, 16], scale=FAKE),
+                                         v=t(B_.FP8_E4M3FN, [100, 8, 128, 16], scale=FAKE)), ERR_UNSUPPORTED, "fp8"),
+    ("misaligned q", lambda B_, g: g.update(pq=t(B_.BF16, [40, 32, 128], data=FAKE + 2)), ERR_UNSUPPORTED, "aligned"),
+    ("misaligned out", lambda B_, g: g.update(pout=t(B_.BF16, [40, 32, 128], data=FAKE + 4)), ERR_UNSUPPORTED,
+     "aligned"),
+    ("non-finite scale", lambda B_, g: None, ERR_INVALID, "scale"),
+]
+
+
+@pytest.mark.parametrize("name,mut,code,msg", PREFILL_CASES, ids=[c[0] for c in PREFILL_CASES])
+def test_prefill_rejects(B, name, mut, code, msg):
+    g = prompt(B, good(B))
+    mut(B, g)
+    lib = B.library()
+    scale = float("nan") if name == "non-finite scale" else 0.125
+    rc = lib.bellman_prefill_attention(g["pq"], g["k"], g["v"], g["bt"], g["sl"], g["qs"], scale, g["pout"], None)
+    assert rc == code
+    assert msg in B.last_error()
+
+
+WRITE_CASES = [
+    ("k_new heads", lambda B_, g: g.update(pkn=t(B_.BF16, [40, 4, 128])), ERR_INVALID, "k_new: shape"),
+    ("v_new rows", lambda B_, g: g.update(pvn=t(B_.BF16, [39, 8, 128])), ERR_INVALID, "v_new: shape"),
+    ("q_start size", lambda B_, g: g.update(qs=t(B_.INT32, [6])), ERR_INVALID, "q_start"),
+    ("misaligned k_new", lambda B_, g: g.update(pkn=t(B_.BF16, [40, 8, 128], data=FAKE + 8)), ERR_UNSUPPORTED,
+     "aligned"),
+]
+
+
+@pytest.mark.parametrize("name,mut,code,msg", WRITE_CASES, ids=[c[0] for c in WRITE_CASES])
+def test_prompt_write_rejects(B, name, mut, code, msg):
+    g = prompt(B, good(B))
+    mut(B, g)
+    lib = B.library()
+    rc = lib.bellman_kv_write(g["pkn"], g["pvn"], g["k"], g["v"], g["bt"], g["sl"], g["qs"], None)
+    assert rc == code
+    assert msg in B.last_error()
+
+
 def test_option_ranges(B):
     g = good(B)
     lib = B.library()
