@@ -2,6 +2,7 @@
 // and the launch sequence of one decode-attention call.
 #include <hip/hip_runtime.h>
 
+#include <float.h>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -578,7 +579,10 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     a.o_st = out->stride[0];
     a.o_sh = out->stride[1];
     a.num_pages = ps.num_pages;
+    // the kernel takes |scale| (with the query's sign flipped for a negative
+    // one) and needs it nonzero; a zero scale becomes the smallest normal
     a.scale_log2 = scale * 1.4426950408889634f;
+    if (fabsf(a.scale_log2) < FLT_MIN) a.scale_log2 = copysignf(FLT_MIN, a.scale_log2);
     a.B = (int)B;
     a.T = (int)T;
     a.H_q = (int)H_q;

@@ -24,13 +24,6 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-__device__ __forceinline__ uint16_t to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-}
-
 __device__ __forceinline__ float swap_halves(float x) {  // value of lane l ^ 32
     const unsigned u = __float_as_uint(x);
     // the swap exchanges the first operand's lanes 32..63 with the second
@@ -172,28 +165,36 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 // -------------------------------------------------------------- attention --
 // Workgroup = 128 query rows of one request and one query head; wave w owns
 // rows 32w..32w+31.  Keys go by steps of 32 (two pages): the step's K and V
-// tiles are copied from the pool into LDS as they are laid out there (K
-// [page][D/8 chunks][16 slots][8], V [page][D][16 slots]), double-buffered,
-// and read by all four waves.
+// tiles are copied from the pool into LDS in the pool's own layout (K [page]
+// [D/8 chunks][16 slots][8], V [page][D][16 slots]), double-buffered, and read
+// by all four waves.
 //
-// S^T = K Q^T on 32x32x16 MFMAs (A = 32 keys x 16 dims from LDS, B = the
-// wave's 32 query columns, held in registers for the whole kernel).  The
-// result leaves lane (h, c) (h = lane / 32) with query c and the 16 keys
-// 8 (j / 4) + 4 h + j % 4, so the row max needs only the partner lane c + 32,
-// and the lane's own probabilities are exactly the B operand of
-// O^T += V^T P^T for the same query column: per 16-key half u, keys
-// 16 u + {4h..4h+3, 8+4h..8+4h+3}, whose V^T elements are two 8-byte runs of
-// the dim-major V rows.  Online softmax in base 2; O is rescaled only when a
-// running max grows.  P enters as bf16 (hi), and with SPLIT also as the bf16
-// remainder (lo), carrying it to ~2^-17.
-template <int D, bool SPLIT>
-__global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
-    constexpr int KT = 2 * D * kPage;   // elements of a two-page K (or V) tile
-    constexpr int UNITS = 2 * KT / 8;   // 16-byte units of K + V per step
-    constexpr int PER = UNITS / 256;    // per thread
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2 * KT];
+// S^T = K Q^T on 32x32x16 MFMAs: A = 32 keys x 16 dims from LDS, B = the
+// wave's 32 query columns, held in registers for the whole kernel.  A's row i
+// holds key pi(i) = 16 (i / 16) + 8 ((i / 4) % 2) + 4 ((i / 8) % 2) + i % 4,
+// which leaves lane (h, c) (h = lane / 32) of the result with query c and the
+// keys 16 u + 8 h + 0..7 for u = 0, 1: the row max needs only the partner lane
+// c + 32, and the lane's probabilities are exactly the B operand of
+// O^T += V^T P^T for the 16 keys of page u, whose V^T elements are one
+// 16-byte run of each dim-major V row.  Online softmax in base 2 with a lazy
+// max: O and l are rescaled only when some column's max grows by more than
+// 2^8, so P stays below 2^8.  P enters as bf16 (hi), and with SPLIT also as
+// the bf16 remainder (lo), carrying it to ~2^-17.
+constexpr float kLazyMax = 8.0f;
+constexpr int kPageWindow = 1024;   // block-table entries staged in LDS (512 steps)
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+template <int D, bool SPLIT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+prefill_attn_kernel(PrefillArgs a) {
+    constexpr int PE = D * kPage;       // elements of one page of one head (K or V)
+    constexpr int KT = 2 * PE;          // a step's K (or V) tile
+    constexpr int UPP = PE / 8;         // 16-byte units per page
+    constexpr int PER = 4 * UPP / 256;  // units of K + V per thread per step
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2 * KT];
+    __shared__ int pages[kPageWindow];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 31, hl = lane >> 5;
     const int h = blockIdx.y, g = h / a.G;
     const int total = a.tile_start[a.B];
@@ -221,11 +222,19 @@ __global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
     const int pos = p0 + row;                      // keys 0..pos are visible to this column
     const int wave_steps = rw < n ? (p0 + min(rw + 31, n - 1)) / 32 + 1 : 0;
 
+    // softmax(scale * s) = softmax(|scale| * (-s)): for a negative scale the
+    // query's sign bits are flipped (the host keeps |scale| >= FLT_MIN)
+    const float sl = fabsf(a.scale_log2);
     bf16x8 qv[D / 16];
     {
+        const uint32_t flip = a.scale_log2 < 0.f ? 0x80008000u : 0u;
         const uint16_t* qrow = a.q + (int64_t)(t0 + row) * a.q_st + (int64_t)h * a.q_sh + 8 * hl;
 #pragma unroll
-        for (int kb = 0; kb < D / 16; ++kb) qv[kb] = *(const bf16x8*)(qrow + 16 * kb);
+        for (int kb = 0; kb < D / 16; ++kb) {
+            u32x4 v = *(const u32x4*)(qrow + 16 * kb);
+            v ^= flip;
+            qv[kb] = __builtin_bit_cast(bf16x8, v);
+        }
     }
     f32x16 o[D / 32];
 #pragma unroll
@@ -233,82 +242,100 @@ __global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
     float m = -INFINITY, l = 0.f;
     bool bad = false;
 
-    // thread tid stages units tid + 256 k: unit u < KT/8 is K, the rest V;
-    // within a tile, unit v covers elements [8v, 8v + 8) of page v / (D*2)
+    // the block-table entries of 512 steps at a time sit in LDS, refilled
+    // when no copy is in flight, so a step's pages cost two LDS reads
+    auto refill = [&](int j) {
+        for (int e = tid; e < kPageWindow; e += 256) pages[e] = bt[min(2 * j + e, np - 1)];
+        __syncthreads();
+    };
+    // unit u = 256 k + tid of a step: tensor u / (2 UPP) (K, V), page
+    // (u / UPP) % 2, 16-byte unit u % UPP of that page; a wave's 64 units are
+    // consecutive and lie in one page.  The next step's units are loaded into
+    // registers while this step computes and written to LDS after it.
     u32x4 stage[PER];
-    auto load = [&](int s) {
+    auto load = [&](int j) {
+        const int e = 2 * (j % (kPageWindow / 2));
+        int pa = pages[e], pb = pages[e + 1];
+        if ((unsigned)pa >= (unsigned)a.num_pages) {
+            pa = 0;
+            bad = true;
+        }
+        if ((unsigned)pb >= (unsigned)a.num_pages) {
+            pb = 0;
+            bad = true;
+        }
 #pragma unroll
         for (int k = 0; k < PER; ++k) {
-            const int u = tid + 256 * k;
-            const bool isv = u >= KT / 8;
-            const int v = isv ? u - KT / 8 : u;
-            const int pp = v / (D * 2);            // page of the step (0, 1)
-            int pg = bt[min(2 * s + pp, np - 1)];
-            if ((unsigned)pg >= (unsigned)a.num_pages) {
-                pg = 0;
-                bad = true;
-            }
-            const char* base = (const char*)(isv ? a.v_pages : a.k_pages) +
-                               ((int64_t)pg * a.H_kv + g) * (int64_t)(D * kPage * 2);
-            stage[k] = *(const u32x4*)(base + (int64_t)(v - pp * D * 2) * 16);
+            const int ub = 256 * k + 64 * w;       // the wave's first unit
+            const int isv = ub / (2 * UPP), pp = (ub / UPP) & 1;
+            const uint16_t* src = (const uint16_t*)(isv ? a.v_pages : a.k_pages) +
+                                  ((int64_t)(pp ? pb : pa) * a.H_kv + g) * PE + (int64_t)(ub % UPP + lane) * 8;
+            stage[k] = *(const u32x4*)src;
         }
     };
-    auto store = [&](int s, int buf) {
-        const bool tail = 32 * s + 32 > L;         // keys past the length in this step
+    auto store = [&](int buf) {
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int u = tid + 256 * k;
-            u32x4 val = stage[k];
-            if (tail && u >= KT / 8) {
-                // V unit: dim row (v % (2D)) / 2 of page pp, slots 8 (v % 2) .. +7
-                const int v = u - KT / 8;
-                const int pp = v / (D * 2);
-                const int key0 = 32 * s + 16 * pp + 8 * (v & 1);
-                const int live = L - key0;         // keys < L keep their values
-                if (live <= 0) {
-                    val = u32x4{0u, 0u, 0u, 0u};
-                } else if (live < 8) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int k0 = 2 * e;
-                        const uint32_t keep = (k0 + 1 < live ? 0xffff0000u : 0u) | (k0 < live ? 0x0000ffffu : 0u);
-                        val[e] &= keep;
-                    }
-                }
-            }
-            *(u32x4*)(&lds[buf][8 * u]) = val;
+        for (int k = 0; k < PER; ++k) *(u32x4*)&lds[buf][8 * (256 * k + tid)] = stage[k];
+    };
+    // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
+    // 0 * NaN must not reach O, so the tail step's slots are cleared
+    auto clear_tail = [&](int s, int buf) {
+        uint16_t* V = lds[buf] + KT;
+        for (int e = tid; e < KT; e += 256) {
+            const int key = 32 * s + 16 * (e / PE) + (e & 15);
+            if (key >= L) V[e] = 0;
         }
     };
 
+    // lane (h, c) reads A row c = key pi(c)
+    const int kk = 16 * (c >> 4) + 8 * ((c >> 2) & 1) + 4 * ((c >> 3) & 1) + (c & 3);
+    const int k_off = (kk >> 4) * PE + hl * (kPage * 8) + (kk & 15) * 8;
+    const int v_off = KT + c * kPage + 8 * hl;
+
+    refill(0);
     load(0);
-    store(0, 0);
+    store(0);
     __syncthreads();
+    if (32 * 1 > L) {
+        clear_tail(0, 0);
+        __syncthreads();
+    }
     for (int s = 0; s < nsteps; ++s) {
         const int cur = s & 1;
-        if (s + 1 < nsteps) load(s + 1);
+        if (s + 1 < nsteps) {
+            if ((s + 1) % (kPageWindow / 2) == 0) refill(s + 1);
+            load(s + 1);
+        }
         if (s < wave_steps) {
-            const uint16_t* K = lds[cur];
-            const uint16_t* V = lds[cur] + KT;
-            // S^T = K Q^T: A lane (h, c) = key c, dims 16 kb + 8 h ..: chunk 2 kb + h
+            const uint16_t* K = lds[cur] + k_off;
             f32x16 sc = f32x16{};
-            const int kk = c;
 #pragma unroll
             for (int kb = 0; kb < D / 16; ++kb) {
-                const bf16x8 ka = *(const bf16x8*)(K + (kk >> 4) * (D * kPage) + (2 * kb + hl) * (kPage * 8) +
-                                                   (kk & 15) * 8);
+                const bf16x8 ka = *(const bf16x8*)(K + kb * (2 * kPage * 8));
                 sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc, 0, 0, 0);
             }
-            float xs[16];
-            float mx = -INFINITY;
+            // V^T operands of the step, read while the softmax runs
+            bf16x8 va[2][D / 32];
+            const uint16_t* V = lds[cur] + v_off;
 #pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const int key = 32 * s + 8 * (j >> 2) + 4 * hl + (j & 3);
-                xs[j] = key <= pos ? sc[j] * a.scale_log2 : -INFINITY;
-                mx = fmaxf(mx, xs[j]);
+            for (int u = 0; u < 2; ++u)
+#pragma unroll
+                for (int t = 0; t < D / 32; ++t) va[u][t] = *(const bf16x8*)(V + (u * D + 32 * t) * kPage);
+            // keys above a column's position are masked only on the steps
+            // the wave's diagonal crosses
+            if (32 * s + 31 > p0 + rw) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int key = 32 * s + 16 * (j >> 3) + 8 * hl + (j & 7);
+                    sc[j] = key <= pos ? sc[j] : -INFINITY;
+                }
             }
+            float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+#pragma unroll
+            for (int j = 3; j < 16; ++j) mx = fmaxf(mx, sc[j]);
             mx = fmaxf(mx, swap_halves(mx));
-            const float m_new = fmaxf(m, mx);
-            if (__any(m_new > m)) {
+            const float m_new = fmaxf(m, mx * sl);     // scaled units
+            if (__any(m_new > m + kLazyMax)) {
                 const float alpha = __builtin_amdgcn_exp2f(m - m_new);
                 l *= alpha;
 #pragma unroll
@@ -319,34 +346,37 @@ __global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
             float psum = 0.f;
 #pragma unroll
             for (int j = 0; j < 16; j += 2) {
-                const f32x2 pq = {__builtin_amdgcn_exp2f(xs[j] - m), __builtin_amdgcn_exp2f(xs[j + 1] - m)};
+                const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[j], sl, -m)),
+                                  __builtin_amdgcn_exp2f(__builtin_fmaf(sc[j + 1], sl, -m))};
                 psum += pq.x + pq.y;
-                const bf16x2 hi = __builtin_convertvector(pq, bf16x2);   // round to nearest even
-                ph[j / 2] = __builtin_bit_cast(uint32_t, hi);
+                const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
+                ph[j / 2] = __builtin_bit_cast(uint32_t, hi2);
                 if constexpr (SPLIT)   // the remainder is exact in fp32; rounded again
-                    pl[j / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi, f32x2), bf16x2));
+                    pl[j / 2] = __builtin_bit_cast(uint32_t,
+                                                   __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
             }
             l += psum;
-            // O^T += V^T P^T, per 32-dim tile t and 16-key half u
+            // O^T += V^T P^T, per 16-key page u and 32-dim tile t
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 const bf16x8 bh = __builtin_bit_cast(bf16x8, u32x4{ph[4 * u], ph[4 * u + 1], ph[4 * u + 2], ph[4 * u + 3]});
-                bf16x8 bl;
-                if constexpr (SPLIT)
-                    bl = __builtin_bit_cast(bf16x8, u32x4{pl[4 * u], pl[4 * u + 1], pl[4 * u + 2], pl[4 * u + 3]});
 #pragma unroll
-                for (int t = 0; t < D / 32; ++t) {
-                    const uint16_t* vr = V + (u * D + 32 * t + c) * kPage + 4 * hl;
-                    const u32x2 v0 = *(const u32x2*)vr;
-                    const u32x2 v1 = *(const u32x2*)(vr + 8);
-                    const bf16x8 va = __builtin_bit_cast(bf16x8, u32x4{v0.x, v0.y, v1.x, v1.y});
-                    o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
-                    if constexpr (SPLIT) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                for (int t = 0; t < D / 32; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[u][t], bh, o[t], 0, 0, 0);
+                if constexpr (SPLIT) {
+                    const bf16x8 bl = __builtin_bit_cast(bf16x8, u32x4{pl[4 * u], pl[4 * u + 1], pl[4 * u + 2], pl[4 * u + 3]});
+#pragma unroll
+                    for (int t = 0; t < D / 32; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[u][t], bl, o[t], 0, 0, 0);
                 }
             }
         }
-        if (s + 1 < nsteps) store(s + 1, cur ^ 1);
-        __syncthreads();
+        if (s + 1 < nsteps) {
+            store(cur ^ 1);
+            __syncthreads();
+            if (32 * (s + 2) > L) {
+                clear_tail(s + 1, cur ^ 1);
+                __syncthreads();
+            }
+        }
     }
     if (bad && lane == 0) atomicOr(a.err, kErrPage);
     if (rw >= n) return;
@@ -358,9 +388,11 @@ __global__ void __launch_bounds__(256) prefill_attn_kernel(PrefillArgs a) {
         for (int t = 0; t < D / 32; ++t)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
+                const f32x2 v01 = {o[t][4 * r4] * f, o[t][4 * r4 + 1] * f};
+                const f32x2 v23 = {o[t][4 * r4 + 2] * f, o[t][4 * r4 + 3] * f};
                 u32x2 pk;
-                pk.x = (uint32_t)to_bf16_rne(o[t][4 * r4] * f) | ((uint32_t)to_bf16_rne(o[t][4 * r4 + 1] * f) << 16);
-                pk.y = (uint32_t)to_bf16_rne(o[t][4 * r4 + 2] * f) | ((uint32_t)to_bf16_rne(o[t][4 * r4 + 3] * f) << 16);
+                pk.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(v01, bf16x2));
+                pk.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(v23, bf16x2));
                 *(u32x2*)(orow + 32 * t + 8 * r4 + 4 * hl) = pk;
             }
     }
