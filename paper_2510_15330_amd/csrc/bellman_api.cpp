@@ -559,6 +559,9 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
         return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
     if (H_q > 65535) return fail(BELLMAN_ERR_UNSUPPORTED, "more than 65535 query heads");
     if (T > INT32_MAX / 2 || B > INT32_MAX / 2) return fail(BELLMAN_ERR_UNSUPPORTED, "too many tokens or requests");
+    // tiles x query heads must fit the kernel's 32-bit work index
+    if (((T + kPrefillRows - 1) / kPrefillRows + B) * H_q > INT32_MAX / 2)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "too many query tiles x heads");
     if (T == 0 || B == 0) return BELLMAN_OK;
 
     int dev;

@@ -164,10 +164,11 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 
 // -------------------------------------------------------------- attention --
 // Workgroup = 128 query rows of one request and one query head; wave w owns
-// rows 32w..32w+31.  Keys go by steps of 32 (two pages): the step's K and V
+// rows 32w..32w+31.  Keys go by steps of 64 (four pages).  The step's K and V
 // tiles are copied from the pool into LDS in the pool's own layout (K [page]
-// [D/8 chunks][16 slots][8], V [page][D][16 slots]), double-buffered, and read
-// by all four waves.
+// [D/8 chunks][16 slots][8], V [page][D][16 slots], both XOR-swizzled against
+// bank conflicts), double-buffered, with K one step ahead of V, and read by
+// all four waves.
 //
 // S^T = K Q^T on 32x32x16 MFMAs: A = 32 keys x 16 dims from LDS, B = the
 // wave's 32 query columns, held in registers for the whole kernel.  A's row i
@@ -180,26 +181,47 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 // max: O and l are rescaled only when some column's max grows by more than
 // 2^8, so P stays below 2^8.  P enters as bf16 (hi), and with SPLIT also as
 // the bf16 remainder (lo), carrying it to ~2^-17.
+//
+// The loop is software-pipelined: step s masks and takes the max of S(s)
+// (computed one step earlier), then issues the MFMAs of S(s + 1)
+// interleaved with the exponentials of P(s), then the PV MFMAs of step s.
 constexpr float kLazyMax = 8.0f;
-constexpr int kPageWindow = 1024;   // block-table entries staged in LDS (512 steps)
+constexpr int kPageWindow = 1024;   // block-table entries staged in LDS
+constexpr int kXcds = 8;            // accelerator complexes; workgroup i runs on XCD i % 8
+// VALU instructions of the softmax placed between consecutive S MFMAs
+constexpr int kValuPerMfma = 7;
 
-template <int D, bool SPLIT>
+template <int D, int NH, bool SPLIT>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_attn_kernel(PrefillArgs a) {
+    constexpr int KS = 32 * NH;         // keys per step
+    constexpr int PPS = KS / kPage;     // pages per step
     constexpr int PE = D * kPage;       // elements of one page of one head (K or V)
-    constexpr int KT = 2 * PE;          // a step's K (or V) tile
+    constexpr int KT = PPS * PE;        // a step's K (or V) tile
     constexpr int UPP = PE / 8;         // 16-byte units per page
-    constexpr int PER = 4 * UPP / 256;  // units of K + V per thread per step
-    __shared__ __attribute__((aligned(16))) uint16_t lds[2][2 * KT];
+    constexpr int PER = 2 * PPS * UPP / 256;   // units of K + V per thread per step
+    constexpr int WIN = kPageWindow / PPS;     // steps per block-table window
+    __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][KT];
+    __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][KT];
     __shared__ int pages[kPageWindow];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 31, hl = lane >> 5;
-    const int h = blockIdx.y, g = h / a.G;
-    const int total = a.tile_start[a.B];
-    const int x = total - 1 - (int)blockIdx.x;   // last tiles (the longest) first
-    if (x < 0) return;
+    // work item r = ((g * tiles) + i) * G + j: KV head g, the i-th tile from
+    // the end (the longest first), query head g G + j.  Each of the 8 XCDs
+    // (workgroups go to XCD blockIdx % 8) takes a contiguous share of the
+    // items, so the G query heads and the neighbouring tiles that stream the
+    // same keys and values run together and share that XCD's L2.
+    const int tiles = a.tile_start[a.B];
+    const int items = tiles * a.H_q;
+    const int share = (items + kXcds - 1) / kXcds;
+    const int kq = (int)blockIdx.x / kXcds;
+    const int r = ((int)blockIdx.x % kXcds) * share + kq;
+    if (kq >= share || r >= items) return;
+    const int g = r / (tiles * a.G);
+    const int x = tiles - 1 - (r % (tiles * a.G)) / a.G;
+    const int h = g * a.G + r % a.G;
     int lo = 0, hi = a.B - 1;
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
@@ -213,14 +235,14 @@ prefill_attn_kernel(PrefillArgs a) {
     const int p0 = L - n;                          // position of query token 0
     const int r0 = (x - a.tile_start[b]) * kPrefillRows;
     const int kv_end = p0 + min(r0 + kPrefillRows, n);   // keys [0, kv_end)
-    const int nsteps = (kv_end + 31) / 32;
+    const int nsteps = (kv_end + KS - 1) / KS;
     const int np = (L + kPage - 1) / kPage;
     const int32_t* bt = a.block_table + (int64_t)b * a.bt_stride;
 
     const int rw = r0 + 32 * w;                    // this wave's first row
     const int row = min(rw + c, n - 1);            // padding columns repeat the last row
     const int pos = p0 + row;                      // keys 0..pos are visible to this column
-    const int wave_steps = rw < n ? (p0 + min(rw + 31, n - 1)) / 32 + 1 : 0;
+    const int wave_steps = rw < n ? (p0 + min(rw + 31, n - 1)) / KS + 1 : 0;
 
     // softmax(scale * s) = softmax(|scale| * (-s)): for a negative scale the
     // query's sign bits are flipped (the host keeps |scale| >= FLT_MIN)
@@ -242,97 +264,144 @@ prefill_attn_kernel(PrefillArgs a) {
     float m = -INFINITY, l = 0.f;
     bool bad = false;
 
-    // the block-table entries of 512 steps at a time sit in LDS, refilled
-    // when no copy is in flight, so a step's pages cost two LDS reads
+    // the block-table entries of WIN steps at a time sit in LDS, refilled when
+    // no copy is in flight, so a step's pages cost LDS reads only
     auto refill = [&](int j) {
-        for (int e = tid; e < kPageWindow; e += 256) pages[e] = bt[min(2 * j + e, np - 1)];
+        for (int e = tid; e < kPageWindow; e += 256) pages[e] = bt[min(PPS * j + e, np - 1)];
         __syncthreads();
     };
-    // unit u = 256 k + tid of a step: tensor u / (2 UPP) (K, V), page
-    // (u / UPP) % 2, 16-byte unit u % UPP of that page; a wave's 64 units are
-    // consecutive and lie in one page.  The next step's units are loaded into
-    // registers while this step computes and written to LDS after it.
+    // unit u = 256 k + tid of a step: tensor u / (PPS UPP) (K, V), page
+    // (u / UPP) % PPS, 16-byte unit u % UPP of that page; a wave's 64 units
+    // are consecutive and lie in one page.  K runs one step ahead of V: while
+    // step s computes, K of step s + 2 and V of step s + 1 are loaded into
+    // registers, and written to LDS after it.
     u32x4 stage[PER];
-    auto load = [&](int j) {
-        const int e = 2 * (j % (kPageWindow / 2));
-        int pa = pages[e], pb = pages[e + 1];
-        if ((unsigned)pa >= (unsigned)a.num_pages) {
-            pa = 0;
-            bad = true;
-        }
-        if ((unsigned)pb >= (unsigned)a.num_pages) {
-            pb = 0;
-            bad = true;
-        }
+    const char* kbase = (const char*)a.k_pages + (int64_t)g * PE * 2;
+    const char* vbase = (const char*)a.v_pages + (int64_t)g * PE * 2;
+    const int64_t page_bytes = (int64_t)a.H_kv * PE * 2;
+    int64_t offk[PPS], offv[PPS];      // byte offsets of the pages of the next K / V loads
+    auto pages_of = [&](int j, int64_t (&off)[PPS]) {
+        const int e = PPS * (j % WIN);
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int ub = 256 * k + 64 * w;       // the wave's first unit
-            const int isv = ub / (2 * UPP), pp = (ub / UPP) & 1;
-            const uint16_t* src = (const uint16_t*)(isv ? a.v_pages : a.k_pages) +
-                                  ((int64_t)(pp ? pb : pa) * a.H_kv + g) * PE + (int64_t)(ub % UPP + lane) * 8;
-            stage[k] = *(const u32x4*)src;
+        for (int q = 0; q < PPS; ++q) {
+            int pg = pages[e + q];
+            if ((unsigned)pg >= (unsigned)a.num_pages) {
+                pg = 0;
+                bad = true;
+            }
+            off[q] = (int64_t)pg * page_bytes;
         }
     };
-    auto store = [&](int buf) {
+    // 256 units hold 256 / UPP pages (1 at D = 128, 2 at D = 64, where
+    // waves 2 and 3 take the second page): every array index is a constant
+    constexpr int BPP = 256 / UPP;
+    const int lane_off = ((64 * w) % UPP + lane) * 16;
+    auto load = [&](bool do_k, bool do_v) {
 #pragma unroll
-        for (int k = 0; k < PER; ++k) *(u32x4*)&lds[buf][8 * (256 * k + tid)] = stage[k];
+        for (int k = 0; k < PER; ++k) {
+            const int first = (256 * k) / UPP;                    // first page of the block
+            const bool isv = first / PPS;
+            const int pp = first % PPS;
+            const int64_t* off = isv ? offv : offk;
+            int64_t o_pg = off[pp];
+            if constexpr (BPP == 2) o_pg = (w >> 1) ? off[(pp + 1) % PPS] : o_pg;
+            if (isv ? do_v : do_k) stage[k] = *(const u32x4*)((isv ? vbase : kbase) + o_pg + lane_off);
+        }
+    };
+    // LDS swizzles, so that the lanes of one read spread over the banks: in a
+    // K page (unit = 16 slots x D/8 chunks, slot-minor) slot bit 2 is flipped
+    // by slot bit 3; in a V page (unit = one half of a dim row) the halves
+    // of dim d swap when bit 2 of d differs from bit 3
+    auto store = [&](uint16_t* kdst, uint16_t* vdst) {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int u = 256 * k + tid;
+            const int v = u % UPP;
+            if (u < PPS * UPP) {
+                if (kdst) *(u32x4*)&kdst[8 * (u ^ (((v >> 3) & 1) << 2))] = stage[k];
+            } else {
+                if (vdst) *(u32x4*)&vdst[8 * ((u - PPS * UPP) ^ (((v >> 3) ^ (v >> 4)) & 1))] = stage[k];
+            }
+        }
     };
     // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
     // 0 * NaN must not reach O, so the tail step's slots are cleared
-    auto clear_tail = [&](int s, int buf) {
-        uint16_t* V = lds[buf] + KT;
+    auto clear_tail = [&](int s, uint16_t* V) {
         for (int e = tid; e < KT; e += 256) {
-            const int key = 32 * s + 16 * (e / PE) + (e & 15);
+            const int d = (e % PE) >> 4;
+            const int half = ((e >> 3) & 1) ^ (((d >> 2) ^ (d >> 3)) & 1);
+            const int key = KS * s + 16 * (e / PE) + 8 * half + (e & 7);
             if (key >= L) V[e] = 0;
         }
     };
 
-    // lane (h, c) reads A row c = key pi(c)
+    // lane (h, c) reads A row c = key pi(c) of each 32-key half
     const int kk = 16 * (c >> 4) + 8 * ((c >> 2) & 1) + 4 * ((c >> 3) & 1) + (c & 3);
-    const int k_off = (kk >> 4) * PE + hl * (kPage * 8) + (kk & 15) * 8;
-    const int v_off = KT + c * kPage + 8 * hl;
+    const int kslot = (kk & 15) ^ (((kk >> 3) & 1) << 2);
+    const int k_off = (kk >> 4) * PE + hl * (kPage * 8) + kslot * 8;
+    const int v_off = c * kPage + 8 * (hl ^ (((c >> 2) ^ (c >> 3)) & 1));
 
+    auto qk = [&](const uint16_t* Kt, f32x16 (&sc)[NH]) {
+        const uint16_t* K = Kt + k_off;
+#pragma unroll
+        for (int hh = 0; hh < NH; ++hh) sc[hh] = f32x16{};
+#pragma unroll
+        for (int kb = 0; kb < D / 16; ++kb)
+#pragma unroll
+            for (int hh = 0; hh < NH; ++hh) {
+                const bf16x8 ka = *(const bf16x8*)(K + hh * 2 * PE + kb * (2 * kPage * 8));
+                sc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc[hh], 0, 0, 0);
+            }
+    };
+
+    // prologue: K and V of step 0, K of step 1, S of step 0
     refill(0);
-    load(0);
-    store(0);
+    pages_of(0, offk);
+#pragma unroll
+    for (int q = 0; q < PPS; ++q) offv[q] = offk[q];
+    load(true, true);
+    store(lds_k[0], lds_v[0]);
+    if (nsteps > 1) {
+        pages_of(1, offk);
+        load(true, false);
+        store(lds_k[1], nullptr);
+    }
     __syncthreads();
-    if (32 * 1 > L) {
-        clear_tail(0, 0);
+    if (KS > L) {
+        clear_tail(0, lds_v[0]);
         __syncthreads();
     }
+    f32x16 sc[NH];
+    if (0 < wave_steps) qk(lds_k[0], sc);
+
     for (int s = 0; s < nsteps; ++s) {
-        const int cur = s & 1;
-        if (s + 1 < nsteps) {
-            if ((s + 1) % (kPageWindow / 2) == 0) refill(s + 1);
-            load(s + 1);
+        // loads of this step: K of step s + 2, V of step s + 1 (whose pages
+        // are those the previous step's K load used)
+#pragma unroll
+        for (int q = 0; q < PPS; ++q) offv[q] = offk[q];
+        const bool more_k = s + 2 < nsteps, more_v = s + 1 < nsteps;
+        if (more_k) {
+            if ((s + 2) % WIN == 0) refill(s + 2);
+            pages_of(s + 2, offk);
         }
+        load(more_k, more_v);
         if (s < wave_steps) {
-            const uint16_t* K = lds[cur] + k_off;
-            f32x16 sc = f32x16{};
-#pragma unroll
-            for (int kb = 0; kb < D / 16; ++kb) {
-                const bf16x8 ka = *(const bf16x8*)(K + kb * (2 * kPage * 8));
-                sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc, 0, 0, 0);
-            }
-            // V^T operands of the step, read while the softmax runs
-            bf16x8 va[2][D / 32];
-            const uint16_t* V = lds[cur] + v_off;
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int t = 0; t < D / 32; ++t) va[u][t] = *(const bf16x8*)(V + (u * D + 32 * t) * kPage);
             // keys above a column's position are masked only on the steps
             // the wave's diagonal crosses
-            if (32 * s + 31 > p0 + rw) {
+            if (KS * s + KS - 1 > p0 + rw) {
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int key = 32 * s + 16 * (j >> 3) + 8 * hl + (j & 7);
-                    sc[j] = key <= pos ? sc[j] : -INFINITY;
-                }
+                for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int key = KS * s + 32 * hh + 16 * (j >> 3) + 8 * hl + (j & 7);
+                        sc[hh][j] = key <= pos ? sc[hh][j] : -INFINITY;
+                    }
             }
-            float mx = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+            float mx = -INFINITY;
 #pragma unroll
-            for (int j = 3; j < 16; ++j) mx = fmaxf(mx, sc[j]);
+            for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sc[hh][j]);
             mx = fmaxf(mx, swap_halves(mx));
             const float m_new = fmaxf(m, mx * sl);     // scaled units
             if (__any(m_new > m + kLazyMax)) {
@@ -342,38 +411,71 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int t = 0; t < D / 32; ++t) o[t] *= alpha;
                 m = m_new;
             }
-            uint32_t ph[8], pl[8];
+            // S of step s + 1 on the matrix cores while P of step s is formed
+            // (past a wave's last step the result is not used)
+            f32x16 scn[NH];
+            qk(lds_k[(s + 1) & 1], scn);
+            uint32_t ph[NH][8], pl[NH][8];
             float psum = 0.f;
 #pragma unroll
-            for (int j = 0; j < 16; j += 2) {
-                const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[j], sl, -m)),
-                                  __builtin_amdgcn_exp2f(__builtin_fmaf(sc[j + 1], sl, -m))};
-                psum += pq.x + pq.y;
-                const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
-                ph[j / 2] = __builtin_bit_cast(uint32_t, hi2);
-                if constexpr (SPLIT)   // the remainder is exact in fp32; rounded again
-                    pl[j / 2] = __builtin_bit_cast(uint32_t,
-                                                   __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
-            }
-            l += psum;
-            // O^T += V^T P^T, per 16-key page u and 32-dim tile t
+            for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const bf16x8 bh = __builtin_bit_cast(bf16x8, u32x4{ph[4 * u], ph[4 * u + 1], ph[4 * u + 2], ph[4 * u + 3]});
-#pragma unroll
-                for (int t = 0; t < D / 32; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[u][t], bh, o[t], 0, 0, 0);
-                if constexpr (SPLIT) {
-                    const bf16x8 bl = __builtin_bit_cast(bf16x8, u32x4{pl[4 * u], pl[4 * u + 1], pl[4 * u + 2], pl[4 * u + 3]});
-#pragma unroll
-                    for (int t = 0; t < D / 32; ++t) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[u][t], bl, o[t], 0, 0, 0);
+                for (int j = 0; j < 16; j += 2) {
+                    const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j], sl, -m)),
+                                      __builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j + 1], sl, -m))};
+                    psum += pq.x + pq.y;
+                    const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
+                    ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
+                    if constexpr (SPLIT)   // the remainder is exact in fp32; rounded again
+                        pl[hh][j / 2] = __builtin_bit_cast(
+                            uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
                 }
+            l += psum;
+            // K reads run two MFMAs ahead of the S MFMAs, with the softmax
+            // VALU work spread between them
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+            for (int i = 0; i < 8 * NH; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // an MFMA of S
+                if (i + 2 < 8 * NH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // a K read
+                __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);   // softmax VALU
             }
+            // O^T += V^T P^T, per 16-key page u of each half and 32-dim tile t
+            const uint16_t* Vt = lds_v[s & 1] + v_off;
+#pragma unroll
+            for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const bf16x8 bh = __builtin_bit_cast(
+                        bf16x8, u32x4{ph[hh][4 * u], ph[hh][4 * u + 1], ph[hh][4 * u + 2], ph[hh][4 * u + 3]});
+                    bf16x8 bl;
+                    if constexpr (SPLIT)
+                        bl = __builtin_bit_cast(
+                            bf16x8, u32x4{pl[hh][4 * u], pl[hh][4 * u + 1], pl[hh][4 * u + 2], pl[hh][4 * u + 3]});
+#pragma unroll
+                    for (int t = 0; t < D / 32; ++t) {
+                        const bf16x8 va = *(const bf16x8*)(Vt + hh * 2 * PE + (u * D + 32 * t) * kPage);
+                        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
+                        if constexpr (SPLIT) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                    }
+                }
+            // V reads run four MFMAs ahead of the PV MFMAs
+            constexpr int MF = SPLIT ? 2 : 1;
+            constexpr int NV = 2 * NH * (D / 32);
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+            for (int i = 0; i < NV; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, MF, 0);
+                if (i + 4 < NV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+#pragma unroll
+            for (int hh = 0; hh < NH; ++hh) sc[hh] = scn[hh];
         }
-        if (s + 1 < nsteps) {
-            store(cur ^ 1);
+        if (more_v) {
+            store(more_k ? lds_k[s & 1] : nullptr, lds_v[(s + 1) & 1]);
             __syncthreads();
-            if (32 * (s + 2) > L) {
-                clear_tail(s + 1, cur ^ 1);
+            if (KS * (s + 2) > L) {
+                clear_tail(s + 1, lds_v[(s + 1) & 1]);
                 __syncthreads();
             }
         }
@@ -405,15 +507,18 @@ void launch_kv_write(const WriteArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(lens_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
 }
 
+constexpr int kHalves = 2;   // 32-key halves per step: 64 keys, four pages
 void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s) {
     hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a);
-    const dim3 grid((unsigned)((a.T + kPrefillRows - 1) / kPrefillRows + a.B), (unsigned)a.H_q);
+    // an upper bound on tiles x query heads, rounded up to whole XCD rows
+    const int64_t items = ((int64_t)(a.T + kPrefillRows - 1) / kPrefillRows + a.B) * a.H_q;
+    const dim3 grid((unsigned)((items + kXcds - 1) / kXcds * kXcds));
     if (a.D == 128) {
-        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<128, true>), grid, dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((prefill_attn_kernel<128, false>), grid, dim3(256), 0, s, a);
+        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, false>), grid, dim3(256), 0, s, a);
     } else {
-        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<64, true>), grid, dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((prefill_attn_kernel<64, false>), grid, dim3(256), 0, s, a);
+        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, true>), grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, false>), grid, dim3(256), 0, s, a);
     }
 }
 
