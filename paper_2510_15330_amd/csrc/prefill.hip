@@ -188,6 +188,7 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 constexpr float kLazyMax = 8.0f;
 constexpr int kPageWindow = 1024;   // block-table entries staged in LDS
 constexpr int kXcds = 8;            // accelerator complexes; workgroup i runs on XCD i % 8
+constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 // VALU instructions of the softmax placed between consecutive S MFMAs
 constexpr int kValuPerMfma = 7;
 
@@ -275,12 +276,13 @@ prefill_attn_kernel(PrefillArgs a) {
     // are consecutive and lie in one page.  K runs one step ahead of V: while
     // step s computes, K of step s + 2 and V of step s + 1 are loaded into
     // registers, and written to LDS after it.
-    u32x4 stage[PER];
+    constexpr int PERH = PER / 2;      // units of one tensor per thread per step
+    u32x4 stage[PERH];
     const char* kbase = (const char*)a.k_pages + (int64_t)g * PE * 2;
     const char* vbase = (const char*)a.v_pages + (int64_t)g * PE * 2;
     const int64_t page_bytes = (int64_t)a.H_kv * PE * 2;
-    int64_t offk[PPS], offv[PPS];      // byte offsets of the pages of the next K / V loads
-    auto pages_of = [&](int j, int64_t (&off)[PPS]) {
+    int64_t offk[PPS];                 // byte offsets of the pages of the last K load
+    auto pages_of = [&](int j) {
         const int e = PPS * (j % WIN);
 #pragma unroll
         for (int q = 0; q < PPS; ++q) {
@@ -289,39 +291,39 @@ prefill_attn_kernel(PrefillArgs a) {
                 pg = 0;
                 bad = true;
             }
-            off[q] = (int64_t)pg * page_bytes;
+            offk[q] = (int64_t)pg * page_bytes;
         }
     };
-    // 256 units hold 256 / UPP pages (1 at D = 128, 2 at D = 64, where
-    // waves 2 and 3 take the second page): every array index is a constant
+    // unit u = 256 k + tid of one tensor's step tile: page u / UPP, 16-byte
+    // unit u % UPP of it; 256 units hold 256 / UPP pages (1 at D = 128, 2 at
+    // D = 64, where waves 2 and 3 take the second), so every index is constant
     constexpr int BPP = 256 / UPP;
     const int lane_off = ((64 * w) % UPP + lane) * 16;
-    auto load = [&](bool do_k, bool do_v) {
+    auto load = [&](const char* base) {
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int first = (256 * k) / UPP;                    // first page of the block
-            const bool isv = first / PPS;
-            const int pp = first % PPS;
-            const int64_t* off = isv ? offv : offk;
-            int64_t o_pg = off[pp];
-            if constexpr (BPP == 2) o_pg = (w >> 1) ? off[(pp + 1) % PPS] : o_pg;
-            if (isv ? do_v : do_k) stage[k] = *(const u32x4*)((isv ? vbase : kbase) + o_pg + lane_off);
+        for (int k = 0; k < PERH; ++k) {
+            const int pp = (256 * k) / UPP;
+            int64_t o_pg = offk[pp];
+            if constexpr (BPP == 2) o_pg = (w >> 1) ? offk[pp + 1] : o_pg;
+            stage[k] = *(const u32x4*)(base + o_pg + lane_off);
         }
     };
     // LDS swizzles, so that the lanes of one read spread over the banks: in a
     // K page (unit = 16 slots x D/8 chunks, slot-minor) slot bit 2 is flipped
     // by slot bit 3; in a V page (unit = one half of a dim row) the halves
     // of dim d swap when bit 2 of d differs from bit 3
-    auto store = [&](uint16_t* kdst, uint16_t* vdst) {
+    auto store_k = [&](uint16_t* dst) {
 #pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int u = 256 * k + tid;
-            const int v = u % UPP;
-            if (u < PPS * UPP) {
-                if (kdst) *(u32x4*)&kdst[8 * (u ^ (((v >> 3) & 1) << 2))] = stage[k];
-            } else {
-                if (vdst) *(u32x4*)&vdst[8 * ((u - PPS * UPP) ^ (((v >> 3) ^ (v >> 4)) & 1))] = stage[k];
-            }
+        for (int k = 0; k < PERH; ++k) {
+            const int u = 256 * k + tid, v = u % UPP;
+            *(u32x4*)&dst[8 * (u ^ (((v >> 3) & 1) << 2))] = stage[k];
+        }
+    };
+    auto store_v = [&](uint16_t* dst) {
+#pragma unroll
+        for (int k = 0; k < PERH; ++k) {
+            const int u = 256 * k + tid, v = u % UPP;
+            *(u32x4*)&dst[8 * (u ^ (((v >> 3) ^ (v >> 4)) & 1))] = stage[k];
         }
     };
     // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
@@ -356,35 +358,31 @@ prefill_attn_kernel(PrefillArgs a) {
 
     // prologue: K and V of step 0, K of step 1, S of step 0
     refill(0);
-    pages_of(0, offk);
-#pragma unroll
-    for (int q = 0; q < PPS; ++q) offv[q] = offk[q];
-    load(true, true);
-    store(lds_k[0], lds_v[0]);
+    pages_of(0);
+    load(kbase);
+    store_k(lds_k[0]);
+    load(vbase);
+    store_v(lds_v[0]);
     if (nsteps > 1) {
-        pages_of(1, offk);
-        load(true, false);
-        store(lds_k[1], nullptr);
+        pages_of(1);
+        load(kbase);
+        store_k(lds_k[1]);
     }
     __syncthreads();
     if (KS > L) {
         clear_tail(0, lds_v[0]);
         __syncthreads();
     }
-    f32x16 sc[NH];
-    if (0 < wave_steps) qk(lds_k[0], sc);
+    f32x16 sca[NH], scb[NH];
+    if (0 < wave_steps) qk(lds_k[0], sca);
 
-    for (int s = 0; s < nsteps; ++s) {
-        // loads of this step: K of step s + 2, V of step s + 1 (whose pages
-        // are those the previous step's K load used)
-#pragma unroll
-        for (int q = 0; q < PPS; ++q) offv[q] = offk[q];
+    // one step; sc holds S(s), scn receives S(s + 1)
+    auto step = [&](const int s, f32x16 (&sc)[NH], f32x16 (&scn)[NH]) {
+        // loads of this step: V of step s + 1 now (its pages are those of the
+        // last K load), K of step s + 2 once V has gone to LDS mid-step
         const bool more_k = s + 2 < nsteps, more_v = s + 1 < nsteps;
-        if (more_k) {
-            if ((s + 2) % WIN == 0) refill(s + 2);
-            pages_of(s + 2, offk);
-        }
-        load(more_k, more_v);
+        if (more_v) load(vbase);
+        uint32_t ph[NH][8], pl[NH][8];
         if (s < wave_steps) {
             // keys above a column's position are masked only on the steps
             // the wave's diagonal crosses
@@ -413,9 +411,7 @@ prefill_attn_kernel(PrefillArgs a) {
             }
             // S of step s + 1 on the matrix cores while P of step s is formed
             // (past a wave's last step the result is not used)
-            f32x16 scn[NH];
             qk(lds_k[(s + 1) & 1], scn);
-            uint32_t ph[NH][8], pl[NH][8];
             float psum = 0.f;
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh)
@@ -423,12 +419,15 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int j = 0; j < 16; j += 2) {
                     const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j], sl, -m)),
                                       __builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j + 1], sl, -m))};
-                    psum += pq.x + pq.y;
                     const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
                     ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
-                    if constexpr (SPLIT)   // the remainder is exact in fp32; rounded again
+                    if constexpr (SPLIT) {   // the remainder is exact in fp32; rounded again
+                        psum += pq.x + pq.y;
                         pl[hh][j / 2] = __builtin_bit_cast(
                             uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
+                    } else {   // P as rounded: the normaliser sums what multiplies V
+                        psum = __builtin_amdgcn_fdot2_f32_bf16(hi2, kOnes, psum, false);
+                    }
                 }
             l += psum;
             // K reads run two MFMAs ahead of the S MFMAs, with the softmax
@@ -440,6 +439,15 @@ prefill_attn_kernel(PrefillArgs a) {
                 if (i + 2 < 8 * NH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // a K read
                 __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);   // softmax VALU
             }
+        }
+        // V(s + 1) to LDS (its buffer was last read in step s - 1), then K(s + 2)
+        if (more_v) store_v(lds_v[(s + 1) & 1]);
+        if (more_k) {
+            if ((s + 2) % WIN == 0) refill(s + 2);
+            pages_of(s + 2);
+            load(kbase);
+        }
+        if (s < wave_steps) {
             // O^T += V^T P^T, per 16-key page u of each half and 32-dim tile t
             const uint16_t* Vt = lds_v[s & 1] + v_off;
 #pragma unroll
@@ -468,17 +476,20 @@ prefill_attn_kernel(PrefillArgs a) {
                 __builtin_amdgcn_sched_group_barrier(0x008, MF, 0);
                 if (i + 4 < NV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
-#pragma unroll
-            for (int hh = 0; hh < NH; ++hh) sc[hh] = scn[hh];
         }
         if (more_v) {
-            store(more_k ? lds_k[s & 1] : nullptr, lds_v[(s + 1) & 1]);
+            if (more_k) store_k(lds_k[s & 1]);
             __syncthreads();
             if (KS * (s + 2) > L) {
                 clear_tail(s + 1, lds_v[(s + 1) & 1]);
                 __syncthreads();
             }
         }
+    };
+    // unrolled by two so that S(s) and S(s + 1) alternate between register sets
+    for (int s = 0; s < nsteps; s += 2) {
+        step(s, sca, scb);
+        if (s + 1 < nsteps) step(s + 1, scb, sca);
     }
     if (bad && lane == 0) atomicOr(a.err, kErrPage);
     if (rw >= n) return;
