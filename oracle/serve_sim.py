@@ -46,13 +46,22 @@ vLLM's paged KV allocation, chunked prefill and preemption by recomputation):
 Thresholds for a controlled run come from an uncontrolled run: T1 and T2 are
 the median and 75th percentile of its per-second TBT averages (Sec. 4,
 "Default unbounded run").
+
+Controller variants (Sec. 5, "Toward novel LLM congestion control"): with
+``controller`` 2, 3 or 4 the MPC, BBR-style or PCC controller of
+``oracle.controller`` takes the tick instead, observing (samples > 0, their
+mean TBT in ns, the tokens they decoded, the tick in seconds); a tick
+without samples is still an observation for them.  Per-class policies
+("Nuanced fairness issues"): request j of class c gets
+``cap_for_class(L, r, weight[c], bypass_len[c], r_max)``.
 """
 from __future__ import annotations
 
 from collections import deque
 from dataclasses import dataclass, field
 
-from .controller import OracleController, calibrate_thresholds
+from .controller import (OracleBBR, OracleController, OracleLinear, OracleMPC, OraclePCC, calibrate_thresholds,
+                         cap_for_class)
 
 PAGE = 16
 QUEUED, PREFILL, DECODE, DONE = 1, 2, 3, 4
@@ -68,12 +77,15 @@ class SimConfig:
     tick_ns: int = 1_000_000_000
     prefill_chunk_tokens: int = 0
     watermark_pages: int = 0
-    controller: bool = False
+    controller: int = 0          # 0 none, 1 linear, 2 MPC, 3 BBR-style, 4 PCC
     t1: float = 0.0
     t2: float = 0.0
     window: int = 5
     r_min: float = 0.05
     r_max: float = 0.20
+    ctl_params: dict = field(default_factory=dict)   # variant parameters (oracle.controller names)
+    class_weight: tuple = (1.0,)                      # per class: r multiplier
+    class_bypass: tuple = (0,)                        # per class: lengths at or below are not reduced
 
 
 @dataclass
@@ -94,15 +106,31 @@ def ceil_pages(tokens):
     return -(-int(tokens) // PAGE)
 
 
-def simulate(arrival_ns, prompt, length, cfg: SimConfig) -> SimResult:
+def make_controller(cfg: SimConfig):
+    k = int(cfg.controller)
+    if k == 0:
+        return None
+    if k == 1:
+        return OracleLinear(cfg.t1, cfg.t2, cfg.window, cfg.r_min, cfg.r_max)
+    if k == 2:
+        return OracleMPC(cfg.t1, cfg.t2, window=cfg.window, r_min=cfg.r_min, r_max=cfg.r_max, **cfg.ctl_params)
+    if k == 3:
+        return OracleBBR(r_max=cfg.r_max, **cfg.ctl_params)
+    if k == 4:
+        return OraclePCC(cfg.t1, cfg.t2, r_max=cfg.r_max, **cfg.ctl_params)
+    raise ValueError(f"controller {k}")
+
+
+def simulate(arrival_ns, prompt, length, cfg: SimConfig, cls=None) -> SimResult:
     n = len(arrival_ns)
     arrival_ns = [int(v) for v in arrival_ns]
     prompt = [int(v) for v in prompt]
     length = [int(v) for v in length]
+    cls = [0] * n if cls is None else [int(v) for v in cls]
     for j in range(n):
         if ceil_pages(prompt[j] + length[j]) + cfg.watermark_pages > cfg.kv_capacity_pages:
             raise ValueError(f"request {j} does not fit the page budget")
-    ctl = OracleController(cfg.t1, cfg.t2, cfg.window, cfg.r_min, cfg.r_max) if cfg.controller else None
+    ctl = make_controller(cfg)
     res = SimResult([0] * n, [0.0] * n, [-1] * n, [-1] * n, [-1] * n, [0] * n)
     state = [0] * n
     gen = [0] * n
@@ -123,13 +151,16 @@ def simulate(arrival_ns, prompt, length, cfg: SimConfig) -> SimResult:
             ta = arrival_ns[i] if i < n else None
             if next_tick <= now and (ta is None or next_tick <= ta):
                 s, c = windows.pop(next_tick // cfg.tick_ns, (0, 0))
-                if ctl is not None and c > 0:
-                    ctl.push(s / c)
+                if ctl is not None:
+                    # mean TBT in ns (the thresholds' unit), tokens, tick in seconds
+                    ctl.observe(c > 0, s / c if c > 0 else 0.0, float(c), cfg.tick_ns / 1e9)
                 res.ticks.append((next_tick, c, s, ctl.r if ctl else 0.0, len(queue), len(running)))
                 next_tick += cfg.tick_ns
                 continue
             if ta is not None and ta <= now:
-                res.target[i] = ctl.cap(length[i]) if ctl else length[i]
+                k = cls[i]
+                res.target[i] = (cap_for_class(length[i], ctl.r, cfg.class_weight[k], cfg.class_bypass[k], cfg.r_max)
+                                 if ctl else length[i])
                 res.r_at_queue[i] = ctl.r if ctl else 0.0
                 state[i] = QUEUED
                 queue.append(i)
