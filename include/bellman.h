@@ -276,6 +276,109 @@ int32_t bellman_length_cap(const bellman_load_signal_t *load_signal);
  * (fractional rank p/100 * (n - 1)).  Host arrays; n >= 1. */
 int bellman_calibrate_thresholds(const double *tbt, int64_t n, double *t1, double *t2);
 
+/* ------------------------------------------------- controller variants --
+ * The controllers the paper's future-work section names (Sec. 5, "Toward
+ * novel LLM congestion control") and per-class policies ("Nuanced fairness
+ * issues").  The paper gives their goals, not algorithms; these are this
+ * library's readings.  A variant observes one tick at a time
+ * (bellman_controller_observe): whether TBT samples arrived, their mean
+ * tbt (same unit as t1, t2), the tokens they decoded and the tick length.
+ *
+ * MPC (BELLMAN_CTL_MPC): on a tick with samples, once `window` samples exist
+ *   a least-squares line through the last `window` gives slope s (per tick)
+ *   and value v at the newest (before that s = 0, v = the newest sample); the
+ *   floor b is the least of the last floor_window samples.  For a candidate
+ *   rc, h ticks ahead:  u_h = max(v + s h, b);  f_h = 1 - exp(-h / tau)
+ *   (the share of decode work from requests capped at rc);
+ *   y_h = b + (u_h - b) ((1 - f_h) + f_h (1 - rc) / (1 - r)), and
+ *   J = sum_{h=1..horizon} w_lat (max(0, y_h - t1) / (t2 - t1))^2
+ *       + horizon (w_quality - w_energy) rc + w_delta ((rc - r) / r_max)^2.
+ *   Candidates 0, r_min, r_min + step, ... (below r_max), r_max; the first
+ *   with the least J becomes r.  Needs t2 > t1.
+ * BBR-style (BELLMAN_CTL_BBR): x = tokens / tick_s each tick; BtlBw = max x of
+ *   the last bw_window ticks; RTprop = min TBT of the last rt_window ticks
+ *   with samples.  On a tick with samples: if TBT > RTprop (1 + margin) and
+ *   x >= (1 - margin) BtlBw, r_base += bbr_step (at most r_max); else if
+ *   TBT <= RTprop (1 + margin / 2), r_base -= bbr_step (at least 0).  Applied
+ *   r = clamp(r_base + o, 0, r_max) with o = -probe on the first tick of each
+ *   `cycle`-tick cycle, +probe on the second, 0 otherwise.
+ * PCC (BELLMAN_CTL_PCC): rounds of two monitor intervals of `interval` ticks
+ *   at center + epsilon and center - epsilon (clamped to [0, r_max]), up
+ *   first in even rounds and down first in odd ones.  An interval's utility
+ *   U = -pcc_w_lat max(0, mean TBT - t1) / (t2 - t1) - pcc_w_quality r / r_max
+ *   (no latency term without samples); after a round
+ *   center = clamp(center + gain (U_a - U_b) / (r_a - r_b), 0, r_max)
+ *   (no step when the two rates coincide).  r is the running interval's rate.
+ *   Needs t2 > t1.
+ * Linear (BELLMAN_CTL_LINEAR): the controller above; a tick pushes its mean
+ *   TBT when it has samples.
+ * Arithmetic is binary64 in the order stated, without fused multiply-adds.
+ */
+typedef enum bellman_ctl_kind {
+    BELLMAN_CTL_LINEAR = 1,
+    BELLMAN_CTL_MPC = 2,
+    BELLMAN_CTL_BBR = 3,
+    BELLMAN_CTL_PCC = 4
+} bellman_ctl_kind_t;
+
+typedef struct bellman_ctl_params {
+    int32_t kind;                 /* bellman_ctl_kind_t */
+    int32_t window;               /* linear: MA samples; MPC: trend-fit samples (>= 1) */
+    double t1, t2;                /* TBT thresholds (linear, MPC, PCC) */
+    double r_min, r_max;          /* 0 <= r_min <= r_max < 1 */
+    int32_t horizon;              /* MPC: ticks predicted (>= 1) */
+    int32_t floor_window;         /* MPC: samples behind the TBT floor (>= 1) */
+    double tau;                   /* MPC: ticks for a new rate to reach the load (> 0) */
+    double w_lat, w_quality, w_energy, w_delta;   /* MPC cost weights (>= 0) */
+    double step;                  /* MPC: candidate spacing (> 0) */
+    int32_t bw_window, rt_window; /* BBR: ticks behind BtlBw and RTprop (>= 1) */
+    int32_t cycle;                /* BBR: probe / drain cycle, ticks (>= 1) */
+    int32_t reserved0;            /* 0 */
+    double margin;                /* BBR: queueing margin over RTprop, in [0, 1) */
+    double bbr_step, probe;       /* BBR: r_base step per tick, probe offset (>= 0) */
+    int32_t interval;             /* PCC: ticks per monitor interval (>= 1) */
+    int32_t reserved1;            /* 0 */
+    double epsilon, gain;         /* PCC: rate offset of an experiment, gradient step (>= 0) */
+    double pcc_w_lat, pcc_w_quality;  /* PCC utility weights (>= 0) */
+} bellman_ctl_params_t;
+
+/* Fill *p with the defaults of `kind` and thresholds t1, t2: window 5,
+ * r in [0.05, 0.20]; MPC horizon 10, floor_window 60, tau 20, weights
+ * 1 / 0.25 / 0.1 / 0.2, step 0.01; BBR windows 10 and 30, cycle 8, margin
+ * 0.25, step 0.02, probe 0.02; PCC interval 10, epsilon 0.02, gain 0.02,
+ * weights 1 / 0.5.  Returns 0 or BELLMAN_ERR_INVALID_ARG. */
+int bellman_ctl_params_default(int32_t kind, double t1, double t2, bellman_ctl_params_t *p);
+
+/* A controller of any kind (destroy with bellman_controller_destroy), or
+ * NULL on invalid parameters. */
+bellman_controller_t *bellman_controller_create_ex(const bellman_ctl_params_t *p);
+
+typedef struct bellman_ctl_obs {
+    int32_t has_sample;           /* 1: TBT samples arrived in the tick */
+    int32_t reserved;             /* 0 */
+    double tbt_avg;               /* their mean (finite when has_sample) */
+    double tokens;                /* tokens they decoded (>= 0) */
+    double tick_s;                /* tick length in seconds (> 0) */
+} bellman_ctl_obs_t;
+
+/* Feed one tick; returns the new rate r (>= 0) or a negative status (NULL
+ * arguments, non-finite sample, negative tokens, tick_s <= 0).
+ * bellman_length_cap's sample is a tick with no token count. */
+double bellman_controller_observe(bellman_controller_t *ctl, const bellman_ctl_obs_t *obs);
+
+typedef struct bellman_class_policy {
+    double weight;                /* the class applies min(weight r, r_max); 0 exempts it */
+    int32_t bypass_len;           /* predicted lengths at or below this are not reduced */
+    int32_t reserved;             /* 0 */
+} bellman_class_policy_t;
+
+/* Length cap for a request of a class: N = L when L <= bypass_len, else
+ * N = max(1, floor(L (1 - rc) + 0.5)) with rc = min(weight r, r_max)
+ * (N = L when rc = 0 or L = 0).  Negative status on NULL arguments, L < 0
+ * or a negative or non-finite weight. */
+int32_t bellman_length_cap_class(const bellman_controller_t *ctl, int32_t predicted_len,
+                                 const bellman_class_policy_t *policy);
+
 /* ------------------------------------------- closed-loop serving model --
  * A discrete-event model of the paper's evaluation (Sec. 4, "Setup and
  * trace", "Default unbounded run", "beLLMan in action"): requests arrive
@@ -288,10 +391,10 @@ int bellman_calibrate_thresholds(const double *tbt, int64_t n, double *t1, doubl
  * arithmetic in integer nanoseconds; each iteration, in this order:
  *  1. Ticks (k * tick_ns) and arrivals up to the current time, in time order,
  *     a tick first on ties.  A tick averages the TBT samples of the tokens
- *     decoded in ((k-1) tick_ns, k tick_ns] and pushes the average to the
- *     controller (nothing for a second without samples).  An arrival is
- *     queued with target N = bellman_length_cap(L) under the current rate
- *     (N = L without a controller).
+ *     decoded in ((k-1) tick_ns, k tick_ns] and gives the controller that
+ *     tick (the linear controller takes only ticks with samples).  An
+ *     arrival is queued with target N = bellman_length_cap_class(L) under
+ *     the current rate and its class's policy (N = L without a controller).
  *  2. First-come first-served admission while fewer than max_running run: the
  *     queue head must prefill P = prompt + generated tokens (generated > 0
  *     after a preemption) and is admitted if ceil(P / 16) pages can be taken
@@ -317,7 +420,10 @@ int bellman_calibrate_thresholds(const double *tbt, int64_t n, double *t1, doubl
  */
 typedef enum bellman_sim_controller_kind {
     BELLMAN_SIM_NO_CONTROL = 0,   /* targets = predicted lengths */
-    BELLMAN_SIM_LINEAR = 1        /* the paper's linear controller (t1, t2, window, r_min, r_max) */
+    BELLMAN_SIM_LINEAR = 1,       /* the paper's linear controller (t1, t2, window, r_min, r_max) */
+    BELLMAN_SIM_MPC = 2,          /* controller variants (see above); each tick is an observation */
+    BELLMAN_SIM_BBR = 3,          /* with the tick's TBT samples, their mean, the tokens they */
+    BELLMAN_SIM_PCC = 4           /* decoded and tick_ns / 1e9 seconds */
 } bellman_sim_controller_kind_t;
 
 typedef struct bellman_sim_config {
@@ -340,6 +446,12 @@ typedef struct bellman_sim_config {
     int32_t live_head_dim;        /* live: 64 or 128 */
     int32_t reserved;             /* 0 */
     void *stream;                 /* live: hipStream_t for the kernels (NULL = null stream) */
+    const bellman_ctl_params_t *ctl_params;  /* controller parameters, kind = controller; NULL:
+                                                the defaults with t1, t2, window, r_min, r_max above */
+    const int32_t *req_class;     /* per-request class in [0, n_classes), or NULL (all class 0) */
+    const bellman_class_policy_t *classes;   /* n_classes policies, or NULL (weight 1, no bypass) */
+    int32_t n_classes;            /* >= 1 when req_class or classes is given */
+    int32_t reserved2;            /* 0 */
 } bellman_sim_config_t;
 
 typedef struct bellman_sim_request {

@@ -43,6 +43,33 @@ class PrefillOpts(ctypes.Structure):
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
+CTL_LINEAR, CTL_MPC, CTL_BBR, CTL_PCC = 1, 2, 3, 4
+
+
+class CtlParams(ctypes.Structure):
+    _fields_ = [
+        ("kind", ctypes.c_int32), ("window", ctypes.c_int32),
+        ("t1", ctypes.c_double), ("t2", ctypes.c_double), ("r_min", ctypes.c_double), ("r_max", ctypes.c_double),
+        ("horizon", ctypes.c_int32), ("floor_window", ctypes.c_int32), ("tau", ctypes.c_double),
+        ("w_lat", ctypes.c_double), ("w_quality", ctypes.c_double), ("w_energy", ctypes.c_double),
+        ("w_delta", ctypes.c_double), ("step", ctypes.c_double),
+        ("bw_window", ctypes.c_int32), ("rt_window", ctypes.c_int32), ("cycle", ctypes.c_int32),
+        ("reserved0", ctypes.c_int32), ("margin", ctypes.c_double), ("bbr_step", ctypes.c_double),
+        ("probe", ctypes.c_double), ("interval", ctypes.c_int32), ("reserved1", ctypes.c_int32),
+        ("epsilon", ctypes.c_double), ("gain", ctypes.c_double), ("pcc_w_lat", ctypes.c_double),
+        ("pcc_w_quality", ctypes.c_double),
+    ]
+
+
+class CtlObs(ctypes.Structure):
+    _fields_ = [("has_sample", ctypes.c_int32), ("reserved", ctypes.c_int32), ("tbt_avg", ctypes.c_double),
+                ("tokens", ctypes.c_double), ("tick_s", ctypes.c_double)]
+
+
+class ClassPolicy(ctypes.Structure):
+    _fields_ = [("weight", ctypes.c_double), ("bypass_len", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
 class LoadSignal(ctypes.Structure):
     _fields_ = [
         ("controller", ctypes.c_void_p),
@@ -86,6 +113,15 @@ def library():
     lib.bellman_controller_create.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_int32,
                                               ctypes.c_double, ctypes.c_double]
     lib.bellman_controller_create.restype = P
+    lib.bellman_ctl_params_default.argtypes = [ctypes.c_int32, ctypes.c_double, ctypes.c_double,
+                                               ctypes.POINTER(CtlParams)]
+    lib.bellman_ctl_params_default.restype = ctypes.c_int
+    lib.bellman_controller_create_ex.argtypes = [ctypes.POINTER(CtlParams)]
+    lib.bellman_controller_create_ex.restype = P
+    lib.bellman_controller_observe.argtypes = [P, ctypes.POINTER(CtlObs)]
+    lib.bellman_controller_observe.restype = ctypes.c_double
+    lib.bellman_length_cap_class.argtypes = [P, ctypes.c_int32, ctypes.POINTER(ClassPolicy)]
+    lib.bellman_length_cap_class.restype = ctypes.c_int32
     lib.bellman_controller_destroy.argtypes = [P]
     lib.bellman_controller_destroy.restype = None
     lib.bellman_controller_rate.argtypes = [P]
@@ -278,6 +314,57 @@ def length_cap(controller: Controller, predicted_len: int, tbt_avg: float | None
     if n < 0:
         raise BellmanError(n, "invalid load signal")
     return n
+
+
+def ctl_params(kind, t1=0.0, t2=0.0, **overrides) -> CtlParams:
+    """bellman_ctl_params_default for `kind`, then the given fields."""
+    p = CtlParams()
+    _check(library().bellman_ctl_params_default(int(kind), float(t1), float(t2), ctypes.byref(p)))
+    for k, v in overrides.items():
+        if k not in dict(CtlParams._fields_):
+            raise TypeError(f"unknown controller parameter {k!r}")
+        setattr(p, k, v)
+    return p
+
+
+class VariantController:
+    """A controller of any kind (bellman_controller_create_ex), fed one tick
+    at a time with observe()."""
+
+    def __init__(self, kind, t1=0.0, t2=0.0, **overrides):
+        self.params = ctl_params(kind, t1, t2, **overrides)
+        self._h = library().bellman_controller_create_ex(ctypes.byref(self.params))
+        if not self._h:
+            raise BellmanError(-1, "invalid controller parameters")
+
+    def close(self):
+        if self._h:
+            library().bellman_controller_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def rate(self) -> float:
+        return library().bellman_controller_rate(self._h)
+
+    def observe(self, has_sample, tbt=0.0, tokens=0.0, tick_s=1.0) -> float:
+        o = CtlObs(int(bool(has_sample)), 0, float(tbt), float(tokens), float(tick_s))
+        r = library().bellman_controller_observe(self._h, ctypes.byref(o))
+        if r < 0:
+            raise BellmanError(int(r), last_error() or "controller rejected the tick")
+        return r
+
+    def cap(self, predicted_len, weight=1.0, bypass_len=0) -> int:
+        pol = ClassPolicy(float(weight), int(bypass_len), 0)
+        n = library().bellman_length_cap_class(self._h, int(predicted_len), ctypes.byref(pol))
+        if n < 0:
+            raise BellmanError(n, "length cap rejected its arguments")
+        return n
 
 
 def calibrate_thresholds(tbt):

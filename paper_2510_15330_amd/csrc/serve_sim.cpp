@@ -173,8 +173,16 @@ int check_config(const bellman_sim_config_t* c) {
     if (c->fixed_ns < 0 || c->attn_ps_per_token < 0 || c->prefill_ps_per_token < 0 || c->prefill_chunk_tokens < 0)
         return set_error(BELLMAN_ERR_INVALID_ARG, "sim: negative time coefficient or chunk");
     if (c->tick_ns < 1) return set_error(BELLMAN_ERR_INVALID_ARG, "sim: tick_ns must be >= 1");
-    if (c->controller != BELLMAN_SIM_NO_CONTROL && c->controller != BELLMAN_SIM_LINEAR)
+    if (c->controller < BELLMAN_SIM_NO_CONTROL || c->controller > BELLMAN_SIM_PCC)
         return set_error(BELLMAN_ERR_INVALID_ARG, "sim: unknown controller kind %d", c->controller);
+    if (c->ctl_params && c->ctl_params->kind != c->controller)
+        return set_error(BELLMAN_ERR_INVALID_ARG, "sim: controller parameters of kind %d for controller %d",
+                         c->ctl_params->kind, c->controller);
+    if ((c->req_class || c->classes) && c->n_classes < 1)
+        return set_error(BELLMAN_ERR_INVALID_ARG, "sim: classes given with n_classes %d", c->n_classes);
+    for (int32_t k = 0; c->classes && k < c->n_classes; ++k)
+        if (!(c->classes[k].weight >= 0.0) || !isfinite(c->classes[k].weight))
+            return set_error(BELLMAN_ERR_INVALID_ARG, "sim: class %d weight %g", k, c->classes[k].weight);
     if (c->live) {
         if (c->live_layers < 1) return set_error(BELLMAN_ERR_INVALID_ARG, "sim: live_layers must be >= 1");
         if (c->live_head_dim != 64 && c->live_head_dim != 128)
@@ -216,14 +224,28 @@ extern "C" int bellman_sim_run(const bellman_sim_config_t* cfg, int64_t n, const
                              (long long)j, (long long)need, (long long)cfg->kv_capacity_pages,
                              (long long)cfg->watermark_pages);
         max_pages = std::max(max_pages, need);
+        if (cfg->req_class && (cfg->req_class[j] < 0 || cfg->req_class[j] >= cfg->n_classes))
+            return set_error(BELLMAN_ERR_INVALID_ARG, "sim: request %lld has class %d of %d", (long long)j,
+                             cfg->req_class[j], cfg->n_classes);
     }
     memset(stats, 0, sizeof *stats);
 
     bellman_controller_t* ctl = nullptr;
-    if (cfg->controller == BELLMAN_SIM_LINEAR) {
-        ctl = bellman_controller_create(cfg->t1, cfg->t2, cfg->window, cfg->r_min, cfg->r_max);
+    if (cfg->controller != BELLMAN_SIM_NO_CONTROL) {
+        bellman_ctl_params_t p;
+        if (cfg->ctl_params) {
+            p = *cfg->ctl_params;
+        } else {
+            bellman_ctl_params_default(cfg->controller, cfg->t1, cfg->t2, &p);
+            p.window = cfg->window;
+            p.r_min = cfg->r_min;
+            p.r_max = cfg->r_max;
+        }
+        ctl = bellman_controller_create_ex(&p);
         if (!ctl) return set_error(BELLMAN_ERR_INVALID_ARG, "sim: invalid controller parameters");
     }
+    const bellman_class_policy_t default_class{1.0, 0, 0};
+    const double tick_s = (double)cfg->tick_ns / 1e9;
     struct CtlGuard {
         bellman_controller_t* c;
         ~CtlGuard() {
@@ -303,9 +325,10 @@ extern "C" int bellman_sim_run(const bellman_sim_config_t* cfg, int64_t n, const
                     c = it->second.second;
                     windows.erase(it);
                 }
-                if (ctl && c > 0) {
-                    bellman_load_signal_t sig{ctl, 1, (double)s / (double)c, 0};
-                    if (bellman_length_cap(&sig) < 0) return set_error(BELLMAN_ERR_INVALID_ARG, "sim: controller rejected a sample");
+                if (ctl) {
+                    const bellman_ctl_obs_t obs{c > 0 ? 1 : 0, 0, c > 0 ? (double)s / (double)c : 0.0, (double)c, tick_s};
+                    if (bellman_controller_observe(ctl, &obs) < 0.0)
+                        return set_error(BELLMAN_ERR_INVALID_ARG, "sim: controller rejected a tick");
                 }
                 if (stats->ticks < max_ticks)
                     ticks[stats->ticks] = bellman_sim_tick_t{next_tick, c, s, rate(), (int32_t)queue.size(), (int32_t)running.size()};
@@ -316,8 +339,9 @@ extern "C" int bellman_sim_run(const bellman_sim_config_t* cfg, int64_t n, const
             if (more && arrival_ns[i] <= now) {
                 int32_t Nt = length[i];
                 if (ctl) {
-                    bellman_load_signal_t sig{ctl, 0, 0.0, length[i]};
-                    Nt = bellman_length_cap(&sig);
+                    const int32_t k = cfg->req_class ? cfg->req_class[i] : 0;
+                    Nt = bellman_length_cap_class(ctl, length[i], cfg->classes ? &cfg->classes[k] : &default_class);
+                    if (Nt < 0) return set_error(BELLMAN_ERR_INVALID_ARG, "sim: length cap failed");
                 }
                 target[(size_t)i] = Nt;
                 requests[i].target = Nt;

@@ -14,7 +14,7 @@ import numpy as np
 
 from . import _binding
 
-NO_CONTROL, LINEAR = 0, 1
+NO_CONTROL, LINEAR, MPC, BBR, PCC = 0, 1, 2, 3, 4
 
 
 class SimConfig(ctypes.Structure):
@@ -29,6 +29,9 @@ class SimConfig(ctypes.Structure):
         ("live", ctypes.c_int32), ("live_layers", ctypes.c_int32), ("live_q_heads", ctypes.c_int32),
         ("live_kv_heads", ctypes.c_int32), ("live_head_dim", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("stream", ctypes.c_void_p),
+        ("ctl_params", ctypes.POINTER(_binding.CtlParams)), ("req_class", ctypes.c_void_p),
+        ("classes", ctypes.POINTER(_binding.ClassPolicy)), ("n_classes", ctypes.c_int32),
+        ("reserved2", ctypes.c_int32),
     ]
 
 
@@ -107,12 +110,37 @@ def make_config(stream=None, **kw) -> SimConfig:
     return c
 
 
-def run(trace, stream=None, max_ticks=None, max_iterations=0, **kw) -> SimOutput:
+def run(trace, stream=None, max_ticks=None, max_iterations=0, ctl_params=None, cls=None, classes=None,
+        **kw) -> SimOutput:
+    """``ctl_params``: parameter overrides of the controller variant (names of
+    bellman_ctl_params_t; defaults otherwise, with t1, t2, window, r_min,
+    r_max taken from the keywords); ``cls``: per-request class; ``classes``:
+    a (weight, bypass_len) policy per class."""
     arr = np.ascontiguousarray(trace.arrival_ns, dtype=np.int64)
     prompt = np.ascontiguousarray(trace.prompt, dtype=np.int32)
     length = np.ascontiguousarray(trace.length, dtype=np.int32)
     n = len(arr)
     cfg = make_config(stream=stream, **kw)
+    keep = []
+    if ctl_params is not None:
+        base = {k: kw[k] for k in ("window", "r_min", "r_max") if k in kw}
+        base.update(ctl_params)
+        p = _binding.ctl_params(cfg.controller, cfg.t1, cfg.t2, **{k: v for k, v in base.items()})
+        keep.append(p)
+        cfg.ctl_params = ctypes.pointer(p)
+    if cls is not None:
+        c = np.ascontiguousarray(cls, dtype=np.int32)
+        if c.shape != (n,):
+            raise ValueError("cls must give one class per request")
+        keep.append(c)
+        cfg.req_class = c.ctypes.data
+    if classes is not None:
+        arrp = (_binding.ClassPolicy * len(classes))(*[_binding.ClassPolicy(float(w), int(b), 0) for w, b in classes])
+        keep.append(arrp)
+        cfg.classes = arrp
+        cfg.n_classes = len(classes)
+    elif cls is not None:
+        cfg.n_classes = int(np.max(cls)) + 1 if n else 1
     if max_ticks is None:
         max_ticks = 1 << 16
     req = np.zeros(n, dtype=REQUEST_DTYPE)
