@@ -279,6 +279,65 @@ def paper_experiment(seed=0, live=False, stream=None, capacity_rps=PAPER_CAPACIT
     return s, (tr, unb, bnd)
 
 
+CONTROLLER_NAMES = {NO_CONTROL: "none", LINEAR: "linear", MPC: "mpc", BBR: "bbr", PCC: "pcc"}
+
+
+def run_metrics(trace, out: SimOutput, base: SimOutput | None = None):
+    """Latency, control activity, output kept and busy time of one run."""
+    arr = trace.arrival_ns.astype(np.float64) / 1e9
+    r = out.requests
+    e2e = r["finish_ns"] / 1e9 - arr
+    ttft = r["first_ns"] / 1e9 - arr
+    rs = out.ticks["r"]
+    busy_s = float(out.log["dt_ns"].sum()) / 1e9 if len(out.log) else float("nan")
+    m = {
+        "e2e_p50_s": float(np.median(e2e)), "e2e_p99_s": float(np.percentile(e2e, 99)),
+        "e2e_max_s": float(e2e.max()), "ttft_p99_s": float(np.percentile(ttft, 99)),
+        "queue_max_s": float((r["admit_ns"] / 1e9 - arr).max()),
+        "control_active_fraction": float((rs > 0).mean()) if len(rs) else 0.0,
+        "rate_switches": int(np.count_nonzero(np.diff((rs > 0).astype(np.int8)))) if len(rs) else 0,
+        "mean_abs_rate_change": float(np.abs(np.diff(rs)).mean()) if len(rs) > 1 else 0.0,
+        "mean_r": float(r["r_at_queue"].mean()),
+        "output_kept": float(r["target"].sum() / trace.length.sum()),
+        "busy_s": busy_s,
+        "end_s": out.end_ns / 1e9,
+        "preemptions": out.preemptions,
+    }
+    if base is not None and len(base.log) and len(out.log):
+        m["busy_vs_uncontrolled"] = busy_s / (float(base.log["dt_ns"].sum()) / 1e9)
+    return m
+
+
+def compare_controllers(seed=0, duration_s=None, capacity_rps=PAPER_CAPACITY_RPS, kinds=(LINEAR, MPC, BBR, PCC),
+                        cls=None, classes=None, log=None, **server):
+    """Uncontrolled run, thresholds from it, then one run per controller kind
+    on the same trace (model mode); returns {name: metrics}."""
+    from . import traces
+    cfg = dict(PAPER_SERVER)
+    cfg.update(server)
+    cfg = {k: v for k, v in cfg.items() if not k.startswith("live")}
+    tr = traces.paper_trace(capacity_rps, seed=seed, duration_s=duration_s)
+    big = 1 << 23
+    unb = run(tr, controller=NO_CONTROL, max_iterations=big, **cfg)
+    t1, t2 = thresholds(unb)
+    res = {"none": run_metrics(tr, unb), "t1_ms": t1 / 1e6, "t2_ms": t2 / 1e6, "requests": len(tr)}
+    for k in kinds:
+        out = run(tr, controller=k, t1=t1, t2=t2, max_iterations=big, cls=cls, classes=classes, **cfg)
+        res[CONTROLLER_NAMES[k]] = run_metrics(tr, out, unb)
+        if cls is not None:
+            per = {}
+            for c in np.unique(cls):
+                sel = np.asarray(cls) == c
+                e2e = out.requests["finish_ns"][sel] / 1e9 - tr.arrival_ns[sel] / 1e9
+                per[int(c)] = {"requests": int(sel.sum()),
+                               "output_kept": float(out.requests["target"][sel].sum() / tr.length[sel].sum()),
+                               "e2e_p50_s": float(np.median(e2e))}
+            res[CONTROLLER_NAMES[k]]["classes"] = per
+        if log:
+            log(f"[serve] {CONTROLLER_NAMES[k]}: done")
+    return res
+
+
 def main():
     import argparse
     import json
@@ -286,12 +345,18 @@ def main():
     ap.add_argument("--live", action="store_true", help="time the real kernels on the GPU for the attention term")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--duration", type=float, default=None, help="trace length in seconds (default: all 1320 s)")
+    ap.add_argument("--compare", action="store_true",
+                    help="model mode: the linear, MPC, BBR-style and PCC controllers on the same trace")
     args = ap.parse_args()
+    import sys
+    if args.compare:
+        print(json.dumps(compare_controllers(seed=args.seed, duration_s=args.duration,
+                                             log=lambda m: print(m, file=sys.stderr, flush=True))), flush=True)
+        return
     stream = None
     if args.live:
         import torch
         stream = torch.cuda.current_stream().cuda_stream
-    import sys
     s, _ = paper_experiment(seed=args.seed, live=args.live, stream=stream, duration_s=args.duration,
                             log=lambda m: print(m, file=sys.stderr, flush=True))
     print(json.dumps(s), flush=True)
