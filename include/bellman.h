@@ -184,7 +184,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
  * n_b - 1 (page block_table[b][pos / 16], slot pos % 16), then set
  * seq_lens[b] += n_b.
  *   k_new, v_new  [T, H_kv, D] in the pools' element type, innermost
- *                 contiguous (k_new rows 16-byte aligned); T = q_start[B].
+ *                 contiguous, rows 16-byte aligned; T = q_start[B].
  *   k_pages, v_pages, block_table: as for bellman_kv_append; the pages of
  *                 every new position must already be assigned.
  *   seq_lens      int32 [B] contiguous (read, then advanced).

@@ -499,7 +499,7 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     const int64_t T = k_new->shape[0];
     const size_t eb = ps.fp8 ? 1 : 2;
     if ((rc = check_rows(k_new, "k_new", k_pages->dtype, T, ps.H_kv, ps.D, 16))) return rc;
-    if ((rc = check_rows(v_new, "v_new", k_pages->dtype, T, ps.H_kv, ps.D, eb))) return rc;
+    if ((rc = check_rows(v_new, "v_new", k_pages->dtype, T, ps.H_kv, ps.D, 16))) return rc;
     if ((rc = check_seq_lens(seq_lens, seq_lens ? seq_lens->shape[0] : 0))) return rc;
     const int64_t B = seq_lens->shape[0];
     if ((rc = check_block_table(block_table, B))) return rc;
@@ -507,10 +507,12 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     if (T > INT32_MAX || B > INT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "too many tokens or requests");
     if (T == 0 || B == 0) return BELLMAN_OK;
 
+    if (T / 16 + 2 * B + 1 > (int64_t)UINT32_MAX) return fail(BELLMAN_ERR_UNSUPPORTED, "too many tokens or requests");
+
     int dev;
     if ((rc = current_device(&dev))) return rc;
     char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), &base))) return rc;
     WriteArgs a;
     a.k_new = k_new->data;
     a.v_new = v_new->data;
@@ -532,7 +534,7 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     a.D = ps.D;
     a.max_pages = (int)block_table->shape[1];
     a.elem_bytes = (int)eb;
-    launch_kv_write(a, (hipStream_t)stream);
+    launch_kv_write(a, (int32_t*)(base + sizeof(WorkspaceHeader)), (hipStream_t)stream);
     return launch_status("kv_write");
 }
 

@@ -110,7 +110,7 @@ void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 // Prefill launchers (prefill.hip).
-void launch_kv_write(const WriteArgs& a, hipStream_t s);
+void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
 void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s);
 
 // Record the calling thread's last-error text (bellman_last_error) and

@@ -33,57 +33,145 @@ __device__ __forceinline__ float swap_halves(float x) {  // value of lane l ^ 32
     return __uint_as_float((threadIdx.x & 32) ? r[0] : r[1]);
 }
 
-// Request whose range [q_start[b], q_start[b+1]) holds token i (q_start
-// non-decreasing), or -1.
-__device__ __forceinline__ int find_request(const int32_t* q_start, int B, int i) {
-    int lo = 0, hi = B - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (q_start[mid] <= i) lo = mid;
-        else hi = mid - 1;
+// ----------------------------------------------------------- prompt write --
+// Work is cut by (request, page the request's new positions touch, KV head):
+// write_plan_kernel scans the touched-page counts of the requests into
+// page_start[0..B]; kv_write_kernel takes one item per workgroup.  A K page
+// [D/x chunks][16 slots][x] takes 16-byte units with consecutive threads on
+// consecutive slots; the V rows of the page's tokens go through LDS and
+// leave as 16-byte runs of the dim-major V page [D][16 slots] (element by
+// element where the page is only partly written).  Lengths are advanced
+// afterwards by lens_kernel, so every item sees its request's old length.
+constexpr int kPlanThreads = 1024;
+
+// Inclusive scan of one value per thread over a kPlanThreads block.
+__device__ __forceinline__ int block_scan(int v, int* part) {
+    const int tid = threadIdx.x;
+    part[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {
+        const int x = tid >= off ? part[tid - off] : 0;
+        __syncthreads();
+        part[tid] += x;
+        __syncthreads();
     }
-    return (q_start[lo] <= i && i < q_start[lo + 1]) ? lo : -1;
+    return part[tid];
 }
 
-// ----------------------------------------------------------- prompt write --
-// One workgroup per prompt token: its K row goes in 16-byte chunks and its V
-// row element by element (V pages are dim-major) to position
-// seq_lens[b] + (i - q_start[b]).  Lengths are advanced afterwards by
-// lens_kernel, so every token sees its request's old length.
-__global__ void __launch_bounds__(256) kv_write_kernel(WriteArgs a) {
-    const int i = blockIdx.x;
-    const int b = find_request(a.q_start, a.B, i);
-    if (b < 0) {
-        if (threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
+// Pages request b's new positions touch, or -1 for a malformed request
+// (negative or reversed range, rows past T, negative length).
+__device__ __forceinline__ int pages_touched(const WriteArgs& a, int b) {
+    const int s0 = a.q_start[b], s1 = a.q_start[b + 1];
+    const int L = a.seq_lens[b];
+    if (s0 < 0 || s1 < s0 || s1 > a.T || L < 0) return -1;
+    if (s1 == s0) return 0;
+    const int64_t last = (int64_t)L + (s1 - s0) - 1;
+    return (int)(last / kPage - L / kPage + 1);
+}
+
+__global__ void __launch_bounds__(kPlanThreads) write_plan_kernel(WriteArgs a, int32_t* page_start) {
+    __shared__ int part[kPlanThreads];
+    __shared__ int malformed;
+    const int tid = threadIdx.x;
+    if (tid == 0) malformed = (a.q_start[0] < 0 || a.q_start[a.B] > a.T) ? 1 : 0;
+    __syncthreads();
+    const int per = (a.B + kPlanThreads - 1) / kPlanThreads;
+    const int b0 = tid * per;
+    int sum = 0, bad = 0;
+    for (int k = 0; k < per; ++k) {
+        const int b = b0 + k;
+        if (b >= a.B) break;
+        if (a.q_start[b + 1] < a.q_start[b]) atomicOr(&malformed, 1);
+        const int t = pages_touched(a, b);
+        if (t < 0) bad = 1;
+        else sum += t;
+    }
+    if (bad) atomicOr(a.err, kErrAppendSlot);
+    const int incl = block_scan(sum, part);
+    if (malformed) {
+        for (int k = 0; k < per; ++k)
+            if (b0 + k < a.B) page_start[b0 + k] = 0;
+        if (tid == 0) {
+            page_start[a.B] = 0;
+            atomicOr(a.err, kErrAppendSlot);
+        }
         return;
     }
-    const int pos = a.seq_lens[b] + (i - a.q_start[b]);
-    const int pi = pos / kPage;
+    int run = incl - sum;
+    for (int k = 0; k < per; ++k) {
+        const int b = b0 + k;
+        if (b < a.B) {
+            page_start[b] = run;
+            run += max(pages_touched(a, b), 0);
+        }
+    }
+    if (tid == kPlanThreads - 1) {
+        page_start[a.B] = incl;
+        if (a.q_start[a.B] < a.T) atomicOr(a.err, kErrAppendSlot);   // rows no request owns
+    }
+}
+
+template <int EB>
+__global__ void __launch_bounds__(256) kv_write_kernel(WriteArgs a, const int32_t* page_start) {
+    __shared__ __attribute__((aligned(16))) uint8_t vst[kPage * 128 * 2];   // the page's V rows, one head
+    const int item = blockIdx.x, g = blockIdx.y, tid = threadIdx.x;
+    if (item >= page_start[a.B]) return;
+    int lo = 0, hi = a.B - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (page_start[mid] <= item) lo = mid;
+        else hi = mid - 1;
+    }
+    const int b = lo;
+    const int s0 = a.q_start[b], L = a.seq_lens[b];
+    const int n = a.q_start[b + 1] - s0;
+    const int pi = L / kPage + (item - page_start[b]);
+    const int64_t first = (int64_t)kPage * pi;              // position of slot 0
+    const int slot_lo = (int)(max((int64_t)L, first) - first);
+    const int slot_hi = (int)(min((int64_t)L + n, first + kPage) - first);
     int pg = -1;
-    if (pos >= 0 && pi < a.max_pages) pg = a.block_table[(int64_t)b * a.bt_stride + pi];
+    if (pi < a.max_pages) pg = a.block_table[(int64_t)b * a.bt_stride + pi];
     if (pg < 0 || pg >= a.num_pages) {
-        if (threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
+        if (g == 0 && tid == 0) atomicOr(a.err, kErrAppendSlot);
         return;
     }
-    const int slot = pos % kPage;
-    const int eb = a.elem_bytes, x = 16 / eb, chunks = a.D / x;
-    char* kp = (char*)a.k_pages;
-    char* vp = (char*)a.v_pages;
-    const int64_t tile = (int64_t)a.D * kPage;  // elements per (page, head) tile
-    for (int j = threadIdx.x; j < a.H_kv * chunks; j += blockDim.x) {
-        const int g = j / chunks, c = j - g * chunks;
-        const char* src = (const char*)a.k_new + ((int64_t)i * a.k_st + (int64_t)g * a.k_sh + (int64_t)c * x) * eb;
-        const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;   // 16-byte units
-        *(u32x4*)(kp + dst * 16) = *(const u32x4*)src;
+    const int64_t row0 = s0 + (first - L);                   // token row of slot 0
+    constexpr int x = 16 / EB;                               // elements per 16-byte unit
+    const int chunks = a.D / x;
+    const char* kn = (const char*)a.k_new;
+    const char* vn = (const char*)a.v_new;
+    char* kp = (char*)a.k_pages + ((int64_t)pg * a.H_kv + g) * (int64_t)a.D * kPage * EB;
+    char* vp = (char*)a.v_pages + ((int64_t)pg * a.H_kv + g) * (int64_t)a.D * kPage * EB;
+    for (int u = tid; u < chunks * kPage; u += 256) {
+        const int c = u / kPage, sl = u % kPage;
+        if (sl < slot_lo || sl >= slot_hi) continue;
+        const char* src = kn + ((row0 + sl) * a.k_st + (int64_t)g * a.k_sh + (int64_t)c * x) * EB;
+        *(u32x4*)(kp + (int64_t)u * 16) = *(const u32x4*)src;
     }
-    for (int j = threadIdx.x; j < a.H_kv * a.D; j += blockDim.x) {
-        const int g = j / a.D, d = j - g * a.D;
-        const int64_t src = (int64_t)i * a.v_st + (int64_t)g * a.v_sh + d;
-        const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile + (int64_t)d * kPage + slot;
-        if (eb == 2)
-            *(uint16_t*)(vp + dst * 2) = *(const uint16_t*)((const char*)a.v_new + src * 2);
-        else
-            *(uint8_t*)(vp + dst) = *(const uint8_t*)((const char*)a.v_new + src);
+    const int row_units = a.D * EB / 16;                     // 16-byte units of one token's V row
+    for (int u = tid; u < kPage * row_units; u += 256) {
+        const int sl = u / row_units, k = u % row_units;
+        if (sl < slot_lo || sl >= slot_hi) continue;
+        *(u32x4*)&vst[u * 16] = *(const u32x4*)(vn + ((row0 + sl) * a.v_st + (int64_t)g * a.v_sh) * EB + k * 16);
+    }
+    __syncthreads();
+    // V page rows: unit (d, h) holds slots h x .. h x + x - 1 of dim d
+    const int row_bytes = a.D * EB;
+    for (int u = tid; u < a.D * EB; u += 256) {
+        const int d = u / EB, h = u % EB;
+        const int sa = h * x;
+        char* dst = vp + (int64_t)u * 16;
+        if (sa >= slot_lo && sa + x <= slot_hi) {
+            uint8_t buf[16];
+#pragma unroll
+            for (int e = 0; e < x; ++e)
+#pragma unroll
+                for (int q = 0; q < EB; ++q) buf[e * EB + q] = vst[(sa + e) * row_bytes + d * EB + q];
+            *(u32x4*)dst = *(const u32x4*)buf;
+        } else {
+            for (int sl = max(sa, slot_lo); sl < min(sa + x, slot_hi); ++sl)
+                for (int q = 0; q < EB; ++q) dst[(sl - sa) * EB + q] = (char)vst[sl * row_bytes + d * EB + q];
+        }
     }
 }
 
@@ -108,8 +196,6 @@ __global__ void lens_kernel(WriteArgs a) {
 // that is not non-decreasing from a non-negative start up to at most T gives
 // no request any tile (so the tiles always fit the grid of
 // ceil(T / 128) + B workgroups).
-constexpr int kPlanThreads = 1024;
-
 __device__ __forceinline__ int tiles_of(const PrefillArgs& a, int b) {
     const int n = a.q_start[b + 1] - a.q_start[b], L = a.seq_lens[b];
     if (n < 0 || n > L || (int64_t)L > (int64_t)a.max_pages * kPage) return -1;
@@ -134,14 +220,7 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
         else sum += t;
     }
     if (bad) atomicOr(a.err, kErrLength);
-    part[tid] = sum;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {  // inclusive scan
-        const int v = tid >= off ? part[tid - off] : 0;
-        __syncthreads();
-        part[tid] += v;
-        __syncthreads();
-    }
+    const int incl = block_scan(sum, part);
     if (malformed) {
         for (int k = 0; k < per; ++k)
             if (b0 + k < a.B) a.tile_start[b0 + k] = 0;
@@ -151,7 +230,7 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
         }
         return;
     }
-    int run = tid ? part[tid - 1] : 0;
+    int run = incl - sum;
     for (int k = 0; k < per; ++k) {
         const int b = b0 + k;
         if (b < a.B) {
@@ -159,7 +238,7 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
             run += max(tiles_of(a, b), 0);
         }
     }
-    if (tid == kPlanThreads - 1) a.tile_start[a.B] = part[tid];
+    if (tid == kPlanThreads - 1) a.tile_start[a.B] = incl;
 }
 
 // -------------------------------------------------------------- attention --
@@ -513,8 +592,14 @@ prefill_attn_kernel(PrefillArgs a) {
 
 }  // namespace
 
-void launch_kv_write(const WriteArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(kv_write_kernel, dim3(a.T), dim3(256), 0, s, a);
+void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s) {
+    hipLaunchKernelGGL(write_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a, page_start);
+    // an upper bound on the pages touched: ceil(n_b / 16) + 1 per request
+    const unsigned items = (unsigned)(a.T / kPage + 2 * a.B + 1);
+    if (a.elem_bytes == 2)
+        hipLaunchKernelGGL(kv_write_kernel<2>, dim3(items, (unsigned)a.H_kv), dim3(256), 0, s, a, (const int32_t*)page_start);
+    else
+        hipLaunchKernelGGL(kv_write_kernel<1>, dim3(items, (unsigned)a.H_kv), dim3(256), 0, s, a, (const int32_t*)page_start);
     hipLaunchKernelGGL(lens_kernel, dim3((a.B + 255) / 256), dim3(256), 0, s, a);
 }
 

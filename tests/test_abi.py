@@ -186,6 +186,8 @@ WRITE_CASES = [
     ("q_start size", lambda B_, g: g.update(qs=t(B_.INT32, [6])), ERR_INVALID, "q_start"),
     ("misaligned k_new", lambda B_, g: g.update(pkn=t(B_.BF16, [40, 8, 128], data=FAKE + 8)), ERR_UNSUPPORTED,
      "aligned"),
+    ("misaligned v_new", lambda B_, g: g.update(pvn=t(B_.BF16, [40, 8, 128], data=FAKE + 8)), ERR_UNSUPPORTED,
+     "aligned"),
 ]
 
 

@@ -226,3 +226,37 @@ def test_prefill_full_size_sampled_rows(name):
     ref = _oracle_prefill(w, kp, vp, seq_lens=lens, q_bits=q_bits,
                           q_start=np.arange(len(rows) + 1, dtype=np.int32), block_table=bt)
     assert_close(_out_f64(out)[rows], ref, "bf16", name)
+
+
+def test_kv_write_fp8_codes_bit_exact():
+    # 1-byte pools (fp8 codes, copied as bytes): random codes everywhere,
+    # four requests with unaligned cached prefixes
+    rng = np.random.default_rng(44)
+    B, H_kv, D = 4, 2, 128
+    cached, new = np.array([3, 0, 17, 40]), np.array([29, 16, 1, 70])
+    need = (cached + new + 15) // 16
+    NP = int(need.sum()) + 4
+    perm = rng.permutation(NP).astype(np.int32)
+    bt = np.full((B, int(need.max()) + 1), -1, dtype=np.int32)
+    pos = 0
+    for b in range(B):
+        bt[b, :need[b]] = perm[pos:pos + need[b]]
+        pos += need[b]
+    kp = rng.integers(0, 256, size=(NP, H_kv, D // 16, 16, 16), dtype=np.uint8)
+    vp = rng.integers(0, 256, size=(NP, H_kv, D, 16), dtype=np.uint8)
+    T = int(new.sum())
+    kn = rng.integers(0, 256, size=(T, H_kv, D), dtype=np.uint8)
+    vn = rng.integers(0, 256, size=(T, H_kv, D), dtype=np.uint8)
+    qs = np.concatenate([[0], np.cumsum(new)]).astype(np.int32)
+    sl = cached.astype(np.int32)
+    # every device tensor stays referenced until the call has run (a
+    # descriptor holds only the pointer)
+    gk, gv, gsl = (torch.from_numpy(x).cuda() for x in (kp, vp, sl))
+    gkn, gvn, gbt, gqs = (torch.from_numpy(x).cuda() for x in (kn, vn, bt, qs))
+    bl.kv_write(gkn, gvn, gk, gv, gbt, gsl, gqs)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    ek, ev, esl = kp.copy(), vp.copy(), sl.copy()
+    oracle.kv_write(kn, vn, ek, ev, bt, esl, qs, kv_dtype=oracle.FP8_E4M3FN)
+    assert np.array_equal(gk.cpu().numpy(), ek) and np.array_equal(gv.cpu().numpy(), ev)
+    assert gsl.cpu().tolist() == esl.tolist() == (cached + new).tolist()
