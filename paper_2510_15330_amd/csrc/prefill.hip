@@ -11,6 +11,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "../../include/bellman.h"
 #include "internal.h"
 
@@ -244,10 +246,12 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 // -------------------------------------------------------------- attention --
 // Workgroup = 128 query rows of one request and one query head; wave w owns
 // rows 32w..32w+31.  Keys go by steps of 64 (four pages).  The step's K and V
-// tiles are copied from the pool into LDS in the pool's own layout (K [page]
-// [D/8 chunks][16 slots][8], V [page][D][16 slots], both XOR-swizzled against
-// bank conflicts), double-buffered, with K one step ahead of V, and read by
-// all four waves.
+// tiles are copied from the pool straight into LDS (global_load_lds, 16 bytes
+// a lane) in the pool's own layout (K [page][D/8 chunks][16 slots][8],
+// V [page][D][16 slots], both XOR-swizzled against bank conflicts by the
+// choice of unit each lane fetches), double-buffered in four separate arrays
+// (so no read of one buffer waits on a copy into another), with K one step
+// ahead of V, and read by all four waves.
 //
 // S^T = K Q^T on 32x32x16 MFMAs: A = 32 keys x 16 dims from LDS, B = the
 // wave's 32 query columns, held in registers for the whole kernel.  A's row i
@@ -281,8 +285,10 @@ prefill_attn_kernel(PrefillArgs a) {
     constexpr int UPP = PE / 8;         // 16-byte units per page
     constexpr int PER = 2 * PPS * UPP / 256;   // units of K + V per thread per step
     constexpr int WIN = kPageWindow / PPS;     // steps per block-table window
-    __shared__ __attribute__((aligned(16))) uint16_t lds_k[2][KT];
-    __shared__ __attribute__((aligned(16))) uint16_t lds_v[2][KT];
+    __shared__ __attribute__((aligned(16))) uint16_t kb0[KT];
+    __shared__ __attribute__((aligned(16))) uint16_t kb1[KT];
+    __shared__ __attribute__((aligned(16))) uint16_t vb0[KT];
+    __shared__ __attribute__((aligned(16))) uint16_t vb1[KT];
     __shared__ int pages[kPageWindow];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -356,12 +362,11 @@ prefill_attn_kernel(PrefillArgs a) {
     // step s computes, K of step s + 2 and V of step s + 1 are loaded into
     // registers, and written to LDS after it.
     constexpr int PERH = PER / 2;      // units of one tensor per thread per step
-    u32x4 stage[PERH];
     const char* kbase = (const char*)a.k_pages + (int64_t)g * PE * 2;
     const char* vbase = (const char*)a.v_pages + (int64_t)g * PE * 2;
     const int64_t page_bytes = (int64_t)a.H_kv * PE * 2;
-    int64_t offk[PPS];                 // byte offsets of the pages of the last K load
-    auto pages_of = [&](int j) {
+    int64_t off1[PPS], off2[PPS];      // page byte offsets of steps s + 1 and s + 2
+    auto pages_of = [&](int j, int64_t (&off)[PPS]) {
         const int e = PPS * (j % WIN);
 #pragma unroll
         for (int q = 0; q < PPS; ++q) {
@@ -370,39 +375,22 @@ prefill_attn_kernel(PrefillArgs a) {
                 pg = 0;
                 bad = true;
             }
-            offk[q] = (int64_t)pg * page_bytes;
+            off[q] = (int64_t)pg * page_bytes;
         }
     };
-    // unit u = 256 k + tid of one tensor's step tile: page u / UPP, 16-byte
-    // unit u % UPP of it; 256 units hold 256 / UPP pages (1 at D = 128, 2 at
-    // D = 64, where waves 2 and 3 take the second), so every index is constant
     constexpr int BPP = 256 / UPP;
-    const int lane_off = ((64 * w) % UPP + lane) * 16;
-    auto load = [&](const char* base) {
+    // direct copies into LDS: lane l of a wave lands at unit (wave base + l);
+    // it fetches the global unit the swizzle maps there (the swizzles are
+    // involutions within a page)
+    auto dma = [&](const char* base, const int64_t (&off)[PPS], uint16_t* dst, bool isv) {
 #pragma unroll
         for (int k = 0; k < PERH; ++k) {
             const int pp = (256 * k) / UPP;
-            int64_t o_pg = offk[pp];
-            if constexpr (BPP == 2) o_pg = (w >> 1) ? offk[pp + 1] : o_pg;
-            stage[k] = *(const u32x4*)(base + o_pg + lane_off);
-        }
-    };
-    // LDS swizzles, so that the lanes of one read spread over the banks: in a
-    // K page (unit = 16 slots x D/8 chunks, slot-minor) slot bit 2 is flipped
-    // by slot bit 3; in a V page (unit = one half of a dim row) the halves
-    // of dim d swap when bit 2 of d differs from bit 3
-    auto store_k = [&](uint16_t* dst) {
-#pragma unroll
-        for (int k = 0; k < PERH; ++k) {
-            const int u = 256 * k + tid, v = u % UPP;
-            *(u32x4*)&dst[8 * (u ^ (((v >> 3) & 1) << 2))] = stage[k];
-        }
-    };
-    auto store_v = [&](uint16_t* dst) {
-#pragma unroll
-        for (int k = 0; k < PERH; ++k) {
-            const int u = 256 * k + tid, v = u % UPP;
-            *(u32x4*)&dst[8 * (u ^ (((v >> 3) ^ (v >> 4)) & 1))] = stage[k];
+            int64_t o_pg = off[pp];
+            if constexpr (BPP == 2) o_pg = (w >> 1) ? off[pp + 1] : o_pg;
+            const int v = ((256 * k + 64 * w) % UPP) + lane;          // LDS unit within its page
+            const int vg = isv ? v ^ (((v >> 3) ^ (v >> 4)) & 1) : v ^ (((v >> 3) & 1) << 2);
+            __builtin_amdgcn_global_load_lds(base + o_pg + vg * 16, dst + 8 * (256 * k + 64 * w), 16, 0, 0);
         }
     };
     // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
@@ -437,30 +425,36 @@ prefill_attn_kernel(PrefillArgs a) {
 
     // prologue: K and V of step 0, K of step 1, S of step 0
     refill(0);
-    pages_of(0);
-    load(kbase);
-    store_k(lds_k[0]);
-    load(vbase);
-    store_v(lds_v[0]);
+    pages_of(0, off2);
+    dma(kbase, off2, kb0, false);
+    dma(vbase, off2, vb0, true);
     if (nsteps > 1) {
-        pages_of(1);
-        load(kbase);
-        store_k(lds_k[1]);
+        pages_of(1, off1);
+        dma(kbase, off1, kb1, false);
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (KS > L) {
-        clear_tail(0, lds_v[0]);
+        clear_tail(0, vb0);
         __syncthreads();
     }
     f32x16 sca[NH], scb[NH];
-    if (0 < wave_steps) qk(lds_k[0], sca);
+    if (0 < wave_steps) qk(kb0, sca);
 
     // one step; sc holds S(s), scn receives S(s + 1)
-    auto step = [&](const int s, f32x16 (&sc)[NH], f32x16 (&scn)[NH]) {
-        // loads of this step: V of step s + 1 now (its pages are those of the
-        // last K load), K of step s + 2 once V has gone to LDS mid-step
+    auto step = [&](auto par, const int s, f32x16 (&sc)[NH], f32x16 (&scn)[NH]) {
+        constexpr int P = decltype(par)::value;   // s % 2
+        uint16_t* k_rd = P ? kb0 : kb1;   // K(s + 1)
+        uint16_t* k_wr = P ? kb1 : kb0;   // K(s + 2), over K(s)
+        uint16_t* v_rd = P ? vb1 : vb0;   // V(s)
+        uint16_t* v_wr = P ? vb0 : vb1;   // V(s + 1), over V(s - 1)
         const bool more_k = s + 2 < nsteps, more_v = s + 1 < nsteps;
-        if (more_v) load(vbase);
+        if (more_v) dma(vbase, off1, v_wr, true);
+        if (more_k) {
+            if ((s + 2) % WIN == 0) refill(s + 2);
+            pages_of(s + 2, off2);
+            dma(kbase, off2, k_wr, false);
+        }
         uint32_t ph[NH][8], pl[NH][8];
         if (s < wave_steps) {
             // keys above a column's position are masked only on the steps
@@ -490,7 +484,7 @@ prefill_attn_kernel(PrefillArgs a) {
             }
             // S of step s + 1 on the matrix cores while P of step s is formed
             // (past a wave's last step the result is not used)
-            qk(lds_k[(s + 1) & 1], scn);
+            qk(k_rd, scn);
             float psum = 0.f;
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh)
@@ -518,17 +512,8 @@ prefill_attn_kernel(PrefillArgs a) {
                 if (i + 2 < 8 * NH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // a K read
                 __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);   // softmax VALU
             }
-        }
-        // V(s + 1) to LDS (its buffer was last read in step s - 1), then K(s + 2)
-        if (more_v) store_v(lds_v[(s + 1) & 1]);
-        if (more_k) {
-            if ((s + 2) % WIN == 0) refill(s + 2);
-            pages_of(s + 2);
-            load(kbase);
-        }
-        if (s < wave_steps) {
             // O^T += V^T P^T, per 16-key page u of each half and 32-dim tile t
-            const uint16_t* Vt = lds_v[s & 1] + v_off;
+            const uint16_t* Vt = v_rd + v_off;
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
@@ -557,18 +542,20 @@ prefill_attn_kernel(PrefillArgs a) {
             }
         }
         if (more_v) {
-            if (more_k) store_k(lds_k[s & 1]);
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
             if (KS * (s + 2) > L) {
-                clear_tail(s + 1, lds_v[(s + 1) & 1]);
+                clear_tail(s + 1, v_wr);
                 __syncthreads();
             }
         }
+#pragma unroll
+        for (int q = 0; q < PPS; ++q) off1[q] = off2[q];
     };
     // unrolled by two so that S(s) and S(s + 1) alternate between register sets
     for (int s = 0; s < nsteps; s += 2) {
-        step(s, sca, scb);
-        if (s + 1 < nsteps) step(s + 1, scb, sca);
+        step(std::integral_constant<int, 0>{}, s, sca, scb);
+        if (s + 1 < nsteps) step(std::integral_constant<int, 1>{}, s + 1, scb, sca);
     }
     if (bad && lane == 0) atomicOr(a.err, kErrPage);
     if (rw >= n) return;
