@@ -121,10 +121,11 @@ int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_n
  *   scale        finite fp32 softmax scale (usually 1/sqrt(D)).
  *   out          bf16 [B, H_q, D], innermost contiguous (written; rounded to
  *                nearest even).  A request of length 0 gets zeros.
- * The (request, KV head, page) units of the batch are dealt to the GPU's
- * resident wavefronts in equal contiguous shares; a request cut by a share
- * boundary has its partial softmax statistics merged in a second pass.  The
- * shares are planned on the device, so the call never waits for the GPU.
+ * The work of the batch, as (request, KV head, step of consecutive pages)
+ * units, is dealt to the GPU's resident wavefronts in equal contiguous
+ * shares; a request cut by a share boundary has its partial softmax
+ * statistics merged in a second pass.  The shares are planned on the device,
+ * so the call never waits for the GPU.
  * Limits: B <= 8192 and B * H_kv * maxP < 2^31.  Scratch memory is a
  * per-device library workspace grown on demand (hipMalloc) and released by
  * bellman_shutdown(); calls on different streams of one device must not

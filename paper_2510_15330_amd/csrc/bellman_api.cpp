@@ -403,7 +403,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
         bpc = attention_blocks_per_cu(pps, depth, ps.fp8, ps.D);
         if (depth == 2) bpc = 1;  // one wavefront per SIMD
     }
-    // Every resident wave takes an equal share of the flattened page stream.
+    // Every resident wave takes an equal share of the flattened step stream.
     int64_t waves = (int64_t)g_cu_count[dev] * bpc * (kAttnBlock / kWaveSize);
     if (max_waves > 0 && waves > max_waves) waves = max_waves;
     const int64_t grid = (waves + (kAttnBlock / kWaveSize) - 1) / (kAttnBlock / kWaveSize);
@@ -441,6 +441,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.D = ps.D;
     a.max_pages = (int)max_pages;
     a.waves = (int)waves;
+    a.pp = pps;
     a.hdr = (WorkspaceHeader*)base;
     a.b_info = (int4*)(base + off_binfo);
     a.wave_start = (int4*)(base + off_wstart);

@@ -18,7 +18,7 @@ constexpr int kErrPage = 4;
 // Header of the per-device workspace; the variable-size regions follow it.
 struct WorkspaceHeader {
     int32_t err_flags;    // sticky error bits, cleared by the host
-    int32_t total_pages;  // flattened (request, KV head, page) units of the current call
+    int32_t total_units;  // flattened (request, KV head, step) units of the current call
     int32_t pad[62];
 };
 static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte aligned");
@@ -56,11 +56,12 @@ struct AttnArgs {
     int64_t num_pages;
     float scale_log2;    // softmax scale * log2(e)
     int B, H_q, H_kv, G, D, max_pages;
-    int waves;           // waves sharing the flattened page stream (the grid's waves)
+    int waves;           // waves sharing the flattened step stream (the grid's waves)
+    int pp;              // pages per step of the launched attention kernel
     // workspace
     WorkspaceHeader* hdr;
-    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, 0)
-    int4* wave_start;    // [waves]: (request, KV head, page) of the wave's first unit
+    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head)
+    int4* wave_start;    // [waves]: (request, KV head, first page) of the wave's first step
     float2* part_ml;     // [(B*H_kv + waves) * G]: (running max in log2 units, sum)
     float* part_o;       // [(B*H_kv + waves) * G * D]
 };

@@ -141,12 +141,17 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 
 // -------------------------------------------------------------- planner ---
 // One workgroup.  The work of a call is the flattened sequence of units
-// (request b, KV head g, page p), request-major, then head, then page.  The
-// planner clamps each length to the block-table width, scans the pages per
-// request into each request's first unit, and gives every one of the W waves
-// the contiguous range [floor(w*P/W), floor((w+1)*P/W)) of the P units,
-// recording the (b, g, p) where that range starts.  Requests are split only
-// where a wave boundary falls inside them.
+// (request b, KV head g, step j), request-major, then head, then step, where
+// step j of a (request, head) covers its pages [j*PP, min((j+1)*PP, pages))
+// and PP is the attention kernel's pages per step.  A step costs the same
+// whether it holds PP pages or the last few (its loads are issued for all PP
+// pages), so dealing steps rather than pages keeps the waves' times equal
+// when many requests end in a short step.  The planner clamps each length to
+// the block-table width, scans the steps per request into each request's
+// first unit, and gives every one of the W waves the contiguous range
+// [floor(w*P/W), floor((w+1)*P/W)) of the P units, recording the (b, g, first
+// page) where that range starts.  Requests are split only where a wave
+// boundary falls inside them, and always between steps.
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanMaxBatch = 8192;   // request starts kept in LDS for the search
 
@@ -160,7 +165,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
     __syncthreads();
     for (int base = 0; base < a.B; base += kPlanThreads) {
         const int b = base + tid;
-        int units = 0, L = 0, np = 0;
+        int units = 0, L = 0, np = 0, ns = 0;
         if (b < a.B) {
             L = a.seq_lens[b];
             if (L < 0 || L > maxL) {
@@ -168,7 +173,8 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
                 L = L < 0 ? 0 : maxL;
             }
             np = (L + kPage - 1) / kPage;
-            units = np * a.H_kv;
+            ns = (np + a.pp - 1) / a.pp;
+            units = ns * a.H_kv;
         }
         scan[tid] = units;
         __syncthreads();
@@ -181,7 +187,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
         const int excl = carry + scan[tid] - units;
         if (b < a.B) {
             first[b] = excl;
-            a.b_info[b] = make_int4(excl, np, L, 0);
+            a.b_info[b] = make_int4(excl, np, L, ns);
         }
         __syncthreads();
         if (tid == kPlanThreads - 1) carry += scan[kPlanThreads - 1];
@@ -190,7 +196,7 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
     const int P = carry;
     if (tid == 0) {
         first[a.B] = P;
-        a.hdr->total_pages = P;
+        a.hdr->total_units = P;
     }
     __syncthreads();
     for (int w = tid; w < a.waves; w += kPlanThreads) {
@@ -198,25 +204,25 @@ __global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
         const int x1 = (int)((int64_t)(w + 1) * P / a.waves);
         int4 ws = make_int4(-1, 0, 0, 0);
         if (x < x1) {
-            // last request whose first unit is <= x (it has pages, since x < P)
+            // last request whose first unit is <= x (it has steps, since x < P)
             int lo = 0, hi = a.B - 1;
             while (lo < hi) {
                 const int mid = (lo + hi + 1) >> 1;
                 if (first[mid] <= x) lo = mid; else hi = mid - 1;
             }
-            const int np = (first[lo + 1] - first[lo]) / a.H_kv;
+            const int ns = (first[lo + 1] - first[lo]) / a.H_kv;
             const int off = x - first[lo];
-            ws = make_int4(lo, off / np, off % np, 0);
+            ws = make_int4(lo, off / ns, (off % ns) * a.pp, 0);
         }
         a.wave_start[w] = ws;
     }
 }
 
 // ------------------------------------------------ partial attention (MFMA) --
-// Each wave takes work items = (request b, split s, KV head g) in turn and
-// streams each split's pages two at a time:
+// Each wave walks its contiguous share of the planner's steps, a step being
+// PP consecutive pages of one (request b, KV head g); for bf16 pages:
 //   S^T[slot, head] = K_page[slot, :] . Q^T[:, head]   (v_mfma 16x16x32 bf16)
-//   online softmax per head in base 2, once per 32 tokens
+//   online softmax per head in base 2, once per step
 //   O^T[dim, head] += V_pair^T[dim, token] . P^T[token, head]  (v_mfma 16x16x32)
 // Lane l = 16*qg + n.  In the QK product n is the page slot (A row) and the
 // query head of the group (B column); the result leaves lane (qg, n) with the
@@ -687,33 +693,32 @@ __device__ __forceinline__ void consume(const PageK<D, FP8>& r) { consume(r.k); 
 template <int D, bool FP8>
 __device__ __forceinline__ void consume(const PageV<D, FP8>& r) { consume(r.v); }
 
-// A position in a wave's stream: a step of `len` consecutive pages starting
-// at unit x, which is page p of request b, KV head g.  Wave-uniform.
+// A position in a wave's stream: step x, the `len` consecutive pages from
+// page p of request b, KV head g.  Wave-uniform.
 struct Cursor {
     int b, g, p;   // request, KV head, first page of the step within the request
     int np, L;     // the request's pages and clamped length
-    int x;         // flattened unit of the step's first page
-    int len;       // pages in the step (1..PP; never crosses a request or the range end)
+    int x;         // flattened unit (step) index
+    int len;       // pages in the step (1..PP; never crosses a request)
     bool live;     // false once past the wave's range
 };
 
 template <int PP>
-__device__ __forceinline__ void cursor_len(Cursor& c, int r1) {
-    c.len = min(PP, min(c.np - c.p, r1 - c.x));
+__device__ __forceinline__ void cursor_len(Cursor& c) {
+    c.len = min(PP, c.np - c.p);
 }
 
-// Step to the next group of pages.  A cursor that would leave the range
-// keeps its last position (so loads issued for it stay in bounds) and stops
-// being live.
+// Step to the next unit.  A cursor that would leave the range keeps its last
+// position (so loads issued for it stay in bounds) and stops being live.
 template <int PP>
 __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1) {
     if (!c.live) return;
-    if (c.x + c.len >= r1) {
+    if (c.x + 1 >= r1) {
         c.live = false;
         return;
     }
-    c.x += c.len;
-    c.p += c.len;
+    c.x += 1;
+    c.p += PP;
     if (c.p >= c.np) {
         c.p = 0;
         if (++c.g >= a.H_kv) {
@@ -727,7 +732,7 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1
             } while (c.np == 0 && c.b + 1 < a.B);
         }
     }
-    cursor_len<PP>(c, r1);
+    cursor_len<PP>(c);
 }
 
 // DEPTH steps of PP pages are in flight per wave while it computes one.  With
@@ -746,7 +751,7 @@ attn_mfma_kernel(AttnArgs a) {
     // wave index, made provably uniform so that all stream bookkeeping is scalar
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6));
     if (w >= a.waves) return;
-    const int P = a.hdr->total_pages;
+    const int P = a.hdr->total_units;
     const int r0 = (int)((int64_t)w * P / a.waves);
     const int r1 = (int)((int64_t)(w + 1) * P / a.waves);
     if (r0 >= r1) return;
@@ -769,7 +774,7 @@ attn_mfma_kernel(AttnArgs a) {
         cur[0].L = bi.z;
         cur[0].x = r0;
         cur[0].live = true;
-        cursor_len<PP>(cur[0], r1);
+        cursor_len<PP>(cur[0]);
     }
 #pragma unroll
     for (int j = 1; j < DEPTH + 2; ++j) {
@@ -846,8 +851,8 @@ attn_mfma_kernel(AttnArgs a) {
     // request's head lies entirely in this wave's range, else a partial.
     auto finish = [&](const Cursor& c, float vs) {
         const float l_tot = group_sum4(st.l);
-        const int seg_x0 = c.x - c.p;
-        const bool whole = seg_x0 >= r0 && seg_x0 + c.np <= r1;
+        const int seg_x0 = c.x - c.p / PP;
+        const bool whole = seg_x0 >= r0 && seg_x0 + (c.np + PP - 1) / PP <= r1;
         if (hv) {
             const int h = c.g * a.G + n;
             if (whole) {
@@ -944,7 +949,7 @@ attn_mfma_kernel(AttnArgs a) {
             }
             group_pv<D, FP8, PP>(st, sc4, vb[sc_], sl, nv, qg);
         }
-        if (C.live && (C.p + C.len >= C.np || C.x + C.len >= r1)) finish(C, vs);
+        if (C.live && (C.p + C.len >= C.np || C.x + 1 >= r1)) finish(C, vs);
 #pragma unroll
         for (int j = 0; j < DEPTH + 1; ++j) cur[j] = cur[j + 1];
         cursor_next<PP>(cur[DEPTH + 1], a, r1);
@@ -992,11 +997,12 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
         for (int d = lane; d < D; d += kWaveSize) orow[d] = 0;
         return;
     }
-    const int P = a.hdr->total_pages;
+    const int P = a.hdr->total_units;
     const int W = a.waves;
-    const int x0 = bi.x + g * np;
+    const int ns = bi.w;                 // steps per KV head
+    const int x0 = bi.x + g * ns;
     const int wf = wave_of(x0, P, W);
-    const int wl = wave_of(x0 + np - 1, P, W);
+    const int wl = wave_of(x0 + ns - 1, P, W);
     if (wf == wl) return;
     const int64_t seg = (int64_t)b * a.H_kv + g;
     auto has_units = [&](int v) {
