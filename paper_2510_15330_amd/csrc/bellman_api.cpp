@@ -31,7 +31,7 @@ int fail(int code, const char* fmt, ...) {
 // ------------------------------------------------------------- workspace ---
 
 constexpr int kMaxDevices = 64;
-constexpr int kMaxAttnBatch = 8192;  // request starts the planner keeps in LDS
+constexpr int kMaxAttnBatch = 8192;  // lengths every attention wave reads to find its share
 
 struct Workspace {
     char* base = nullptr;
@@ -410,8 +410,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
 
     const int64_t segs = B * ps.H_kv;
     const size_t off_binfo = sizeof(WorkspaceHeader);
-    const size_t off_wstart = off_binfo + align256(sizeof(int4) * (size_t)B);
-    const size_t off_ml = off_wstart + align256(sizeof(int4) * (size_t)waves);
+    const size_t off_ml = off_binfo + align256(sizeof(int4) * (size_t)B);
     const size_t slots = (size_t)(segs + waves) * (size_t)G;
     const size_t off_o = off_ml + align256(sizeof(float2) * slots);
     const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
@@ -444,15 +443,12 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.pp = pps;
     a.hdr = (WorkspaceHeader*)base;
     a.b_info = (int4*)(base + off_binfo);
-    a.wave_start = (int4*)(base + off_wstart);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
 
     hipStream_t s = (hipStream_t)stream;
     hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
     hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;
-    launch_plan(a, s);
-    if ((rc = launch_status("plan"))) return rc;
     if (ev0) {
         hipError_t e = hipEventRecord(ev0, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));

@@ -60,8 +60,8 @@ struct AttnArgs {
     int pp;              // pages per step of the launched attention kernel
     // workspace
     WorkspaceHeader* hdr;
-    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head)
-    int4* wave_start;    // [waves]: (request, KV head, first page) of the wave's first step
+    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head),
+                         // written by the attention kernel for the merge kernel
     float2* part_ml;     // [(B*H_kv + waves) * G]: (running max in log2 units, sum)
     float* part_o;       // [(B*H_kv + waves) * G * D]
 };
@@ -105,7 +105,6 @@ struct PrefillArgs {
 // Launchers (kernels.hip).  They only enqueue; errors come back through
 // hipGetLastError in the caller.
 void launch_kv_append(const AppendArgs& a, hipStream_t s);
-void launch_plan(const AttnArgs& a, hipStream_t s);
 void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s);
 void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).

@@ -139,83 +139,36 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
     if (threadIdx.x == 0) a.seq_lens[b] = L + 1;
 }
 
-// -------------------------------------------------------------- planner ---
-// One workgroup.  The work of a call is the flattened sequence of units
-// (request b, KV head g, step j), request-major, then head, then step, where
-// step j of a (request, head) covers its pages [j*PP, min((j+1)*PP, pages))
-// and PP is the attention kernel's pages per step.  A step costs the same
-// whether it holds PP pages or the last few (its loads are issued for all PP
-// pages), so dealing steps rather than pages keeps the waves' times equal
-// when many requests end in a short step.  The planner clamps each length to
-// the block-table width, scans the steps per request into each request's
-// first unit, and gives every one of the W waves the contiguous range
-// [floor(w*P/W), floor((w+1)*P/W)) of the P units, recording the (b, g, first
-// page) where that range starts.  Requests are split only where a wave
-// boundary falls inside them, and always between steps.
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanMaxBatch = 8192;   // request starts kept in LDS for the search
+// ---------------------------------------------------------- work split ---
+// The work of a call is the flattened sequence of units (request b, KV head
+// g, step j), request-major, then head, then step, where step j of a
+// (request, head) covers its pages [j*PP, min((j+1)*PP, pages)) and PP is the
+// attention kernel's pages per step.  A step costs the same whether it holds
+// PP pages or the last few (its loads are issued for all PP pages), so
+// dealing steps rather than pages keeps the waves' times equal when many
+// requests end in a short step.  Each of the W waves takes the contiguous
+// range [floor(w*P/W), floor((w+1)*P/W)) of the P units.  Requests are split
+// only where a wave boundary falls inside them, and always between steps.
+// Each wave finds its own range from the lengths (no planner launch): it
+// sums the steps of the whole batch, then scans the requests' first units up
+// to the one holding its first unit.  Lengths are clamped to the block-table
+// width.
+constexpr int kPlanPerLane = 16;                        // lengths per lane per load batch
+constexpr int kPlanBatch = kPlanPerLane * kWaveSize;   // 1024 requests
 
-__global__ void __launch_bounds__(kPlanThreads) plan_kernel(AttnArgs a) {
-    __shared__ int first[kPlanMaxBatch + 1];
-    __shared__ int scan[kPlanThreads];
-    __shared__ int carry;
-    const int tid = threadIdx.x;
-    const int maxL = a.max_pages * kPage;
-    if (tid == 0) carry = 0;
-    __syncthreads();
-    for (int base = 0; base < a.B; base += kPlanThreads) {
-        const int b = base + tid;
-        int units = 0, L = 0, np = 0, ns = 0;
-        if (b < a.B) {
-            L = a.seq_lens[b];
-            if (L < 0 || L > maxL) {
-                atomicOr(&a.hdr->err_flags, kErrLength);
-                L = L < 0 ? 0 : maxL;
-            }
-            np = (L + kPage - 1) / kPage;
-            ns = (np + a.pp - 1) / a.pp;
-            units = ns * a.H_kv;
-        }
-        scan[tid] = units;
-        __syncthreads();
-        for (int off = 1; off < kPlanThreads; off <<= 1) {
-            const int v = tid >= off ? scan[tid - off] : 0;
-            __syncthreads();
-            scan[tid] += v;
-            __syncthreads();
-        }
-        const int excl = carry + scan[tid] - units;
-        if (b < a.B) {
-            first[b] = excl;
-            a.b_info[b] = make_int4(excl, np, L, ns);
-        }
-        __syncthreads();
-        if (tid == kPlanThreads - 1) carry += scan[kPlanThreads - 1];
-        __syncthreads();
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+    for (int o = 1; o < kWaveSize; o <<= 1) {
+        const int t = __shfl_up(v, o, kWaveSize);
+        if (lane >= o) v += t;
     }
-    const int P = carry;
-    if (tid == 0) {
-        first[a.B] = P;
-        a.hdr->total_units = P;
-    }
-    __syncthreads();
-    for (int w = tid; w < a.waves; w += kPlanThreads) {
-        const int x = (int)((int64_t)w * P / a.waves);
-        const int x1 = (int)((int64_t)(w + 1) * P / a.waves);
-        int4 ws = make_int4(-1, 0, 0, 0);
-        if (x < x1) {
-            // last request whose first unit is <= x (it has steps, since x < P)
-            int lo = 0, hi = a.B - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (first[mid] <= x) lo = mid; else hi = mid - 1;
-            }
-            const int ns = (first[lo + 1] - first[lo]) / a.H_kv;
-            const int off = x - first[lo];
-            ws = make_int4(lo, off / ns, (off % ns) * a.pp, 0);
-        }
-        a.wave_start[w] = ws;
-    }
+    return v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int o = kWaveSize / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, kWaveSize);
+    return v;
 }
 
 // ------------------------------------------------ partial attention (MFMA) --
@@ -726,9 +679,8 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1
             // units remain, so a later request with pages exists
             do {
                 ++c.b;
-                const int4 bi = a.b_info[c.b];
-                c.np = bi.y;
-                c.L = bi.z;
+                c.L = min(max(a.seq_lens[c.b], 0), a.max_pages * kPage);
+                c.np = (c.L + kPage - 1) / kPage;
             } while (c.np == 0 && c.b + 1 < a.B);
         }
     }
@@ -751,9 +703,86 @@ attn_mfma_kernel(AttnArgs a) {
     // wave index, made provably uniform so that all stream bookkeeping is scalar
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6));
     if (w >= a.waves) return;
-    const int P = a.hdr->total_units;
+
+    // This wave's range of the P units (see the work split above).  Lane l
+    // holds requests b0 + 16 l .. b0 + 16 l + 15 of each batch of lengths, so
+    // one scan over the lanes gives every lane's first unit.
+    const int maxL = a.max_pages * kPage;
+    int Lk[kPlanPerLane], uk[kPlanPerLane];
+    bool bad_len = false;
+    auto load_lens = [&](int b0) -> int {   // this lane's units in the batch
+        int sum = 0;
+#pragma unroll
+        for (int k = 0; k < kPlanPerLane; ++k) {
+            const int b = b0 + kPlanPerLane * lane + k;
+            int L = b < a.B ? a.seq_lens[b] : 0;
+            if (L < 0 || L > maxL) {
+                bad_len = true;
+                L = L < 0 ? 0 : maxL;
+            }
+            Lk[k] = L;
+            uk[k] = ((L + kPage - 1) / kPage + PP - 1) / PP * a.H_kv;
+            sum += uk[k];
+        }
+        return sum;
+    };
+    int lsum = load_lens(0);
+    int incl = wave_incl_scan(lsum, lane);
+    int P = __builtin_amdgcn_readlane(incl, kWaveSize - 1);
+    for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch)
+        P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
     const int r0 = (int)((int64_t)w * P / a.waves);
     const int r1 = (int)((int64_t)(w + 1) * P / a.waves);
+    // wave 0 also writes each request's (first unit, pages, length, steps per
+    // head) and P for the merge kernel, and raises the length flag
+    const bool lead = w == 0;
+    if (lead) {
+        if (__any(bad_len) && lane == 0) atomicOr(&a.hdr->err_flags, kErrLength);
+        if (lane == 0) a.hdr->total_units = P;
+    }
+    if (r0 >= r1 && !lead) return;
+    int sb = -1, sg = 0, sp = 0, sL = 0;   // request, KV head, page, length at unit r0
+    int carry = 0;                         // units of the requests before this batch
+    for (int b0 = 0; b0 < a.B; b0 += kPlanBatch) {
+        if (b0 > 0) {
+            lsum = load_lens(b0);
+            incl = wave_incl_scan(lsum, lane);
+        } else if (a.B > kPlanBatch) {
+            lsum = load_lens(0);
+            incl = wave_incl_scan(lsum, lane);
+        }
+        const int excl = carry + incl - lsum;
+        if (lead) {
+            int f = excl;
+#pragma unroll
+            for (int k = 0; k < kPlanPerLane; ++k) {
+                const int b = b0 + kPlanPerLane * lane + k;
+                if (b < a.B) a.b_info[b] = make_int4(f, (Lk[k] + kPage - 1) / kPage, Lk[k], uk[k] / a.H_kv);
+                f += uk[k];
+            }
+        }
+        const uint64_t hit = __ballot(lsum > 0 && excl <= r0 && r0 < excl + lsum);
+        if (sb < 0 && hit != 0 && r0 < r1) {
+            // walk the 16 requests of the lane that holds unit r0
+            const int src = __ffsll((unsigned long long)hit) - 1;
+            int x = __builtin_amdgcn_readlane(excl, src);
+#pragma unroll
+            for (int k = 0; k < kPlanPerLane; ++k) {
+                const int u = __builtin_amdgcn_readlane(uk[k], src);
+                if (sb < 0 && r0 < x + u) {
+                    const int ns = u / a.H_kv;
+                    const int off = r0 - x;
+                    sb = b0 + kPlanPerLane * src + k;
+                    sL = __builtin_amdgcn_readlane(Lk[k], src);
+                    sg = off / ns;
+                    sp = off % ns * PP;
+                }
+                x += u;
+            }
+        }
+        carry += __builtin_amdgcn_readlane(incl, kWaveSize - 1);
+        if (sb >= 0 && !lead) break;
+    }
     if (r0 >= r1) return;
 
     const size_t tile_bytes = (size_t)D * kPage * EB;
@@ -765,13 +794,11 @@ attn_mfma_kernel(AttnArgs a) {
     // cur[DEPTH+1] has its block-table entries in flight.
     Cursor cur[DEPTH + 2];
     {
-        const int4 ws = a.wave_start[w];
-        const int4 bi = a.b_info[ws.x];
-        cur[0].b = ws.x;
-        cur[0].g = ws.y;
-        cur[0].p = ws.z;
-        cur[0].np = bi.y;
-        cur[0].L = bi.z;
+        cur[0].b = __builtin_amdgcn_readfirstlane(sb);
+        cur[0].g = __builtin_amdgcn_readfirstlane(sg);
+        cur[0].p = __builtin_amdgcn_readfirstlane(sp);
+        cur[0].L = __builtin_amdgcn_readfirstlane(sL);
+        cur[0].np = (cur[0].L + kPage - 1) / kPage;
         cur[0].x = r0;
         cur[0].live = true;
         cursor_len<PP>(cur[0]);
@@ -1008,22 +1035,48 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     auto has_units = [&](int v) {
         return (int64_t)v * P / W < (int64_t)(v + 1) * P / W;
     };
-    float M = -INFINITY;
-    for (int v = wf; v <= wl; ++v)
-        if (has_units(v)) M = fmaxf(M, a.part_ml[(seg + v) * a.G + n].x);
-    float l = 0.f;
+    // Online merge over batches of kBatch pieces: every load of a batch is
+    // issued before any is used (indices past wl are clamped to wl, so every
+    // read is of a written slot range), and a piece of a wave that has no
+    // units gets weight 0 after the load.  Wave wf holds unit x0, so the
+    // first batch sets a finite M.
+    constexpr int kBatch = 4;
+    float M = -INFINITY, l = 0.f;
     float acc[D / kWaveSize];
 #pragma unroll
     for (int k = 0; k < D / kWaveSize; ++k) acc[k] = 0.f;
-    for (int v = wf; v <= wl; ++v) {
-        if (!has_units(v)) continue;
-        const int64_t slot = (seg + v) * a.G + n;
-        const float2 ml = a.part_ml[slot];
-        const float wt = fast_exp2(ml.x - M);
-        l += wt * ml.y;
-        const float* po = a.part_o + slot * D;
+    for (int v0 = wf; v0 <= wl; v0 += kBatch) {
+        float2 ml[kBatch];
+        float o[kBatch][D / kWaveSize];
 #pragma unroll
-        for (int k = 0; k < D / kWaveSize; ++k) acc[k] += wt * po[lane + kWaveSize * k];
+        for (int j = 0; j < kBatch; ++j) {
+            const int64_t slot = (seg + min(v0 + j, wl)) * a.G + n;
+            ml[j] = a.part_ml[slot];
+#pragma unroll
+            for (int k = 0; k < D / kWaveSize; ++k) o[j][k] = a.part_o[slot * D + lane + kWaveSize * k];
+        }
+        float Mb = M;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const bool live = v0 + j <= wl && has_units(v0 + j);
+            if (!live) ml[j] = make_float2(-INFINITY, 0.f);
+            Mb = fmaxf(Mb, ml[j].x);
+        }
+        if (Mb > M) {             // exact: otherwise the factor is 1
+            const float r = fast_exp2(M - Mb);
+            l *= r;
+#pragma unroll
+            for (int k = 0; k < D / kWaveSize; ++k) acc[k] *= r;
+            M = Mb;
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const bool live = ml[j].x != -INFINITY;
+            const float wt = live ? fast_exp2(ml[j].x - M) : 0.f;
+            l += live ? wt * ml[j].y : 0.f;
+#pragma unroll
+            for (int k = 0; k < D / kWaveSize; ++k) acc[k] += live ? wt * o[j][k] : 0.f;
+        }
     }
     const float inv = 1.f / l;
 #pragma unroll
@@ -1037,10 +1090,6 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 void launch_kv_append(const AppendArgs& a, hipStream_t s) {
     if (a.B == 0) return;
     hipLaunchKernelGGL(kv_append_kernel, dim3(a.B), dim3(256), 0, s, a);
-}
-
-void launch_plan(const AttnArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, a);
 }
 
 template <int D, bool FP8, int PP, int DEPTH>
