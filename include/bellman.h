@@ -129,7 +129,10 @@ int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_n
  * Limits: B <= 8192 and B * H_kv * maxP < 2^31.  Scratch memory is a
  * per-device library workspace grown on demand (hipMalloc) and released by
  * bellman_shutdown(); calls on different streams of one device must not
- * overlap in time.
+ * overlap in time.  Once the workspace has grown to a call's size (an
+ * earlier call of the same shape), the call enqueues only kernels on
+ * `stream`: no memset, copy or host wait, so it can be captured in a HIP
+ * graph and replayed.
  */
 int bellman_decode_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                              const bellman_tensor_t *v_pages,
@@ -191,7 +194,9 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
  *   seq_lens      int32 [B] contiguous (read, then advanced).
  * Byte-exact copies; nothing else is written.  A token outside its
  * request's table or the pool is skipped and flagged (flag 1), and that
- * request's length is left unchanged when its last position does not fit. */
+ * request's length is left unchanged when its last position does not fit.
+ * Once the workspace has grown to the call's size, the call enqueues only
+ * kernels on `stream` (graph-capturable). */
 int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_new,
                      bellman_tensor_t *k_pages, bellman_tensor_t *v_pages,
                      const bellman_tensor_t *block_table, bellman_tensor_t *seq_lens,
@@ -213,7 +218,9 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *                0 or ends past T writes no row at all (flag 2).
  * Each workgroup takes 128 query rows of one request and one query head;
  * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo.  Scratch:
- * B + 1 integers of the per-device workspace. */
+ * B + 1 integers of the per-device workspace.  Like bellman_kv_write, once
+ * the workspace has grown to the call's size the call enqueues only kernels
+ * (graph-capturable). */
 int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                               const bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
                               const bellman_tensor_t *seq_lens, const bellman_tensor_t *q_start,
