@@ -440,6 +440,8 @@ prefill_attn_kernel(PrefillArgs a) {
     }
     f32x16 sca[NH], scb[NH];
     if (0 < wave_steps) qk(kb0, sca);
+    // step 0 copies K(2) over K(0): every wave's reads of K(0) come first
+    __syncthreads();
 
     // one step; sc holds S(s), scn receives S(s + 1)
     auto step = [&](auto par, const int s, f32x16 (&sc)[NH], f32x16 (&scn)[NH]) {
