@@ -285,6 +285,25 @@ def test_random_shapes_and_splits(seed):
                 assert np.all(got[b] == 0.0)
 
 
+@pytest.mark.parametrize("B,kv", [(2500, "bf16"), (8192, "fp8")])
+def test_large_batches_of_short_requests(B, kv):
+    # more than 1024 requests: every attention wave reads the lengths in
+    # several batches of 1024 to find its share
+    rng = np.random.default_rng(B)
+    lens = rng.integers(0, 60, size=B)
+    lens[rng.random(B) < 0.2] = 0
+    case = dn.random_case(rng, B, 8, 2, 64, [int(x) for x in lens], kv)
+    if kv == "fp8":
+        case["k_scale"] = (rng.uniform(0.5, 1.5, size=(B, 2)) / 40.0).astype(np.float32)
+        case["v_scale"] = (rng.uniform(0.5, 1.5, size=(B, 2)) / 40.0).astype(np.float32)
+    scale = 0.125
+    ref = oracle_case(case, scale, kv)
+    for waves, pps in ((0, 0), (1, 1), (37, 2), (3000, 0)):
+        got = run_case(dev_case(case, kv), scale, max_waves=waves, pages_per_step=pps)
+        G.assert_close(got, ref, kv, f"B={B} {kv} waves={waves} pages/step={pps}")
+        assert np.all(got[lens == 0] == 0.0)
+
+
 def test_fp8_every_code_through_single_token_rows():
     """Length-1 requests return their V row times the V scale; with scale 1 the
     output is the e4m3fn value itself, so every finite code is checked."""
