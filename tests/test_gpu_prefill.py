@@ -125,6 +125,29 @@ def test_prefill_matches_oracle(case, split):
     assert_close(_out_f64(out), ref, "bf16" if split else "bf16_p1", f"{name} split={split}")
 
 
+def test_prefill_many_requests():
+    # 1500 short requests (many with nothing cached or nothing new): the
+    # write's and the attention's planners scan the batch in several chunks
+    rng = np.random.default_rng(1500)
+    B = 1500
+    cached = [int(x) for x in rng.integers(0, 40, size=B) * (rng.random(B) < 0.7)]
+    new = [int(x) for x in rng.integers(0, 21, size=B) * (rng.random(B) < 0.8)]
+    w = wl.build_prefill(cached=cached, new=new, H_q=8, H_kv=2, D=64, seed=1500, device="cuda")
+    kp0, vp0 = _host_pools(w)
+    sl0 = w.seq_lens.cpu().numpy().astype(np.int32)
+    _write(w)
+    assert bl.device_errors() == 0
+    kp, vp = _host_pools(w)
+    kx, vx, sx = kp0.copy(), vp0.copy(), sl0.copy()
+    oracle.kv_write(bits16(w.k_new), bits16(w.v_new), kx, vx, w.block_table.cpu().numpy(), sx, w.q_start.cpu().numpy())
+    assert np.array_equal(kp, kx) and np.array_equal(vp, vx), "prompt write bytes"
+    assert np.array_equal(w.seq_lens.cpu().numpy(), sx)
+    out = torch.full((w.T, 8, 64), float("nan"), dtype=torch.bfloat16, device="cuda")
+    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
+    assert bl.device_errors() == 0
+    assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16", "1500 requests")
+
+
 def test_prefill_strided_rows():
     # q and out as column slices of wider tensors (row strides above H * D)
     cached, new, H_q, H_kv, D = [3, 0], [150, 40], 8, 2, 128
