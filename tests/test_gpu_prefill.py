@@ -125,6 +125,50 @@ def test_prefill_matches_oracle(case, split):
     assert_close(_out_f64(out), ref, "bf16" if split else "bf16_p1", f"{name} split={split}")
 
 
+def _sweep_counts(rng, B, edge):
+    out = []
+    for _ in range(B):
+        kind = rng.integers(0, 4)
+        if kind == 0:
+            out.append(0)
+        elif kind == 1:
+            out.append(int(edge * rng.integers(1, 6) + rng.integers(-1, 2)))
+        else:
+            out.append(int(rng.integers(1, 400)))
+    return out
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_prefill_random_sweep(seed):
+    # seeded shapes: GQA group, head_dim, cached prefixes and new-token counts
+    # on and next to page (16), step (64) and tile (128) edges, empty chunks
+    rng = np.random.default_rng(7000 + seed)
+    H_kv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 3, 4, 8, 16]))
+    D = 64 if seed % 2 else 128
+    B = int(rng.integers(1, 7))
+    cached = _sweep_counts(rng, B, 16)
+    new = _sweep_counts(rng, B, int(rng.choice([16, 64, 128])))
+    split = bool(seed % 3)
+    w = wl.build_prefill(cached=cached, new=new, H_q=G * H_kv, H_kv=H_kv, D=D, seed=7000 + seed, device="cuda")
+    kp0, vp0 = _host_pools(w)
+    sl0 = w.seq_lens.cpu().numpy().astype(np.int32)
+    _write(w)
+    assert bl.device_errors() == 0
+    kp, vp = _host_pools(w)
+    kx, vx, sx = kp0.copy(), vp0.copy(), sl0.copy()
+    oracle.kv_write(bits16(w.k_new), bits16(w.v_new), kx, vx, w.block_table.cpu().numpy(), sx, w.q_start.cpu().numpy())
+    what = f"seed={seed} G={G} H_kv={H_kv} D={D} cached={cached} new={new} split={split}"
+    assert np.array_equal(kp, kx) and np.array_equal(vp, vx), what
+    if w.T == 0:
+        return
+    out = torch.full((w.T, G * H_kv, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
+                         split_p=split)
+    assert bl.device_errors() == 0
+    assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16" if split else "bf16_p1", what)
+
+
 def test_prefill_many_requests():
     # 1500 short requests (many with nothing cached or nothing new): the
     # write's and the attention's planners scan the batch in several chunks
