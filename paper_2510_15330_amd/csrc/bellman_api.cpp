@@ -31,6 +31,7 @@ int fail(int code, const char* fmt, ...) {
 // ------------------------------------------------------------- workspace ---
 
 constexpr int kMaxDevices = 64;
+constexpr int kXcdSkew = 10;          // share weights 266 : 246, even : odd XCDs (measured best of 0-28)
 constexpr int kMaxAttnBatch = 8192;  // lengths every attention wave reads to find its share
 
 struct Workspace {
@@ -441,6 +442,7 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.max_pages = (int)max_pages;
     a.waves = (int)waves;
     a.pp = pps;
+    a.skew = bpc == 1 ? kXcdSkew : 0;   // one workgroup per CU (two share each CU at depth 1)
     a.hdr = (WorkspaceHeader*)base;
     a.b_info = (int4*)(base + off_binfo);
     a.part_ml = (float2*)(base + off_ml);

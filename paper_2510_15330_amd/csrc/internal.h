@@ -58,6 +58,7 @@ struct AttnArgs {
     int B, H_q, H_kv, G, D, max_pages;
     int waves;           // waves sharing the flattened step stream (the grid's waves)
     int pp;              // pages per step of the launched attention kernel
+    int skew;            // share weights 256 + skew (even-XCD workgroups) / 256 - skew on long shares; 0..255
     // workspace
     WorkspaceHeader* hdr;
     int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head),

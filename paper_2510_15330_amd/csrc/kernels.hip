@@ -156,6 +156,34 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 constexpr int kPlanPerLane = 16;                        // lengths per lane per load batch
 constexpr int kPlanBatch = kPlanPerLane * kWaveSize;   // 1024 requests
 
+// Shares by weight.  Workgroup i runs on XCD i mod 8, and waves on the
+// odd-numbered XCDs were measured to stream 4-5% slower than those on the
+// even ones; with skew k the waves of even-XCD workgroups (w / 4 even) weigh
+// 256 + k and the others 256 - k, and wave w's range starts at unit
+// floor(C(w) P / C(W)), C the cumulative weight (k = 0: equal shares).  The
+// skew applies only to long shares (at least kSkewMinSteps steps a wave),
+// where the rate difference, not the ramp, sets the finish.
+constexpr int kSkewMinSteps = 256;
+__device__ __forceinline__ int share_skew(int skew, int P, int W) {
+    return (int64_t)P >= (int64_t)kSkewMinSteps * W ? skew : 0;
+}
+__device__ __forceinline__ int64_t share_weight(int w, int skew) {
+    const int64_t a = 256 + skew, b = 256 - skew;
+    const int r = w & 7;
+    return (int64_t)(w >> 3) * 4 * (a + b) + (r <= 4 ? r * a : 4 * a + (r - 4) * b);
+}
+__device__ __forceinline__ int share_bound(int w, int P, int W, int skew) {
+    return (int)(share_weight(w, skew) * P / share_weight(W, skew));
+}
+// the wave v with share_bound(v) <= x < share_bound(v + 1), for 0 <= x < P
+__device__ __forceinline__ int wave_of(int x, int P, int W, int skew) {
+    const int64_t a = 256 + skew, b = 256 - skew;
+    const int64_t c = ((int64_t)(x + 1) * share_weight(W, skew) - 1) / P;   // largest C(v) with v's start <= x
+    const int64_t q = c / (4 * (a + b)), rem = c - q * 4 * (a + b);
+    const int64_t v = 8 * q + (rem <= 4 * a ? rem / a : 4 + (rem - 4 * a) / b);
+    return (int)min(v, (int64_t)W - 1);
+}
+
 __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
 #pragma unroll
     for (int o = 1; o < kWaveSize; o <<= 1) {
@@ -731,8 +759,9 @@ attn_mfma_kernel(AttnArgs a) {
     int P = __builtin_amdgcn_readlane(incl, kWaveSize - 1);
     for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch)
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
-    const int r0 = (int)((int64_t)w * P / a.waves);
-    const int r1 = (int)((int64_t)(w + 1) * P / a.waves);
+    const int skew = share_skew(a.skew, P, a.waves);
+    const int r0 = share_bound(w, P, a.waves, skew);
+    const int r1 = share_bound(w + 1, P, a.waves, skew);
     // wave 0 also writes each request's (first unit, pages, length, steps per
     // head) and P for the merge kernel, and raises the length flag
     const bool lead = w == 0;
@@ -1005,11 +1034,6 @@ attn_mfma_kernel(AttnArgs a) {
 //   M = max_i m_i,  l = sum_i 2^(m_i - M) l_i,  out = sum_i 2^(m_i - M) o_i / l
 // A request's head that one wave covered whole was written by that wave;
 // requests of length 0 get zeros.
-__device__ __forceinline__ int wave_of(int x, int P, int W) {
-    // the wave w with floor(w P / W) <= x < floor((w + 1) P / W)
-    return (int)(((int64_t)(x + 1) * W - 1) / P);
-}
-
 template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int wid = blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6);
@@ -1028,12 +1052,13 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int W = a.waves;
     const int ns = bi.w;                 // steps per KV head
     const int x0 = bi.x + g * ns;
-    const int wf = wave_of(x0, P, W);
-    const int wl = wave_of(x0 + ns - 1, P, W);
+    const int skew = share_skew(a.skew, P, W);
+    const int wf = wave_of(x0, P, W, skew);
+    const int wl = wave_of(x0 + ns - 1, P, W, skew);
     if (wf == wl) return;
     const int64_t seg = (int64_t)b * a.H_kv + g;
     auto has_units = [&](int v) {
-        return (int64_t)v * P / W < (int64_t)(v + 1) * P / W;
+        return share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew);
     };
     // Online merge over batches of kBatch pieces: every load of a batch is
     // issued before any is used (indices past wl are clamped to wl, so every

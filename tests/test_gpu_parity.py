@@ -285,6 +285,18 @@ def test_random_shapes_and_splits(seed):
                 assert np.all(got[b] == 0.0)
 
 
+def test_long_shares_with_weighted_split():
+    # shares of 256 steps or more a wave take the even/odd-XCD weights, also
+    # with wave counts that do not fill a period of eight
+    rng = np.random.default_rng(8192)
+    case = dn.random_case(rng, 2, 32, 8, 128, [8192, 3000], "bf16")
+    scale = float(np.float32(1.0 / np.sqrt(128)))
+    ref = oracle_case(case, scale)
+    for waves in (1, 3, 5, 7, 9):
+        got = run_case(dev_case(case), scale, max_waves=waves, pages_per_step=2, pipeline_depth=2)
+        G.assert_close(got, ref, "bf16", f"long shares waves={waves}")
+
+
 @pytest.mark.parametrize("B,kv", [(2500, "bf16"), (8192, "fp8")])
 def test_large_batches_of_short_requests(B, kv):
     # more than 1024 requests: every attention wave reads the lengths in
