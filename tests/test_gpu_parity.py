@@ -354,6 +354,27 @@ def test_bad_block_table_entry_is_flagged_not_read():
                                              seq_lens=case["seq_lens"][1:]), 0.125), "bf16", "untouched request")
 
 
+def test_lengths_outside_the_table_are_clamped_and_flagged():
+    # a negative length attends nothing (zeros); a length past the table's
+    # width attends the whole row of pages; both raise the length flag
+    rng = np.random.default_rng(25)
+    case = dn.random_case(rng, 3, 8, 2, 64, [0, 48, 30])   # request 1 fills its three pages
+    maxL = case["block_table"].shape[1] * 16
+    assert maxL == 48
+    ref = oracle_case(case, 0.125)
+    for waves in (0, 1, 2, 5):
+        d = dev_case(case)
+        sl = d["sl"].clone()
+        sl[0] = -5
+        sl[1] = maxL + 7
+        d["sl"] = sl
+        bl.device_errors()
+        got = run_case(d, 0.125, max_waves=waves)
+        assert bl.device_errors() & 2, f"waves={waves}"
+        assert np.all(got[0] == 0.0)
+        G.assert_close(got[1:], ref[1:], "bf16", f"clamped lengths waves={waves}")
+
+
 def test_append_out_of_table_is_skipped():
     w = G.to_device(wl.build("tiny", seed=2))
     before_k = G.bits16(w.k_pages)
