@@ -146,9 +146,10 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 // attention kernel's pages per step.  A step costs the same whether it holds
 // PP pages or the last few (its loads are issued for all PP pages), so
 // dealing steps rather than pages keeps the waves' times equal when many
-// requests end in a short step.  Each of the W waves takes the contiguous
-// range [floor(w*P/W), floor((w+1)*P/W)) of the P units.  Requests are split
-// only where a wave boundary falls inside them, and always between steps.
+// requests end in a short step.  Each of the W waves takes a contiguous
+// range of the P units: equal ranges [floor(w*P/W), floor((w+1)*P/W)), or
+// the weighted ones below.  Requests are split only where a wave boundary
+// falls inside them, and always between steps.
 // Each wave finds its own range from the lengths (no planner launch): it
 // sums the steps of the whole batch, then scans the requests' first units up
 // to the one holding its first unit.  Lengths are clamped to the block-table
