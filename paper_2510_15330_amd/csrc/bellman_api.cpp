@@ -442,7 +442,10 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
     a.max_pages = (int)max_pages;
     a.waves = (int)waves;
     a.pp = pps;
-    a.skew = bpc == 1 ? kXcdSkew : 0;   // one workgroup per CU (two share each CU at depth 1)
+    // the XCD weights were measured on a whole MI355X (256 CUs, workgroup i on
+    // XCD i mod 8) with one workgroup per CU; partitioned devices and two
+    // workgroups per CU (depth 1) keep equal shares
+    a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
     a.hdr = (WorkspaceHeader*)base;
     a.b_info = (int4*)(base + off_binfo);
     a.part_ml = (float2*)(base + off_ml);
