@@ -5,6 +5,7 @@
 // (arXiv 2510.15330, Sec. 3) controls: every request attends its one new
 // query token over its own KV cache (prompt plus tokens generated so far).
 #include "internal.h"
+#include "work_split.h"
 
 #include <math.h>
 
@@ -140,50 +141,16 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
 }
 
 // ---------------------------------------------------------- work split ---
-// The work of a call is the flattened sequence of units (request b, KV head
-// g, step j), request-major, then head, then step, where step j of a
-// (request, head) covers its pages [j*PP, min((j+1)*PP, pages)) and PP is the
-// attention kernel's pages per step.  A step costs the same whether it holds
-// PP pages or the last few (its loads are issued for all PP pages), so
-// dealing steps rather than pages keeps the waves' times equal when many
-// requests end in a short step.  Each of the W waves takes a contiguous
-// range of the P units: equal ranges [floor(w*P/W), floor((w+1)*P/W)), or
-// the weighted ones below.  Requests are split only where a wave boundary
-// falls inside them, and always between steps.
-// Each wave finds its own range from the lengths (no planner launch): it
-// sums the steps of the whole batch, then scans the requests' first units up
-// to the one holding its first unit.  Lengths are clamped to the block-table
-// width.
+// Each wave finds its own range of the flattened step stream (work_split.h)
+// from the lengths (no planner launch): it sums the steps of the whole batch,
+// then scans the requests' first units up to the one holding its first unit.
+// Lengths are clamped to the block-table width.  A step costs the same
+// whether it holds PP pages or the last few (its loads are issued for all PP
+// pages), so dealing steps rather than pages keeps the waves' times equal
+// when many requests end in a short step.  Requests are split only where a
+// wave boundary falls inside them, and always between steps.
 constexpr int kPlanPerLane = 16;                        // lengths per lane per load batch
 constexpr int kPlanBatch = kPlanPerLane * kWaveSize;   // 1024 requests
-
-// Shares by weight.  Workgroup i runs on XCD i mod 8, and waves on the
-// odd-numbered XCDs were measured to stream 4-5% slower than those on the
-// even ones; with skew k the waves of even-XCD workgroups (w / 4 even) weigh
-// 256 + k and the others 256 - k, and wave w's range starts at unit
-// floor(C(w) P / C(W)), C the cumulative weight (k = 0: equal shares).  The
-// skew applies only to long shares (at least kSkewMinSteps steps a wave),
-// where the rate difference, not the ramp, sets the finish.
-constexpr int kSkewMinSteps = 256;
-__device__ __forceinline__ int share_skew(int skew, int P, int W) {
-    return (int64_t)P >= (int64_t)kSkewMinSteps * W ? skew : 0;
-}
-__device__ __forceinline__ int64_t share_weight(int w, int skew) {
-    const int64_t a = 256 + skew, b = 256 - skew;
-    const int r = w & 7;
-    return (int64_t)(w >> 3) * 4 * (a + b) + (r <= 4 ? r * a : 4 * a + (r - 4) * b);
-}
-__device__ __forceinline__ int share_bound(int w, int P, int W, int skew) {
-    return (int)(share_weight(w, skew) * P / share_weight(W, skew));
-}
-// the wave v with share_bound(v) <= x < share_bound(v + 1), for 0 <= x < P
-__device__ __forceinline__ int wave_of(int x, int P, int W, int skew) {
-    const int64_t a = 256 + skew, b = 256 - skew;
-    const int64_t c = ((int64_t)(x + 1) * share_weight(W, skew) - 1) / P;   // largest C(v) with v's start <= x
-    const int64_t q = c / (4 * (a + b)), rem = c - q * 4 * (a + b);
-    const int64_t v = 8 * q + (rem <= 4 * a ? rem / a : 4 + (rem - 4 * a) / b);
-    return (int)min(v, (int64_t)W - 1);
-}
 
 __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
 #pragma unroll
