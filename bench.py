@@ -2,21 +2,27 @@
 
 A step is one decode step of the batch: bellman_kv_append (one token per
 request) followed by bellman_decode_attention over the paged cache, for one
-layer.  The default workload is the 256-request summarization batch under
+layer.  The headline workload is the 256-request summarization batch under
 load (32 query / 8 KV heads, head_dim 128, bf16, KV length = prompt
 U{6000..12000} + generated lognormal(median 500, sigma 0.5) clipped to 1500,
-50 steps); the same batch with beLLMan's per-request caps {100, 200, 400} is
-measured beside it.  Inputs are synthetic and resident in HBM before timing.
+50 steps).  The default run also measures, each in a sub-object of the same
+JSON line: the same batch with beLLMan's per-request caps {100, 200, 400};
+equal versus XCD-weighted work shares on the headline batch; the
+Llama-3-8B-shaped batch (64 requests, 100 steps, eager and replayed from one
+HIP graph); the 512-request fp8 stress batch; and the prompt path (write +
+causal prompt attention of four 6-12k-token prompts).  Inputs are synthetic
+and resident in HBM before timing.
 
-``--workload prefill_summarization`` (or ``prefill_chunked``) measures the
-prompt path instead: the prompt write and causal prompt attention of four
-6-12k-token prompts (or their last 2048-token chunks), priced against the
-bf16 matrix-core peak.
+``--workload NAME`` measures one batch alone (``prefill_summarization`` or
+``prefill_chunked`` measure the prompt path, priced against the bf16
+matrix-core peak).
 
 Prints one JSON line.  ``value`` is the algorithmic HBM traffic of the timed
 steps divided by their wall time (GB/s); ``roofline`` prices the attention
-kernel alone, timed with HIP events the library records around it;
-``cpu_baseline`` is the binary64 oracle on a bounded sample of the same step.
+kernel alone, timed with HIP events the library records around it on the
+stream it launches on (``attention_call_us`` adds the merge of the cut
+requests); ``cpu_baseline`` is the binary64 oracle on a bounded sample of the
+same step.
 """
 from __future__ import annotations
 
@@ -46,58 +52,122 @@ def kernel_sha():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measure(name, steps, warmup, impl, max_waves, pps=0, depth=0, seed=0):
+def pct(a, q):
+    return round(float(np.percentile(a, q)) * 1e6, 2)
+
+
+def decode_run(w, steps, warmup, **kw):
+    """Warm up, reset the lengths, and time `steps` decode steps of `w`.
+
+    Per step, two HIP events the library records bracket the attention
+    kernel, and torch events on the same stream bracket the whole step
+    (append + attention + merge) and the attention call (kernel + merge)."""
     import torch
 
     import paper_2510_15330_amd as bl
-    from paper_2510_15330_amd import workloads as wl
 
-    w = wl.build(name, seed=seed, device="cuda", steps=max(steps, warmup, 1))
     out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
-    lens0 = w.seq_lens.clone()
+    lens0 = torch.from_numpy(w.lens0.astype(np.int32)).cuda()
     stream = torch.cuda.current_stream()
 
-    def step(i, events=None):
+    def step(i, kev=None, cev=None):
+        if cev is not None:
+            cev[0].record(stream)
         bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
         bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
-                            stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, impl=impl,
-                            max_waves=max_waves, events=events, pages_per_step=pps,
-                            pipeline_depth=depth)
+                            stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, events=kev, **kw)
+        if cev is not None:
+            cev[1].record(stream)
 
+    w.seq_lens.copy_(lens0)
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     if bl.device_errors() != 0:
         raise RuntimeError("device error flags set during warmup")
     w.seq_lens.copy_(lens0)                       # timed steps start from the initial state
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in evs:
+    mk = lambda: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    kev, cev = mk(), mk()
+    for a, b in kev + cev:
         a.record(stream)
         b.record(stream)
     torch.cuda.synchronize()
 
-    if torch.distributed.is_available() and torch.distributed.is_initialized():
-        torch.distributed.barrier()
-    torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
-        step(i, evs[i])
+        step(i, kev[i], cev[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    if torch.distributed.is_available() and torch.distributed.is_initialized():
-        torch.distributed.barrier()
 
     if bl.device_errors() != 0:
         raise RuntimeError("device error flags set during the timed steps")
     if not torch.isfinite(out.float()).all():
         raise RuntimeError("non-finite attention output")
-    kt = np.array([a.elapsed_time(b) for a, b in evs]) * 1e-3          # seconds per attention kernel
+    kt = np.array([a.elapsed_time(b) for a, b in kev]) * 1e-3          # attention kernel, s
+    st = np.array([a.elapsed_time(b) for a, b in cev]) * 1e-3          # whole step on the GPU, s
+    ct = np.array([a.elapsed_time(c[1]) for (a, _), c in zip(kev, cev)]) * 1e-3   # attention + merge, s
     wall = t1 - t0
     attn_bytes = np.array([w.algorithmic_bytes(i) for i in range(steps)], dtype=np.float64)
     step_bytes = attn_bytes + w.append_bytes()
-    return dict(w=w, wall=wall, kt=kt, attn_bytes=attn_bytes, step_bytes=step_bytes,
+    return dict(wall=wall, kt=kt, st=st, ct=ct, attn_bytes=attn_bytes, step_bytes=step_bytes, out=out,
                 steps_per_s=steps / wall, gbs=step_bytes.sum() / wall / 1e9,
-                kernel_gbs=attn_bytes.mean() / kt.mean() / 1e9)
+                kernel_gbs=attn_bytes.mean() / kt.mean() / 1e9, call_gbs=attn_bytes.mean() / ct.mean() / 1e9)
+
+
+def graph_run(w, steps, reps=3):
+    """The same `steps` decode steps captured in one HIP graph (after an
+    eager run has grown the workspace) and replayed `reps` times from the
+    initial lengths; returns steps/s of the replays and whether the last
+    step's output equals the eager run's bit for bit."""
+    import torch
+
+    import paper_2510_15330_amd as bl
+
+    out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    lens0 = torch.from_numpy(w.lens0.astype(np.int32)).cuda()
+    w.seq_lens.copy_(lens0)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.graph(g, stream=side):
+        for i in range(steps):
+            bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens)
+            bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
+                                k_scale=w.k_scale, v_scale=w.v_scale)
+    times = []
+    for _ in range(reps):
+        w.seq_lens.copy_(lens0)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e-3)
+    if bl.device_errors() != 0:
+        raise RuntimeError("device error flags set during the graph replays")
+    return out, steps / float(np.mean(times))
+
+
+def summary(w, r, steps):
+    return {
+        "workload": w.name,
+        "batch": w.B, "q_heads": w.H_q, "kv_heads": w.H_kv, "kv_dtype": w.kv,
+        "mean_kv_len": round(float(w.lens_at(0).mean()), 1),
+        "steps": steps,
+        "steps_per_s": round(r["steps_per_s"], 2),
+        "value_gbs": round(r["gbs"], 2),
+        "ms_per_step": round(r["wall"] / steps * 1e3, 4),
+        "attention_kernel_us": {"mean": round(r["kt"].mean() * 1e6, 2), "p10": pct(r["kt"], 10),
+                                "p50": pct(r["kt"], 50), "p90": pct(r["kt"], 90)},
+        "attention_call_us_mean": round(r["ct"].mean() * 1e6, 2),
+        "step_gpu_us_mean": round(r["st"].mean() * 1e6, 2),
+        "bytes_per_launch": int(r["attn_bytes"].mean()),
+        "kernel_gbs": round(r["kernel_gbs"], 2),
+        "frac": round(r["kernel_gbs"] / PEAK_HBM_GBS, 4),
+        "call_frac": round(r["call_gbs"] / PEAK_HBM_GBS, 4),
+    }
 
 
 def cpu_baseline(w, target_s=12.0, min_s=10.0):
@@ -169,7 +239,7 @@ def cpu_baseline(w, target_s=12.0, min_s=10.0):
     }
 
 
-def measure_prefill(name, steps, warmup, split_p=True, seed=0):
+def measure_prefill(name, steps, warmup, seed=0):
     """Prompt path: a step restores the cached lengths (one small copy), writes
     the batch's keys and values into their pages and runs causal prompt
     attention over the cache."""
@@ -187,7 +257,7 @@ def measure_prefill(name, steps, warmup, split_p=True, seed=0):
         w.seq_lens.copy_(lens0)
         bl.kv_write(w.k_new, w.v_new, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, stream=stream)
         bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
-                             stream=stream, split_p=split_p, events=events)
+                             stream=stream, events=events)
 
     for _ in range(warmup):
         step()
@@ -256,7 +326,7 @@ def cpu_baseline_prefill(w, target_s=12.0):
 def main_prefill(args):
     steps = args.steps if args.steps is not None else 20
     log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
-    r = measure_prefill(args.workload, steps, args.warmup, split_p=not args.p_bf16)
+    r = measure_prefill(args.workload, steps, args.warmup)
     w = r["w"]
     log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['tflops']:.1f} TFLOP/s per step, "
         f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_tflops']:.1f} TFLOP/s")
@@ -277,7 +347,7 @@ def main_prefill(args):
             "workload": args.workload, "requests": w.B, "tokens": w.T,
             "cached": [int(x) for x in w.cached], "new": [int(x) for x in w.new],
             "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
-            "p_precision": "bf16" if args.p_bf16 else "bf16 hi+lo", "seed": 0,
+            "p_precision": "bf16 hi+lo", "seed": 0,
         },
         "attention_kernel_us": {
             "mean": round(r["kt"].mean() * 1e6, 2),
@@ -310,7 +380,7 @@ def _cpu_model():
     return "unknown"
 
 
-def traffic_for(name, impl):
+def traffic_for(name):
     """Counter-derived HBM bytes per attention launch, if they were taken on
     the current kernel source (profiles/traffic.json)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -324,6 +394,14 @@ def traffic_for(name, impl):
     return ent.get("bytes_per_launch")
 
 
+def free_cuda():
+    import gc
+
+    import torch
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -333,12 +411,13 @@ def main():
                     choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8",
                              "prefill_summarization", "prefill_chunked"],
                     help="decode batches, or prompt batches (prefill_*: the prompt write + prompt attention)")
-    ap.add_argument("--p-bf16", action="store_true", help="prompt attention: P rounded to bf16 once")
-    ap.add_argument("--impl", default="auto", choices=["auto", "mfma", "valu"])
     ap.add_argument("--max-waves", type=int, default=0, help="cap on waves sharing the work (0 = all resident)")
+    ap.add_argument("--xcd-skew", type=int, default=0,
+                    help="work-share weights of even/odd XCDs: 0 = library default, -1 = equal, 1..255")
     ap.add_argument("--pages-per-step", type=int, default=0, help="1, 2 (or 4 for fp8); 0 = library default")
     ap.add_argument("--pipeline-depth", type=int, default=0, help="1 or 2; 0 = library default")
-    ap.add_argument("--no-capped", action="store_true", help="skip the capped companion run")
+    ap.add_argument("--only", action="store_true",
+                    help="measure the named workload alone (no companion batches)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three plain 1 GiB device-to-device copies (the reference kernel "
@@ -372,12 +451,14 @@ def main():
     if args.workload.startswith("prefill_"):
         main_prefill(args)
         return
-    impl = {"auto": bl.IMPL_AUTO, "mfma": bl.IMPL_MFMA, "valu": bl.IMPL_VALU}[args.impl]
+    knobs = dict(max_waves=args.max_waves, xcd_skew=args.xcd_skew, pages_per_step=args.pages_per_step,
+                 pipeline_depth=args.pipeline_depth)
     steps = args.steps if args.steps is not None else wl.CONFIGS[args.workload]["steps"]
+    full = args.workload == "summarization" and not args.only
 
     log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
-    r = measure(args.workload, steps, args.warmup, impl, args.max_waves, args.pages_per_step, args.pipeline_depth)
-    w = r["w"]
+    w = wl.build(args.workload, seed=0, device="cuda", steps=max(steps, args.warmup, 1))
+    r = decode_run(w, steps, args.warmup, **knobs)
     log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['steps_per_s']:.1f} steps/s, step traffic {r['gbs']:.1f} GB/s, "
         f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_gbs']:.1f} GB/s")
 
@@ -398,7 +479,8 @@ def main():
             "workload": args.workload,
             "batch": w.B, "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
             "kv_dtype": w.kv, "mean_kv_len": round(float(w.lens_at(0).mean()), 1),
-            "impl": args.impl, "max_waves": args.max_waves or "all resident",
+            "max_waves": args.max_waves or "all resident",
+            "xcd_skew": args.xcd_skew or "default",
             "pages_per_step": args.pages_per_step or "default",
             "pipeline_depth": args.pipeline_depth or "default", "seed": 0,
         },
@@ -406,48 +488,93 @@ def main():
         "pct_of_peak": round(100.0 * r["gbs"] / PEAK_HBM_GBS, 2),
         "attention_kernel_us": {
             "mean": round(r["kt"].mean() * 1e6, 2),
-            "p10": round(float(np.percentile(r["kt"], 10)) * 1e6, 2),
-            "p50": round(float(np.percentile(r["kt"], 50)) * 1e6, 2),
-            "p90": round(float(np.percentile(r["kt"], 90)) * 1e6, 2),
+            "p10": pct(r["kt"], 10), "p50": pct(r["kt"], 50), "p90": pct(r["kt"], 90),
         },
+        "attention_call_us_mean": round(r["ct"].mean() * 1e6, 2),
         "roofline": {
             "bound": "hbm",
             "achieved": round(r["kernel_gbs"], 2),
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": round(r["kernel_gbs"] / PEAK_HBM_GBS, 4),
-            "traffic": traffic_for(args.workload, args.impl),
+            "traffic": traffic_for(args.workload),
             "kernel": "attn_mfma_kernel (paged decode attention, partial pieces)",
             "bytes_per_launch": int(r["attn_bytes"].mean()),
+            "call_frac": round(r["call_gbs"] / PEAK_HBM_GBS, 4),
         },
     }
 
-    if args.workload == "summarization" and not args.no_capped:
-        c = measure("summarization_capped", steps, args.warmup, impl, args.max_waves, args.pages_per_step,
-                    args.pipeline_depth)
+    if full:
+        # equal shares against the library's XCD weighting, same batch, same process
+        e = decode_run(w, steps, args.warmup, **dict(knobs, xcd_skew=-1))
+        result["xcd_skew_ab"] = {
+            "default_kernel_us_mean": round(r["kt"].mean() * 1e6, 2),
+            "equal_shares_kernel_us_mean": round(e["kt"].mean() * 1e6, 2),
+            "equal_vs_default": round(float(e["kt"].mean() / r["kt"].mean()), 4),
+        }
+        log(f"[bench] equal shares: attention kernel {e['kt'].mean() * 1e6:.1f} us avg")
+        del e
+
+    if full:
         lens_u, info_u = wl.sample_lengths("summarization", 0)
         lens_c, info_c = wl.sample_lengths("summarization_capped", 0)
         p, gu, gc = info_u["prompt"], info_u["generated"], info_c["generated_capped"]
         # decode-attention tokens over each request's whole generation: sum_{t<=g} (prompt + t)
         req_u = float((gu * p + gu * (gu + 1) / 2).sum())
         req_c = float((gc * p + gc * (gc + 1) / 2).sum())
-        result["capped"] = {
-            "workload": "summarization_capped",
-            "steps_per_s": round(c["steps_per_s"], 2),
-            "value_gbs": round(c["gbs"], 2),
-            "ms_per_step": round(c["wall"] / steps * 1e3, 4),
-            "attention_kernel_us_mean": round(c["kt"].mean() * 1e6, 2),
-            "step_time_vs_uncapped": round((c["wall"] / steps) / (result["ms_per_step"] / 1e3), 4),
-            "bytes_per_step_vs_uncapped": round(float(c["attn_bytes"].mean() / result["roofline"]["bytes_per_launch"]), 4),
-            "decode_steps_per_request_vs_uncapped": round(float(gc.mean() / gu.mean()), 4),
-            "request_attention_bytes_vs_uncapped": round(req_c / req_u, 4),
-        }
+        wc = wl.build("summarization_capped", seed=0, device="cuda", steps=max(steps, args.warmup, 1))
+        c = decode_run(wc, steps, args.warmup, **knobs)
+        result["capped"] = dict(
+            summary(wc, c, steps),
+            step_time_vs_uncapped=round((c["wall"] / steps) / (result["ms_per_step"] / 1e3), 4),
+            bytes_per_step_vs_uncapped=round(float(c["attn_bytes"].mean() / r["attn_bytes"].mean()), 4),
+            decode_steps_per_request_vs_uncapped=round(float(gc.mean() / gu.mean()), 4),
+            request_attention_bytes_vs_uncapped=round(req_c / req_u, 4))
         log(f"[bench] capped: {c['steps_per_s']:.1f} steps/s, {c['gbs']:.1f} GB/s")
-        del c
+        del wc, c
+        free_cuda()
 
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(w)
+    del w, r
+    free_cuda()
+
+    if full:
+        n8 = wl.CONFIGS["llama3_8b"]["steps"]
+        w8 = wl.build("llama3_8b", seed=0, device="cuda", steps=n8)
+        r8 = decode_run(w8, n8, args.warmup)
+        eager_out = r8["out"].clone()
+        gout, g_sps = graph_run(w8, n8)
+        if not torch.equal(gout.view(torch.int16), eager_out.view(torch.int16)):
+            raise RuntimeError("graph replay differs from the eager steps")
+        result["llama3_8b"] = dict(summary(w8, r8, n8), graph_steps_per_s=round(g_sps, 2),
+                                   graph_matches_eager=True)
+        log(f"[bench] llama3_8b: {r8['steps_per_s']:.1f} steps/s eager, {g_sps:.1f} from a graph, "
+            f"attention kernel {r8['kt'].mean() * 1e6:.1f} us")
+        del w8, r8, gout, eager_out
+        free_cuda()
+
+        ns = wl.CONFIGS["stress_fp8"]["steps"]
+        ws = wl.build("stress_fp8", seed=0, device="cuda", steps=ns)
+        rs = decode_run(ws, ns, args.warmup)
+        result["stress_fp8"] = summary(ws, rs, ns)
+        log(f"[bench] stress_fp8: {rs['steps_per_s']:.1f} steps/s, attention kernel {rs['kt'].mean() * 1e6:.1f} us "
+            f"-> {rs['kernel_gbs']:.1f} GB/s")
+        del ws, rs
+        free_cuda()
+
+        rp = measure_prefill("prefill_summarization", 20, 5)
+        result["prefill_summarization"] = {
+            "tokens": rp["w"].T, "kernel_tflops": round(rp["kernel_tflops"], 2),
+            "frac_of_bf16_peak": round(rp["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
+            "attention_kernel_us_mean": round(rp["kt"].mean() * 1e6, 2),
+            "step_tflops": round(rp["tflops"], 2),
+        }
+        log(f"[bench] prefill_summarization: {rp['kernel_tflops']:.1f} TFLOP/s attention kernel")
+        del rp
+        free_cuda()
+
     print(json.dumps(result), flush=True)
 
 

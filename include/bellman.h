@@ -127,12 +127,17 @@ int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_n
  * statistics merged in a second pass.  The shares are planned on the device,
  * so the call never waits for the GPU.
  * Limits: B <= 8192 and B * H_kv * maxP < 2^31.  Scratch memory is a
- * per-device library workspace grown on demand (hipMalloc) and released by
- * bellman_shutdown(); calls on different streams of one device must not
- * overlap in time.  Once the workspace has grown to a call's size (an
- * earlier call of the same shape), the call enqueues only kernels on
- * `stream`: no memset, copy or host wait, so it can be captured in a HIP
- * graph and replayed.
+ * per-device library workspace (partial results of the cut requests),
+ * grown on demand (hipMalloc) and released by bellman_shutdown(); calls on
+ * different streams of one device must not overlap in time.  Growing
+ * allocates a larger block and keeps the previous one until
+ * bellman_shutdown(), so work already enqueued and HIP graphs captured
+ * earlier keep valid scratch; a call that would have to grow the workspace
+ * while its stream is being captured fails with BELLMAN_ERR_UNSUPPORTED
+ * (make the same call, or bellman_reserve_workspace, before capturing).
+ * Once the workspace has grown to a call's size, the call enqueues only
+ * kernels on `stream`: no memset, copy or host wait, so it can be captured
+ * in a HIP graph and replayed.
  */
 int bellman_decode_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                              const bellman_tensor_t *v_pages,
@@ -140,18 +145,17 @@ int bellman_decode_attention(const bellman_tensor_t *q, const bellman_tensor_t *
                              const bellman_tensor_t *seq_lens, float scale,
                              bellman_tensor_t *out, void *stream);
 
-/* Kernel choice for bellman_decode_attention_opts. */
-typedef enum bellman_attn_impl {
-    BELLMAN_IMPL_AUTO = 0,  /* the library's choice for the shape */
-    BELLMAN_IMPL_MFMA = 1,  /* QK^T and PV on the matrix cores */
-    BELLMAN_IMPL_VALU = 2   /* QK^T and PV on the vector ALUs */
-} bellman_attn_impl_t;
-
 typedef struct bellman_attn_opts {
     int32_t max_waves;    /* cap on the waves that share the work; 0 = every wave the
                              GPU can keep resident.  Fewer waves split fewer
                              requests (results agree within rounding). */
-    int32_t impl;         /* bellman_attn_impl_t */
+    int32_t xcd_skew;     /* share weights of the waves of even- and odd-numbered
+                             XCDs (workgroup i runs on XCD i mod 8), applied only
+                             when every wave gets at least 256 steps:
+                             0 = the library's choice (k = 10 on a whole 256-CU
+                             device with one workgroup per CU, equal shares
+                             otherwise); -1 = equal shares; k in 1..255 = weights
+                             256 + k : 256 - k.  Results agree within rounding. */
     int32_t pages_per_step; /* 16-token pages per softmax update: 1 or 2 (bf16),
                                1, 2 or 4 (fp8); 0 = the library's choice
                                (2 for bf16, 4 for fp8 pools) */
@@ -161,7 +165,8 @@ typedef struct bellman_attn_opts {
                                1 for fp8 pools) */
     void *event_begin;    /* optional hipEvent_t recorded on the stream right before
                              the main attention kernel (profiling); NULL = none */
-    void *event_end;      /* optional hipEvent_t recorded right after it */
+    void *event_end;      /* optional hipEvent_t recorded right after it (before the
+                             merge of the cut requests) */
 } bellman_attn_opts_t;
 
 /* bellman_decode_attention with explicit tuning options (NULL = defaults).
@@ -217,9 +222,10 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *                table: flag 2) are not written; a q_start that decreases, starts below
  *                0 or ends past T writes no row at all (flag 2).
  * Each workgroup takes 128 query rows of one request and one query head;
- * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo.  Scratch:
- * B + 1 integers of the per-device workspace.  Like bellman_kv_write, once
- * the workspace has grown to the call's size the call enqueues only kernels
+ * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo (P
+ * rounded to bf16 once would spend the bf16 error budget).  Scratch: B + 1
+ * integers of the per-device workspace.  Like bellman_kv_write, once the
+ * workspace has grown to the call's size the call enqueues only kernels
  * (graph-capturable). */
 int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                               const bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
@@ -227,8 +233,6 @@ int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t 
                               float scale, bellman_tensor_t *out, void *stream);
 
 typedef struct bellman_prefill_opts {
-    int32_t split_p;      /* 1 (default): P as bf16 hi + lo; 0: P rounded to bf16 once */
-    int32_t reserved;     /* 0 */
     void *event_begin;    /* optional hipEvent_t recorded before the attention kernels */
     void *event_end;      /* optional hipEvent_t recorded after them */
 } bellman_prefill_opts_t;
@@ -520,7 +524,8 @@ int bellman_sim_run(const bellman_sim_config_t *cfg, int64_t n, const int64_t *a
 const char *bellman_last_error(void);
 
 /* Make sure the current device's workspace holds at least `bytes`
- * (hipMalloc outside any timed region). */
+ * (hipMalloc outside any timed region or graph capture; a smaller block it
+ * replaces stays allocated until bellman_shutdown). */
 int bellman_reserve_workspace(int64_t bytes);
 
 /* Synchronise `stream`, copy the current device's error word to *flags and
@@ -530,7 +535,9 @@ int bellman_reserve_workspace(int64_t bytes);
  * outside the pool (page skipped). */
 int bellman_device_errors(void *stream, int32_t *flags);
 
-/* Free every device's workspace.  No call may be in flight. */
+/* Synchronise every device that holds a workspace and free its blocks
+ * (current and retired).  No call may be in flight, and graphs captured
+ * with library calls must not be replayed afterwards. */
 void bellman_shutdown(void);
 
 /* Library version as "major.minor.patch". */

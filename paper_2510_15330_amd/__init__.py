@@ -9,9 +9,6 @@ library is not built.
 from ._binding import (  # noqa: F401
     BellmanError,
     Controller,
-    IMPL_AUTO,
-    IMPL_MFMA,
-    IMPL_VALU,
     calibrate_thresholds,
     decode_attention,
     device_errors,

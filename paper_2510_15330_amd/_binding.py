@@ -11,7 +11,6 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libbellman.so")
 
 BF16, FP8_E4M3FN, INT32, FP32 = 1, 2, 3, 4
-IMPL_AUTO, IMPL_MFMA, IMPL_VALU = 0, 1, 2
 MAX_DIMS = 5
 
 
@@ -33,14 +32,13 @@ class Tensor(ctypes.Structure):
 
 
 class AttnOpts(ctypes.Structure):
-    _fields_ = [("max_waves", ctypes.c_int32), ("impl", ctypes.c_int32),
+    _fields_ = [("max_waves", ctypes.c_int32), ("xcd_skew", ctypes.c_int32),
                 ("pages_per_step", ctypes.c_int32), ("pipeline_depth", ctypes.c_int32),
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
 class PrefillOpts(ctypes.Structure):
-    _fields_ = [("split_p", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
+    _fields_ = [("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
 
 
 CTL_LINEAR, CTL_MPC, CTL_BBR, CTL_PCC = 1, 2, 3, 4
@@ -212,17 +210,18 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None
 
 
 def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
-                     k_scale=None, v_scale=None, max_waves=0, impl=IMPL_AUTO, events=None,
+                     k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, events=None,
                      pages_per_step=0, pipeline_depth=0):
     """bellman_decode_attention(_opts): one decode step over the paged cache.
 
     ``events`` is an optional pair of recorded-once torch.cuda.Event objects
-    that the library records around its main attention kernel."""
+    that the library records around its main attention kernel; ``xcd_skew``
+    is 0 (the library's choice), -1 (equal shares) or 1..255."""
     _device_tensors(q, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale)
     lib = library()
     args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
             desc(seq_lens), ctypes.c_float(scale), desc(out))
-    if max_waves == 0 and impl == IMPL_AUTO and events is None and pages_per_step == 0 and pipeline_depth == 0:
+    if max_waves == 0 and xcd_skew == 0 and events is None and pages_per_step == 0 and pipeline_depth == 0:
         _check(lib.bellman_decode_attention(*args, _stream(stream)))
     else:
         ev0 = ev1 = None
@@ -230,7 +229,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
             ev0, ev1 = events[0].cuda_event, events[1].cuda_event
             if not ev0 or not ev1:
                 raise ValueError("record each event once before passing it")
-        opts = AttnOpts(int(max_waves), int(impl), int(pages_per_step), int(pipeline_depth), ev0, ev1)
+        opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 
@@ -243,14 +242,14 @@ def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, str
 
 
 def prefill_attention(q, k_pages, v_pages, block_table, seq_lens, q_start, scale, out, stream=None,
-                      split_p=True, events=None):
+                      events=None):
     """bellman_prefill_attention(_opts): causal attention of each request's
     new (last) tokens over its cached ones."""
     _device_tensors(q, k_pages, v_pages, block_table, seq_lens, q_start, out)
     lib = library()
     args = (desc(q), desc(k_pages), desc(v_pages), desc(block_table), desc(seq_lens), desc(q_start),
             ctypes.c_float(scale), desc(out))
-    if split_p and events is None:
+    if events is None:
         _check(lib.bellman_prefill_attention(*args, _stream(stream)))
         return
     ev0 = ev1 = None
@@ -258,7 +257,7 @@ def prefill_attention(q, k_pages, v_pages, block_table, seq_lens, q_start, scale
         ev0, ev1 = events[0].cuda_event, events[1].cuda_event
         if not ev0 or not ev1:
             raise ValueError("record each event once before passing it")
-    opts = PrefillOpts(int(bool(split_p)), 0, ev0, ev1)
+    opts = PrefillOpts(ev0, ev1)
     _check(lib.bellman_prefill_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 

@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libbellman.so")
-SOURCES = ["kernels.hip", "prefill.hip", "bellman_api.cpp", "controller.cpp", "serve_sim.cpp"]
+SOURCES = ["kernels.hip", "prefill.hip", "device_state.hip", "bellman_api.cpp", "controller.cpp", "serve_sim.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

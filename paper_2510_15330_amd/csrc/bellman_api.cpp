@@ -10,9 +10,11 @@
 #include <string.h>
 
 #include <mutex>
+#include <vector>
 
 #include "../../include/bellman.h"
 #include "internal.h"
+#include "work_split.h"
 
 using namespace bellman;
 
@@ -30,13 +32,17 @@ int fail(int code, const char* fmt, ...) {
 
 // ------------------------------------------------------------- workspace ---
 
-constexpr int kMaxDevices = 64;
 constexpr int kXcdSkew = 10;          // share weights 266 : 246, even : odd XCDs (measured best of 0-28)
 constexpr int kMaxAttnBatch = 8192;  // lengths every attention wave reads to find its share
 
+// The growable per-device workspace.  Growing it allocates a larger block
+// and keeps the old one alive until bellman_shutdown, so kernels already
+// enqueued and graphs captured earlier still write into valid memory; no
+// growth happens while the stream is being captured.
 struct Workspace {
     char* base = nullptr;
     size_t cap = 0;
+    std::vector<char*> retired;
 };
 
 std::mutex g_ws_mutex;
@@ -51,33 +57,29 @@ int current_device(int* dev) {
     return BELLMAN_OK;
 }
 
-// Grow the current device's workspace to at least `bytes`.  The header is
-// zeroed on (re)allocation.
-int ensure_workspace(int dev, size_t bytes, char** base) {
+// Grow the current device's workspace to at least `bytes` (its first
+// WorkspaceHeader bytes hold per-call values and need no initialisation).
+int ensure_workspace(int dev, size_t bytes, hipStream_t stream, char** base) {
     std::lock_guard<std::mutex> lock(g_ws_mutex);
     Workspace& w = g_ws[dev];
     if (bytes < sizeof(WorkspaceHeader)) bytes = sizeof(WorkspaceHeader);
     if (w.cap < bytes) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        hipError_t e = hipStreamIsCapturing(stream, &cs);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipStreamIsCapturing: %s", hipGetErrorString(e));
+        if (cs != hipStreamCaptureStatusNone)
+            return fail(BELLMAN_ERR_UNSUPPORTED,
+                        "the workspace would have to grow to %zu bytes during graph capture; make the same call, "
+                        "or bellman_reserve_workspace, before capturing", bytes);
         size_t want = bytes + bytes / 4;
         want = (want + 0xFFFFF) & ~(size_t)0xFFFFF;
-        if (w.base) {
-            hipError_t e = hipDeviceSynchronize();
-            if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipDeviceSynchronize: %s", hipGetErrorString(e));
-            (void)hipFree(w.base);
-            w.base = nullptr;
-            w.cap = 0;
-        }
         void* p = nullptr;
-        hipError_t e = hipMalloc(&p, want);
+        e = hipMalloc(&p, want);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             return fail(BELLMAN_ERR_OOM, "workspace hipMalloc(%zu): %s", want, hipGetErrorString(e));
         }
-        e = hipMemset(p, 0, sizeof(WorkspaceHeader));
-        if (e != hipSuccess) {
-            (void)hipFree(p);
-            return fail(BELLMAN_ERR_HIP, "workspace hipMemset: %s", hipGetErrorString(e));
-        }
+        if (w.base) w.retired.push_back(w.base);
         w.base = (char*)p;
         w.cap = want;
     }
@@ -231,6 +233,140 @@ int launch_status(const char* what) {
     return BELLMAN_OK;
 }
 
+// One decode-attention call.  `fixed` selects the device's fixed scratch
+// array (no allocation; calls whose workspace exceeds it are rejected)
+// instead of the growable library workspace.
+int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
+                     const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
+                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed) {
+    g_last_error[0] = 0;
+    int rc;
+    PoolShape ps;
+    if ((rc = check_pools(k_pages, v_pages, &ps, true))) return rc;
+    if ((rc = check_tensor(q, "q", 3))) return rc;
+    const int64_t B = q->shape[0];
+    const int64_t H_q = q->shape[1];
+    if ((rc = check_rows(q, "q", BELLMAN_BF16, B, H_q, ps.D, 16))) return rc;
+    if ((rc = check_rows(out, "out", BELLMAN_BF16, B, H_q, ps.D, 8))) return rc;
+    if ((rc = check_block_table(block_table, B))) return rc;
+    if ((rc = check_seq_lens(seq_lens, B))) return rc;
+    if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
+    if (H_q < 1 || H_q % ps.H_kv != 0)
+        return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
+    const int64_t G = H_q / ps.H_kv;
+    if (G > 16) return fail(BELLMAN_ERR_UNSUPPORTED, "GQA group %lld > 16", (long long)G);
+    if (B > kMaxAttnBatch) return fail(BELLMAN_ERR_UNSUPPORTED, "batch %lld > %d", (long long)B, kMaxAttnBatch);
+    const int64_t max_pages = block_table->shape[1];
+    if ((double)B * ps.H_kv * (double)max_pages >= 2147483647.0)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "batch x KV heads x block-table width must stay below 2^31 pages");
+    int max_waves = 0, pps = 0, depth = 0, skew_opt = 0;
+    if (opts) {
+        max_waves = opts->max_waves;
+        skew_opt = opts->xcd_skew;
+        pps = opts->pages_per_step;
+        depth = opts->pipeline_depth;
+        if (depth < 0 || depth > 2) return fail(BELLMAN_ERR_UNSUPPORTED, "pipeline_depth %d not in {0, 1, 2}", depth);
+        if (max_waves < 0) return fail(BELLMAN_ERR_INVALID_ARG, "max_waves %d < 0", max_waves);
+        if (pps != 0 && pps != 1 && pps != 2 && pps != 4)
+            return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step %d not in {0, 1, 2, 4}", pps);
+        if (skew_opt < -1 || skew_opt > kMaxSkew)
+            return fail(BELLMAN_ERR_INVALID_ARG, "xcd_skew %d not in [-1, %d]", skew_opt, kMaxSkew);
+    }
+    if (pps == 4 && !ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step 4 is built for fp8 pools only");
+    if (pps == 0) pps = ps.fp8 ? 4 : 2;
+    if (depth == 0) depth = ps.fp8 ? 1 : 2;  // measured: fp8 steps compute more per byte
+    if (B == 0) return BELLMAN_OK;
+
+    int dev;
+    if ((rc = current_device(&dev))) return rc;
+    if (g_cu_count[dev] == 0) {
+        int cu = 0;
+        hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
+        g_cu_count[dev] = cu;
+    }
+    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][pps][depth];
+    if (bpc == 0) {
+        bpc = attention_blocks_per_cu(pps, depth, ps.fp8, ps.D);
+        if (depth == 2) bpc = 1;  // one wavefront per SIMD
+    }
+    // Every resident wave takes an equal share of the flattened step stream.
+    int64_t waves = (int64_t)g_cu_count[dev] * bpc * (kAttnBlock / kWaveSize);
+    if (max_waves > 0 && waves > max_waves) waves = max_waves;
+    const int64_t grid = (waves + (kAttnBlock / kWaveSize) - 1) / (kAttnBlock / kWaveSize);
+
+    const int64_t segs = B * ps.H_kv;
+    const size_t off_binfo = sizeof(WorkspaceHeader);
+    const size_t off_ml = off_binfo + align256(sizeof(int4) * (size_t)B);
+    const size_t slots = (size_t)(segs + waves) * (size_t)G;
+    const size_t off_o = off_ml + align256(sizeof(float2) * slots);
+    const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
+    hipStream_t s = (hipStream_t)stream;
+    char* base;
+    if (fixed) {
+        if (total > kScratchBytes)
+            return fail(BELLMAN_ERR_UNSUPPORTED,
+                        "this call needs %zu bytes of scratch; the fixed scratch array holds %zu "
+                        "((B*H_kv + waves) * G partial slots of %zu bytes)",
+                        total, kScratchBytes, sizeof(float2) + sizeof(float) * (size_t)ps.D);
+        if ((rc = device_scratch(dev, &base))) return rc;
+    } else if ((rc = ensure_workspace(dev, total, s, &base))) {
+        return rc;
+    }
+    int32_t* err;
+    if ((rc = device_error_word(dev, &err))) return rc;
+
+    AttnArgs a;
+    a.q = (const uint16_t*)q->data;
+    a.q_sb = q->stride[0];
+    a.q_sh = q->stride[1];
+    a.k_pages = k_pages->data;
+    a.v_pages = v_pages->data;
+    a.k_scale = k_pages->dequant_scale;
+    a.v_scale = v_pages->dequant_scale;
+    a.block_table = (const int32_t*)block_table->data;
+    a.bt_stride = B > 1 ? block_table->stride[0] : max_pages;
+    a.seq_lens = (const int32_t*)seq_lens->data;
+    a.out = (uint16_t*)out->data;
+    a.o_sb = out->stride[0];
+    a.o_sh = out->stride[1];
+    a.num_pages = ps.num_pages;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    a.B = (int)B;
+    a.H_q = (int)H_q;
+    a.H_kv = ps.H_kv;
+    a.G = (int)G;
+    a.D = ps.D;
+    a.max_pages = (int)max_pages;
+    a.waves = (int)waves;
+    a.pp = pps;
+    // The default XCD weights were measured on a whole MI355X (256 CUs,
+    // workgroup i on XCD i mod 8) with one workgroup per CU; partitioned
+    // devices and two workgroups per CU (depth 1) keep equal shares.
+    if (skew_opt == 0) a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
+    else a.skew = skew_opt < 0 ? 0 : skew_opt;
+    a.err = err;
+    a.hdr = (WorkspaceHeader*)base;
+    a.b_info = (int4*)(base + off_binfo);
+    a.part_ml = (float2*)(base + off_ml);
+    a.part_o = (float*)(base + off_o);
+
+    hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
+    hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;
+    if (ev0) {
+        hipError_t e = hipEventRecord(ev0, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    launch_attention(a, pps, depth, ps.fp8, (int)grid, s);
+    if ((rc = launch_status("attention"))) return rc;
+    if (ev1) {
+        hipError_t e = hipEventRecord(ev1, s);
+        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    }
+    launch_merge(a, s);
+    return launch_status("merge");
+}
+
 }  // namespace
 
 namespace bellman {
@@ -257,7 +393,7 @@ int bellman_reserve_workspace(int64_t bytes) {
     int dev, rc;
     if ((rc = current_device(&dev))) return rc;
     char* base;
-    return ensure_workspace(dev, (size_t)bytes, &base);
+    return ensure_workspace(dev, (size_t)bytes, nullptr, &base);
 }
 
 void bellman_shutdown(void) {
@@ -265,13 +401,15 @@ void bellman_shutdown(void) {
     int cur = 0;
     (void)hipGetDevice(&cur);
     for (int d = 0; d < kMaxDevices; ++d) {
-        if (g_ws[d].base) {
-            (void)hipSetDevice(d);
-            (void)hipDeviceSynchronize();
-            (void)hipFree(g_ws[d].base);
-            g_ws[d].base = nullptr;
-            g_ws[d].cap = 0;
-        }
+        Workspace& w = g_ws[d];
+        if (!w.base && w.retired.empty()) continue;
+        (void)hipSetDevice(d);
+        (void)hipDeviceSynchronize();
+        for (char* p : w.retired) (void)hipFree(p);
+        w.retired.clear();
+        if (w.base) (void)hipFree(w.base);
+        w.base = nullptr;
+        w.cap = 0;
     }
     (void)hipSetDevice(cur);
 }
@@ -281,13 +419,13 @@ int bellman_device_errors(void* stream, int32_t* flags) {
     if (!flags) return fail(BELLMAN_ERR_INVALID_ARG, "flags: null pointer");
     int dev, rc;
     if ((rc = current_device(&dev))) return rc;
-    char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+    int32_t* err;
+    if ((rc = device_error_word(dev, &err))) return rc;
     hipStream_t s = (hipStream_t)stream;
     int32_t v = 0;
-    hipError_t e = hipMemcpyAsync(&v, base + offsetof(WorkspaceHeader, err_flags), sizeof v, hipMemcpyDeviceToHost, s);
+    hipError_t e = hipMemcpyAsync(&v, err, sizeof v, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e == hipSuccess) e = hipMemsetAsync(base + offsetof(WorkspaceHeader, err_flags), 0, sizeof v, s);
+    if (e == hipSuccess) e = hipMemsetAsync(err, 0, sizeof v, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "reading the device error word: %s", hipGetErrorString(e));
     *flags = v;
@@ -318,8 +456,8 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
 
     int dev;
     if ((rc = current_device(&dev))) return rc;
-    char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader), &base))) return rc;
+    int32_t* err;
+    if ((rc = device_error_word(dev, &err))) return rc;
 
     AppendArgs a;
     a.k_new = k_new->data;
@@ -333,7 +471,7 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     a.block_table = (const int32_t*)block_table->data;
     a.bt_stride = block_table->shape[0] > 1 ? block_table->stride[0] : block_table->shape[1];
     a.seq_lens = (int32_t*)seq_lens->data;
-    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.err = err;
     a.num_pages = ps.num_pages;
     a.k_scale = k_pages->dequant_scale;
     a.v_scale = v_pages->dequant_scale;
@@ -351,129 +489,14 @@ int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tenso
                                   const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
                                   const bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
                                   const bellman_attn_opts_t* opts, void* stream) {
-    g_last_error[0] = 0;
-    int rc;
-    PoolShape ps;
-    if ((rc = check_pools(k_pages, v_pages, &ps, true))) return rc;
-    if ((rc = check_tensor(q, "q", 3))) return rc;
-    const int64_t B = q->shape[0];
-    const int64_t H_q = q->shape[1];
-    if ((rc = check_rows(q, "q", BELLMAN_BF16, B, H_q, ps.D, 16))) return rc;
-    if ((rc = check_rows(out, "out", BELLMAN_BF16, B, H_q, ps.D, 8))) return rc;
-    if ((rc = check_block_table(block_table, B))) return rc;
-    if ((rc = check_seq_lens(seq_lens, B))) return rc;
-    if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
-    if (H_q < 1 || H_q % ps.H_kv != 0)
-        return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
-    const int64_t G = H_q / ps.H_kv;
-    if (G > 16) return fail(BELLMAN_ERR_UNSUPPORTED, "GQA group %lld > 16", (long long)G);
-    if (B > kMaxAttnBatch) return fail(BELLMAN_ERR_UNSUPPORTED, "batch %lld > %d", (long long)B, kMaxAttnBatch);
-    const int64_t max_pages = block_table->shape[1];
-    if ((double)B * ps.H_kv * (double)max_pages >= 2147483647.0)
-        return fail(BELLMAN_ERR_UNSUPPORTED, "batch x KV heads x block-table width must stay below 2^31 pages");
-    int max_waves = 0, impl = BELLMAN_IMPL_AUTO, pps = 0, depth = 0;
-    if (opts) {
-        max_waves = opts->max_waves;
-        impl = opts->impl;
-        pps = opts->pages_per_step;
-        depth = opts->pipeline_depth;
-        if (depth < 0 || depth > 2) return fail(BELLMAN_ERR_UNSUPPORTED, "pipeline_depth %d not in {0, 1, 2}", depth);
-        if (max_waves < 0) return fail(BELLMAN_ERR_INVALID_ARG, "max_waves %d < 0", max_waves);
-        if (pps != 0 && pps != 1 && pps != 2 && pps != 4)
-            return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step %d not in {0, 1, 2, 4}", pps);
-        if (impl != BELLMAN_IMPL_AUTO && impl != BELLMAN_IMPL_MFMA && impl != BELLMAN_IMPL_VALU)
-            return fail(BELLMAN_ERR_INVALID_ARG, "unknown impl %d", impl);
-    }
-    if (impl == BELLMAN_IMPL_VALU) return fail(BELLMAN_ERR_UNSUPPORTED, "VALU kernel not built");
-    impl = BELLMAN_IMPL_MFMA;
-    if (pps == 4 && !ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step 4 is built for fp8 pools only");
-    if (pps == 0) pps = ps.fp8 ? 4 : 2;
-    if (depth == 0) depth = ps.fp8 ? 1 : 2;  // measured: fp8 steps compute more per byte
-    if (B == 0) return BELLMAN_OK;
-
-    int dev;
-    if ((rc = current_device(&dev))) return rc;
-    if (g_cu_count[dev] == 0) {
-        int cu = 0;
-        hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
-        if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
-        g_cu_count[dev] = cu;
-    }
-    int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][pps][depth];
-    if (bpc == 0) {
-        bpc = attention_blocks_per_cu(pps, depth, ps.fp8, ps.D);
-        if (depth == 2) bpc = 1;  // one wavefront per SIMD
-    }
-    // Every resident wave takes an equal share of the flattened step stream.
-    int64_t waves = (int64_t)g_cu_count[dev] * bpc * (kAttnBlock / kWaveSize);
-    if (max_waves > 0 && waves > max_waves) waves = max_waves;
-    const int64_t grid = (waves + (kAttnBlock / kWaveSize) - 1) / (kAttnBlock / kWaveSize);
-
-    const int64_t segs = B * ps.H_kv;
-    const size_t off_binfo = sizeof(WorkspaceHeader);
-    const size_t off_ml = off_binfo + align256(sizeof(int4) * (size_t)B);
-    const size_t slots = (size_t)(segs + waves) * (size_t)G;
-    const size_t off_o = off_ml + align256(sizeof(float2) * slots);
-    const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
-    char* base;
-    if ((rc = ensure_workspace(dev, total, &base))) return rc;
-
-    AttnArgs a;
-    a.q = (const uint16_t*)q->data;
-    a.q_sb = q->stride[0];
-    a.q_sh = q->stride[1];
-    a.k_pages = k_pages->data;
-    a.v_pages = v_pages->data;
-    a.k_scale = k_pages->dequant_scale;
-    a.v_scale = v_pages->dequant_scale;
-    a.block_table = (const int32_t*)block_table->data;
-    a.bt_stride = B > 1 ? block_table->stride[0] : max_pages;
-    a.seq_lens = (const int32_t*)seq_lens->data;
-    a.out = (uint16_t*)out->data;
-    a.o_sb = out->stride[0];
-    a.o_sh = out->stride[1];
-    a.num_pages = ps.num_pages;
-    a.scale_log2 = scale * 1.4426950408889634f;
-    a.B = (int)B;
-    a.H_q = (int)H_q;
-    a.H_kv = ps.H_kv;
-    a.G = (int)G;
-    a.D = ps.D;
-    a.max_pages = (int)max_pages;
-    a.waves = (int)waves;
-    a.pp = pps;
-    // the XCD weights were measured on a whole MI355X (256 CUs, workgroup i on
-    // XCD i mod 8) with one workgroup per CU; partitioned devices and two
-    // workgroups per CU (depth 1) keep equal shares
-    a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
-    a.hdr = (WorkspaceHeader*)base;
-    a.b_info = (int4*)(base + off_binfo);
-    a.part_ml = (float2*)(base + off_ml);
-    a.part_o = (float*)(base + off_o);
-
-    hipStream_t s = (hipStream_t)stream;
-    hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
-    hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;
-    if (ev0) {
-        hipError_t e = hipEventRecord(ev0, s);
-        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-    }
-    launch_attention(a, pps, depth, ps.fp8, (int)grid, s);
-    if ((rc = launch_status("attention"))) return rc;
-    if (ev1) {
-        hipError_t e = hipEventRecord(ev1, s);
-        if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
-    }
-    launch_merge(a, s);
-    return launch_status("merge");
+    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, false);
 }
 
 int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
                              const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
                              bellman_tensor_t* out, void* stream) {
-    return bellman_decode_attention_opts(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream);
+    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream, false);
 }
-
 
 // ------------------------------------------------------------ prompt path --
 
@@ -514,7 +537,11 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     int dev;
     if ((rc = current_device(&dev))) return rc;
     char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), &base))) return rc;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), (hipStream_t)stream,
+                               &base)))
+        return rc;
+    int32_t* err;
+    if ((rc = device_error_word(dev, &err))) return rc;
     WriteArgs a;
     a.k_new = k_new->data;
     a.v_new = v_new->data;
@@ -528,7 +555,7 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     a.bt_stride = block_table->shape[0] > 1 ? block_table->stride[0] : block_table->shape[1];
     a.seq_lens = (int32_t*)seq_lens->data;
     a.q_start = (const int32_t*)q_start->data;
-    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.err = err;
     a.num_pages = ps.num_pages;
     a.B = (int)B;
     a.T = (int)T;
@@ -570,8 +597,11 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
 
     int dev;
     if ((rc = current_device(&dev))) return rc;
+    hipStream_t s = (hipStream_t)stream;
     char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), &base))) return rc;
+    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), s, &base))) return rc;
+    int32_t* err;
+    if ((rc = device_error_word(dev, &err))) return rc;
     PrefillArgs a;
     a.q = (const uint16_t*)q->data;
     a.q_st = q->stride[0];
@@ -597,14 +627,13 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     a.G = (int)(H_q / ps.H_kv);
     a.D = ps.D;
     a.max_pages = (int)block_table->shape[1];
-    a.err = &((WorkspaceHeader*)base)->err_flags;
+    a.err = err;
     a.tile_start = (int32_t*)(base + sizeof(WorkspaceHeader));
-    hipStream_t s = (hipStream_t)stream;
     if (opts && opts->event_begin) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_begin, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    launch_prefill(a, opts ? opts->split_p != 0 : true, s);
+    launch_prefill(a, s);
     if ((rc = launch_status("prefill_attention"))) return rc;
     if (opts && opts->event_end) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_end, s);

@@ -15,13 +15,19 @@ constexpr int kErrAppendSlot = 1;
 constexpr int kErrLength = 2;
 constexpr int kErrPage = 4;
 
-// Header of the per-device workspace; the variable-size regions follow it.
+constexpr int kMaxDevices = 64;
+
+// Header of a decode-attention workspace (the library's growable one, or the
+// fixed scratch array); the variable-size regions follow it.
 struct WorkspaceHeader {
-    int32_t err_flags;    // sticky error bits, cleared by the host
     int32_t total_units;  // flattened (request, KV head, step) units of the current call
-    int32_t pad[62];
+    int32_t pad[63];
 };
 static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte aligned");
+
+// Bytes of the fixed per-device scratch array of the no-allocation decode
+// entry point (device_state.hip).
+constexpr size_t kScratchBytes = (size_t)32 << 20;
 
 struct AppendArgs {
     const void* k_new;   // [B, H_kv, D]
@@ -59,6 +65,8 @@ struct AttnArgs {
     int waves;           // waves sharing the flattened step stream (the grid's waves)
     int pp;              // pages per step of the launched attention kernel
     int skew;            // share weights 256 + skew (even-XCD workgroups) / 256 - skew on long shares; 0..255
+                         // (work_split.h)
+    int32_t* err;        // the device's error word
     // workspace
     WorkspaceHeader* hdr;
     int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head),
@@ -112,7 +120,13 @@ void launch_merge(const AttnArgs& a, hipStream_t s);
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 // Prefill launchers (prefill.hip).
 void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
-void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s);
+void launch_prefill(const PrefillArgs& a, hipStream_t s);
+
+// Addresses of the current device's error word and fixed scratch array
+// (device_state.hip); dev must be the current device.  0 or a negative
+// bellman status.
+int device_error_word(int dev, int32_t** p);
+int device_scratch(int dev, char** p);
 
 // Record the calling thread's last-error text (bellman_last_error) and
 // return `code`; shared by the host-side parts of the library.

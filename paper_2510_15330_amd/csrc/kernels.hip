@@ -734,7 +734,7 @@ attn_mfma_kernel(AttnArgs a) {
     // head) and P for the merge kernel, and raises the length flag
     const bool lead = w == 0;
     if (lead) {
-        if (__any(bad_len) && lane == 0) atomicOr(&a.hdr->err_flags, kErrLength);
+        if (__any(bad_len) && lane == 0) atomicOr(a.err, kErrLength);
         if (lane == 0) a.hdr->total_units = P;
     }
     if (r0 >= r1 && !lead) return;
@@ -992,7 +992,7 @@ attn_mfma_kernel(AttnArgs a) {
         if constexpr (DEPTH >= 3) step(std::integral_constant<int, 3>{});
         if (!cur[0].live) break;
     }
-    if (bad_pages) atomicOr(&a.hdr->err_flags, kErrPage);
+    if (bad_pages) atomicOr(a.err, kErrPage);
 }
 
 // ----------------------------------------------------------------- merge ---

@@ -262,8 +262,10 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 // O^T += V^T P^T for the 16 keys of page u, whose V^T elements are one
 // 16-byte run of each dim-major V row.  Online softmax in base 2 with a lazy
 // max: O and l are rescaled only when some column's max grows by more than
-// 2^8, so P stays below 2^8.  P enters as bf16 (hi), and with SPLIT also as
-// the bf16 remainder (lo), carrying it to ~2^-17.
+// 2^8, so P stays below 2^8.  P enters as bf16 (hi) plus the bf16 remainder
+// (lo), carrying it to ~2^-17: P rounded to bf16 once would add up to 2^-9
+// of every weight on top of the output's own 2^-9 rounding, more than the
+// bf16 error budget allows.
 //
 // The loop is software-pipelined: step s masks and takes the max of S(s)
 // (computed one step earlier), then issues the MFMAs of S(s + 1)
@@ -271,11 +273,10 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
 constexpr float kLazyMax = 8.0f;
 constexpr int kPageWindow = 1024;   // block-table entries staged in LDS
 constexpr int kXcds = 8;            // accelerator complexes; workgroup i runs on XCD i % 8
-constexpr bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 // VALU instructions of the softmax placed between consecutive S MFMAs
 constexpr int kValuPerMfma = 7;
 
-template <int D, int NH, bool SPLIT>
+template <int D, int NH>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_attn_kernel(PrefillArgs a) {
     constexpr int KS = 32 * NH;         // keys per step
@@ -496,13 +497,10 @@ prefill_attn_kernel(PrefillArgs a) {
                                       __builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j + 1], sl, -m))};
                     const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
                     ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
-                    if constexpr (SPLIT) {   // the remainder is exact in fp32; rounded again
-                        psum += pq.x + pq.y;
-                        pl[hh][j / 2] = __builtin_bit_cast(
-                            uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
-                    } else {   // P as rounded: the normaliser sums what multiplies V
-                        psum = __builtin_amdgcn_fdot2_f32_bf16(hi2, kOnes, psum, false);
-                    }
+                    // the remainder is exact in fp32, then rounded again
+                    psum += pq.x + pq.y;
+                    pl[hh][j / 2] = __builtin_bit_cast(
+                        uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
                 }
             l += psum;
             // K reads run two MFMAs ahead of the S MFMAs, with the softmax
@@ -522,19 +520,17 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int u = 0; u < 2; ++u) {
                     const bf16x8 bh = __builtin_bit_cast(
                         bf16x8, u32x4{ph[hh][4 * u], ph[hh][4 * u + 1], ph[hh][4 * u + 2], ph[hh][4 * u + 3]});
-                    bf16x8 bl;
-                    if constexpr (SPLIT)
-                        bl = __builtin_bit_cast(
-                            bf16x8, u32x4{pl[hh][4 * u], pl[hh][4 * u + 1], pl[hh][4 * u + 2], pl[hh][4 * u + 3]});
+                    const bf16x8 bl = __builtin_bit_cast(
+                        bf16x8, u32x4{pl[hh][4 * u], pl[hh][4 * u + 1], pl[hh][4 * u + 2], pl[hh][4 * u + 3]});
 #pragma unroll
                     for (int t = 0; t < D / 32; ++t) {
                         const bf16x8 va = *(const bf16x8*)(Vt + hh * 2 * PE + (u * D + 32 * t) * kPage);
                         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
-                        if constexpr (SPLIT) o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
                     }
                 }
             // V reads run four MFMAs ahead of the PV MFMAs
-            constexpr int MF = SPLIT ? 2 : 1;
+            constexpr int MF = 2;
             constexpr int NV = 2 * NH * (D / 32);
             __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
@@ -593,18 +589,15 @@ void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s) {
 }
 
 constexpr int kHalves = 2;   // 32-key halves per step: 64 keys, four pages
-void launch_prefill(const PrefillArgs& a, bool split_p, hipStream_t s) {
+void launch_prefill(const PrefillArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a);
     // an upper bound on tiles x query heads, rounded up to whole XCD rows
     const int64_t items = ((int64_t)(a.T + kPrefillRows - 1) / kPrefillRows + a.B) * a.H_q;
     const dim3 grid((unsigned)((items + kXcds - 1) / kXcds * kXcds));
-    if (a.D == 128) {
-        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, true>), grid, dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, false>), grid, dim3(256), 0, s, a);
-    } else {
-        if (split_p) hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, true>), grid, dim3(256), 0, s, a);
-        else hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, false>), grid, dim3(256), 0, s, a);
-    }
+    if (a.D == 128)
+        hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves>), grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves>), grid, dim3(256), 0, s, a);
 }
 
 }  // namespace bellman

@@ -208,10 +208,11 @@ def test_option_ranges(B):
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
     assert rc == ERR_INVALID and "max_waves" in B.last_error()
-    opts = B.AttnOpts(0, 7, 0, 0)
-    rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
-                                           ctypes.byref(opts), None)
-    assert rc == ERR_INVALID and "impl" in B.last_error()
+    for bad_skew in (-2, 256):
+        opts = B.AttnOpts(0, bad_skew, 0, 0)
+        rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
+                                               ctypes.byref(opts), None)
+        assert rc == ERR_INVALID and "xcd_skew" in B.last_error()
     for bad_pps in (3, 4):   # 4 is built for fp8 pools only; these are bf16
         opts = B.AttnOpts(0, 0, bad_pps, 0)
         rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],

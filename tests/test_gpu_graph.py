@@ -124,3 +124,48 @@ def test_prompt_step_graph_matches_eager():
         assert torch.equal(_bits(out_g), _bits(out_e)), f"prompt replay {i}: attention output"
         assert torch.equal(_bits(A.k_pages), _bits(B.k_pages)) and torch.equal(_bits(A.v_pages), _bits(B.v_pages))
     assert bl.device_errors() == 0
+
+
+def test_graph_survives_workspace_growth():
+    """A graph captured while the workspace was small still replays correctly
+    after a later call has grown the workspace (the old block is kept until
+    bellman_shutdown), and a call that would have to grow the workspace during
+    a capture is refused instead of allocating there."""
+    bl.shutdown()                                  # start from no workspace at all
+    A = wl.build("tiny", seed=12, device="cuda", steps=4)
+    B = wl.build("tiny", seed=12, device="cuda", steps=4)
+    out_g = torch.empty((A.B, A.H_q, A.D), dtype=torch.bfloat16, device="cuda")
+    out_e = torch.empty_like(out_g)
+    kn, vn, q = A.k_new[0].clone(), A.v_new[0].clone(), A.q[0].clone()
+    bl.decode_attention(q, A.k_pages, A.v_pages, A.block_table, A.seq_lens, A.scale, out_g)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        bl.kv_append(kn, vn, A.k_pages, A.v_pages, A.block_table, A.seq_lens)
+        bl.decode_attention(q, A.k_pages, A.v_pages, A.block_table, A.seq_lens, A.scale, out_g)
+    torch.cuda.synchronize()
+    bl.reserve_workspace(256 << 20)                # grows: the captured block is retired, not freed
+    for i in range(4):
+        kn.copy_(A.k_new[i])
+        vn.copy_(A.v_new[i])
+        q.copy_(A.q[i])
+        g.replay()
+        torch.cuda.synchronize()
+        bl.kv_append(B.k_new[i], B.v_new[i], B.k_pages, B.v_pages, B.block_table, B.seq_lens)
+        bl.decode_attention(B.q[i], B.k_pages, B.v_pages, B.block_table, B.seq_lens, B.scale, out_e)
+        torch.cuda.synchronize()
+        assert torch.equal(A.seq_lens, B.seq_lens), f"replay {i}: lengths"
+        assert torch.equal(_bits(out_g), _bits(out_e)), f"replay {i}: attention output"
+    assert bl.device_errors() == 0
+    del g
+    torch.cuda.synchronize()
+
+    bl.shutdown()                                  # no workspace: the next attention must grow it
+    g2 = torch.cuda.CUDAGraph()
+    with pytest.raises(bl.BellmanError) as ei:
+        with torch.cuda.graph(g2):
+            out_g.zero_()
+            bl.decode_attention(q, A.k_pages, A.v_pages, A.block_table, A.seq_lens, A.scale, out_g)
+    assert ei.value.code == -2 and "graph capture" in str(ei.value)
+    del g2
+    torch.cuda.synchronize()

@@ -2,8 +2,8 @@
 byte (pools, lengths, untouched poison), and causal prompt attention element
 by element within the bf16 tolerance, on batches that span several 128-row
 tiles with ragged tails, chunks after a cached prefix, every GQA group size
-the models use, both P precisions, strided rows, empty and malformed
-requests; at the 6-12k-token prompt sizes on sampled rows."""
+the models use, strided rows, empty and malformed requests; at the
+6-12k-token prompt sizes on sampled rows."""
 from __future__ import annotations
 
 import numpy as np
@@ -110,19 +110,17 @@ ATTN_CASES = [
 ]
 
 
-@pytest.mark.parametrize("split", [True, False], ids=["p_hi_lo", "p_bf16"])
 @pytest.mark.parametrize("case", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
-def test_prefill_matches_oracle(case, split):
+def test_prefill_matches_oracle(case):
     name, cached, new, H_q, H_kv, D = case
     w = wl.build_prefill(cached=cached, new=new, H_q=H_q, H_kv=H_kv, D=D, seed=len(name), device="cuda")
     _write(w)
     out = torch.full((w.T, H_q, D), float("nan"), dtype=torch.bfloat16, device="cuda")
-    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
-                         split_p=split)
+    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
     assert bl.device_errors() == 0
     kp, vp = _host_pools(w)
     ref = _oracle_prefill(w, kp, vp)
-    assert_close(_out_f64(out), ref, "bf16" if split else "bf16_p1", f"{name} split={split}")
+    assert_close(_out_f64(out), ref, "bf16", name)
 
 
 def _sweep_counts(rng, B, edge):
@@ -149,7 +147,6 @@ def test_prefill_random_sweep(seed):
     B = int(rng.integers(1, 7))
     cached = _sweep_counts(rng, B, 16)
     new = _sweep_counts(rng, B, int(rng.choice([16, 64, 128])))
-    split = bool(seed % 3)
     w = wl.build_prefill(cached=cached, new=new, H_q=G * H_kv, H_kv=H_kv, D=D, seed=7000 + seed, device="cuda")
     kp0, vp0 = _host_pools(w)
     sl0 = w.seq_lens.cpu().numpy().astype(np.int32)
@@ -158,15 +155,14 @@ def test_prefill_random_sweep(seed):
     kp, vp = _host_pools(w)
     kx, vx, sx = kp0.copy(), vp0.copy(), sl0.copy()
     oracle.kv_write(bits16(w.k_new), bits16(w.v_new), kx, vx, w.block_table.cpu().numpy(), sx, w.q_start.cpu().numpy())
-    what = f"seed={seed} G={G} H_kv={H_kv} D={D} cached={cached} new={new} split={split}"
+    what = f"seed={seed} G={G} H_kv={H_kv} D={D} cached={cached} new={new}"
     assert np.array_equal(kp, kx) and np.array_equal(vp, vx), what
     if w.T == 0:
         return
     out = torch.full((w.T, G * H_kv, D), float("nan"), dtype=torch.bfloat16, device="cuda")
-    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
-                         split_p=split)
+    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
     assert bl.device_errors() == 0
-    assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16" if split else "bf16_p1", what)
+    assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16", what)
 
 
 def test_prefill_many_requests():
