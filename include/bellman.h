@@ -178,6 +178,35 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
                                   bellman_tensor_t *out, const bellman_attn_opts_t *opts,
                                   void *stream);
 
+/* Bytes of the fixed per-device scratch array of
+ * bellman_decode_attention_noalloc. */
+#define BELLMAN_FIXED_SCRATCH_BYTES (32 << 20)
+
+/*
+ * bellman_decode_attention_opts for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, kernels and results as
+ * bellman_decode_attention_opts (NULL opts = defaults); the call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine).  The
+ * scratch of the cut requests lives in a fixed array of
+ * BELLMAN_FIXED_SCRATCH_BYTES that the library's code object holds on every
+ * GPU it runs on until the process ends, instead of the growable workspace.
+ * A call needs 256 + 16 B + slots (8 + 4 D) bytes of it (256-byte aligned
+ * regions), slots = (B * H_kv + W) * G with W the waves the call uses (1024
+ * for bf16 pools and 2048 for fp8 pools on a whole MI355X, or max_waves); a
+ * call that needs more is rejected with BELLMAN_ERR_UNSUPPORTED before
+ * anything is enqueued.  Every call on one GPU shares that GPU's array, and
+ * the array keeps the last call's contents (nothing in it has to start at
+ * zero): calls that overlap in time on one device, on any streams, race and
+ * give wrong results.
+ */
+int bellman_decode_attention_noalloc(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
+                                     const bellman_tensor_t *v_pages,
+                                     const bellman_tensor_t *block_table,
+                                     const bellman_tensor_t *seq_lens, float scale,
+                                     bellman_tensor_t *out, const bellman_attn_opts_t *opts,
+                                     void *stream);
+
 /* ----------------------------------------------------------- prompt path --
  * Before a request decodes, its prompt is prefilled (the step that sets the
  * time to first token, Sec. 3 "Our key proposal"; Sec. 4 "Setup and trace"):

@@ -11,6 +11,7 @@ from ._binding import (  # noqa: F401
     Controller,
     calibrate_thresholds,
     decode_attention,
+    decode_attention_noalloc,
     device_errors,
     kv_append,
     kv_write,

@@ -101,6 +101,9 @@ def library():
     lib.bellman_decode_attention_opts.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                   ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_opts.restype = ctypes.c_int
+    lib.bellman_decode_attention_noalloc.argtypes = [T, T, T, T, T, ctypes.c_float, T,
+                                                     ctypes.POINTER(AttnOpts), P]
+    lib.bellman_decode_attention_noalloc.restype = ctypes.c_int
     lib.bellman_kv_write.argtypes = [T, T, T, T, T, T, T, P]
     lib.bellman_kv_write.restype = ctypes.c_int
     lib.bellman_prefill_attention.argtypes = [T, T, T, T, T, T, ctypes.c_float, T, P]
@@ -231,6 +234,18 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
                 raise ValueError("record each event once before passing it")
         opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
+
+
+def decode_attention_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
+                             k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, pages_per_step=0,
+                             pipeline_depth=0):
+    """bellman_decode_attention_noalloc: decode_attention with its scratch in
+    the device's fixed array (no device allocation)."""
+    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale)
+    opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), None, None)
+    _check(library().bellman_decode_attention_noalloc(
+        desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table), desc(seq_lens),
+        ctypes.c_float(scale), desc(out), ctypes.byref(opts), _stream(stream)))
 
 
 def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, stream=None):

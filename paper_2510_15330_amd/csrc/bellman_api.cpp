@@ -498,6 +498,13 @@ int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* 
     return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream, false);
 }
 
+int bellman_decode_attention_noalloc(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
+                                     const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                                     const bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
+                                     const bellman_attn_opts_t* opts, void* stream) {
+    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, true);
+}
+
 // ------------------------------------------------------------ prompt path --
 
 namespace {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/bellman.h"
+
 namespace bellman {
 
 constexpr int kPage = 16;           // tokens per KV page
@@ -27,7 +29,7 @@ static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte
 
 // Bytes of the fixed per-device scratch array of the no-allocation decode
 // entry point (device_state.hip).
-constexpr size_t kScratchBytes = (size_t)32 << 20;
+constexpr size_t kScratchBytes = (size_t)BELLMAN_FIXED_SCRATCH_BYTES;
 
 struct AppendArgs {
     const void* k_new;   // [B, H_kv, D]
