@@ -188,17 +188,19 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
  * forbid hipMalloc.  Same arguments, kernels and results as
  * bellman_decode_attention_opts (NULL opts = defaults); the call allocates
  * nothing (no hipMalloc, hipFree or allocating library routine).  The
- * scratch of the cut requests lives in a fixed array of
- * BELLMAN_FIXED_SCRATCH_BYTES that the library's code object holds on every
- * GPU it runs on until the process ends, instead of the growable workspace.
- * A call needs 256 + 16 B + slots (8 + 4 D) bytes of it (256-byte aligned
- * regions), slots = (B * H_kv + W) * G with W the waves the call uses (1024
- * for bf16 pools and 2048 for fp8 pools on a whole MI355X, or max_waves); a
- * call that needs more is rejected with BELLMAN_ERR_UNSUPPORTED before
- * anything is enqueued.  Every call on one GPU shares that GPU's array, and
- * the array keeps the last call's contents (nothing in it has to start at
- * zero): calls that overlap in time on one device, on any streams, race and
- * give wrong results.
+ * scratch lives in a fixed array of BELLMAN_FIXED_SCRATCH_BYTES that the
+ * library's code object holds on every GPU it runs on until the process
+ * ends, instead of the growable workspace.  A call needs
+ *     256 + 16 W + 8 S + 4 D S   bytes (regions rounded up to 256 B),
+ *     S = 2 W G partial slots,
+ * W the waves it uses (1024 for bf16 and 2048 for fp8 pools on a whole
+ * MI355X, or max_waves if smaller): up to G = 16 at D = 128 for bf16 pools
+ * and G = 8 for fp8 pools by default; fp8 pools with G = 16 need
+ * max_waves <= 1900.  A call that needs more is rejected with
+ * BELLMAN_ERR_UNSUPPORTED before anything is enqueued.  Every call on one
+ * GPU shares that GPU's array and leaves its contents behind (nothing in it
+ * has to start at any value); calls that overlap in time on one device, on
+ * any streams, race and give wrong results.
  */
 int bellman_decode_attention_noalloc(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                                      const bellman_tensor_t *v_pages,

@@ -7,6 +7,7 @@ that ABI and nothing more.  There is no fallback: every call raises if the
 library is not built.
 """
 from ._binding import (  # noqa: F401
+    FIXED_SCRATCH_BYTES,
     BellmanError,
     Controller,
     calibrate_thresholds,

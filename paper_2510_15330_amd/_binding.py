@@ -12,6 +12,7 @@ _LIB_PATH = os.path.join(_HERE, "libbellman.so")
 
 BF16, FP8_E4M3FN, INT32, FP32 = 1, 2, 3, 4
 MAX_DIMS = 5
+FIXED_SCRATCH_BYTES = 32 << 20     # BELLMAN_FIXED_SCRATCH_BYTES
 
 
 class BellmanError(RuntimeError):

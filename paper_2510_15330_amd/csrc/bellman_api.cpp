@@ -57,12 +57,12 @@ int current_device(int* dev) {
     return BELLMAN_OK;
 }
 
-// Grow the current device's workspace to at least `bytes` (its first
-// WorkspaceHeader bytes hold per-call values and need no initialisation).
+// Grow the current device's workspace to at least `bytes` (no region of it
+// needs initialising).
 int ensure_workspace(int dev, size_t bytes, hipStream_t stream, char** base) {
     std::lock_guard<std::mutex> lock(g_ws_mutex);
     Workspace& w = g_ws[dev];
-    if (bytes < sizeof(WorkspaceHeader)) bytes = sizeof(WorkspaceHeader);
+    if (bytes < kWsHeader) bytes = kWsHeader;
     if (w.cap < bytes) {
         hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
         hipError_t e = hipStreamIsCapturing(stream, &cs);
@@ -295,10 +295,12 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     if (max_waves > 0 && waves > max_waves) waves = max_waves;
     const int64_t grid = (waves + (kAttnBlock / kWaveSize) - 1) / (kAttnBlock / kWaveSize);
 
-    const int64_t segs = B * ps.H_kv;
-    const size_t off_binfo = sizeof(WorkspaceHeader);
-    const size_t off_ml = off_binfo + align256(sizeof(int4) * (size_t)B);
-    const size_t slots = (size_t)(segs + waves) * (size_t)G;
+    if (waves > kMaxWaves) return fail(BELLMAN_ERR_UNSUPPORTED, "%lld waves > %d", (long long)waves, kMaxWaves);
+    // two partial slots per wave and query head: a wave's range cuts at most
+    // the request it starts in and the one it ends in
+    const size_t off_cuts = kWsHeader;
+    const size_t off_ml = off_cuts + align256(sizeof(int4) * (size_t)waves);
+    const size_t slots = 2 * (size_t)waves * (size_t)G;
     const size_t off_o = off_ml + align256(sizeof(float2) * slots);
     const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
     hipStream_t s = (hipStream_t)stream;
@@ -307,7 +309,7 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         if (total > kScratchBytes)
             return fail(BELLMAN_ERR_UNSUPPORTED,
                         "this call needs %zu bytes of scratch; the fixed scratch array holds %zu "
-                        "((B*H_kv + waves) * G partial slots of %zu bytes)",
+                        "(2 * waves * G partial slots of %zu bytes)",
                         total, kScratchBytes, sizeof(float2) + sizeof(float) * (size_t)ps.D);
         if ((rc = device_scratch(dev, &base))) return rc;
     } else if ((rc = ensure_workspace(dev, total, s, &base))) {
@@ -346,8 +348,7 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     if (skew_opt == 0) a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
     else a.skew = skew_opt < 0 ? 0 : skew_opt;
     a.err = err;
-    a.hdr = (WorkspaceHeader*)base;
-    a.b_info = (int4*)(base + off_binfo);
+    a.cuts = (int4*)(base + off_cuts);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
 
@@ -544,8 +545,7 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     int dev;
     if ((rc = current_device(&dev))) return rc;
     char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), (hipStream_t)stream,
-                               &base)))
+    if ((rc = ensure_workspace(dev, kWsHeader + align256((size_t)(B + 1) * 4), (hipStream_t)stream, &base)))
         return rc;
     int32_t* err;
     if ((rc = device_error_word(dev, &err))) return rc;
@@ -570,7 +570,7 @@ int bellman_kv_write(const bellman_tensor_t* k_new, const bellman_tensor_t* v_ne
     a.D = ps.D;
     a.max_pages = (int)block_table->shape[1];
     a.elem_bytes = (int)eb;
-    launch_kv_write(a, (int32_t*)(base + sizeof(WorkspaceHeader)), (hipStream_t)stream);
+    launch_kv_write(a, (int32_t*)(base + kWsHeader), (hipStream_t)stream);
     return launch_status("kv_write");
 }
 
@@ -606,7 +606,7 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     if ((rc = current_device(&dev))) return rc;
     hipStream_t s = (hipStream_t)stream;
     char* base;
-    if ((rc = ensure_workspace(dev, sizeof(WorkspaceHeader) + align256((size_t)(B + 1) * 4), s, &base))) return rc;
+    if ((rc = ensure_workspace(dev, kWsHeader + align256((size_t)(B + 1) * 4), s, &base))) return rc;
     int32_t* err;
     if ((rc = device_error_word(dev, &err))) return rc;
     PrefillArgs a;
@@ -635,7 +635,7 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     a.D = ps.D;
     a.max_pages = (int)block_table->shape[1];
     a.err = err;
-    a.tile_start = (int32_t*)(base + sizeof(WorkspaceHeader));
+    a.tile_start = (int32_t*)(base + kWsHeader);
     if (opts && opts->event_begin) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_begin, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));

@@ -19,13 +19,11 @@ constexpr int kErrPage = 4;
 
 constexpr int kMaxDevices = 64;
 
-// Header of a decode-attention workspace (the library's growable one, or the
-// fixed scratch array); the variable-size regions follow it.
-struct WorkspaceHeader {
-    int32_t total_units;  // flattened (request, KV head, step) units of the current call
-    int32_t pad[63];
-};
-static_assert(sizeof(WorkspaceHeader) == 256, "header keeps the regions 256-byte aligned");
+// A workspace (the library's growable one, or the fixed scratch array)
+// starts with a 256-byte header; the per-call regions follow.  Nothing in it
+// has to start at any value.
+constexpr int kMaxWaves = 16384;
+constexpr size_t kWsHeader = 256;
 
 // Bytes of the fixed per-device scratch array of the no-allocation decode
 // entry point (device_state.hip).
@@ -70,11 +68,12 @@ struct AttnArgs {
                          // (work_split.h)
     int32_t* err;        // the device's error word
     // workspace
-    WorkspaceHeader* hdr;
-    int4* b_info;        // [B]: (first flattened unit of request b, pages, clamped length, steps per head),
-                         // written by the attention kernel for the merge kernel
-    float2* part_ml;     // [(B*H_kv + waves) * G]: (running max in log2 units, sum)
-    float* part_o;       // [(B*H_kv + waves) * G * D]
+    int4* cuts;          // [waves]: (request, KV head, last wave, units) of the (request, head) in
+                         // which wave w's range ends if it began inside the range and runs past
+                         // it, else request -1; written by the attention kernel for the merge
+    float2* part_ml;     // [2 * waves * G]: (running max in log2 units, sum) of each wave's two
+                         // partial pieces (the request cut at its range's start, and at its end)
+    float* part_o;       // [2 * waves * G * D]
 };
 
 // Prompt KV write (prefill.hip).
@@ -117,9 +116,9 @@ struct PrefillArgs {
 // hipGetLastError in the caller.
 void launch_kv_append(const AppendArgs& a, hipStream_t s);
 void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s);
-void launch_merge(const AttnArgs& a, hipStream_t s);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
+void launch_merge(const AttnArgs& a, hipStream_t s);
 // Prefill launchers (prefill.hip).
 void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
 void launch_prefill(const PrefillArgs& a, hipStream_t s);

@@ -620,6 +620,72 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
     }
 }
 
+// ----------------------------------------------------------------- merge ---
+// The pieces of one cut (request b, KV head g), covered by attention waves
+// wf .. wl:
+// wave wf's piece is its kind-1 slot (the request starts inside its range),
+// every later wave's its kind-0 slot; waves with no units left none.  Lane
+// (qg, n) combines head g G + n at dims 16 t + 4 qg .. + 3, online in wave
+// order, two pieces per round trip:
+//   M = max_i m_i,  l = sum_i 2^(m_i - M) l_i,  out = sum_i 2^(m_i - M) o_i / l
+template <int D>
+__device__ __forceinline__ void merge_pieces(const AttnArgs& a, int b, int g, int wf, int wl, int P, int skew, int qg,
+                                             int n) {
+    constexpr int NT = D / 16;
+    constexpr int kBatch = 2;
+    const int W = a.waves;
+    const int nh = min(n, a.G - 1);   // padding lanes repeat the last head and write nothing
+    float M = -INFINITY, l = 0.f;
+    f32x4 acc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int v0 = wf; v0 <= wl; v0 += kBatch) {
+        float2 ml[kBatch];
+        f32x4 o[kBatch][NT];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int v = min(v0 + j, wl);          // past wl: a re-read of wl's piece, weight 0 below
+            const int64_t slot = (int64_t)(2 * v + (v == wf ? 1 : 0)) * a.G + nh;
+            ml[j] = a.part_ml[slot];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
+        }
+        float Mb = M;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int v = v0 + j;
+            const bool live = v <= wl && share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew);
+            if (!live) ml[j] = make_float2(-INFINITY, 0.f);
+            Mb = fmaxf(Mb, ml[j].x);
+        }
+        if (Mb > M) {             // exact: otherwise the factor is 1
+            const float r = fast_exp2(M - Mb);
+            l *= r;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[t] *= r;
+            M = Mb;
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const bool live = ml[j].x != -INFINITY;
+            const float wt = live ? fast_exp2(ml[j].x - M) : 0.f;
+            l += live ? wt * ml[j].y : 0.f;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) acc[t] += live ? wt * o[j][t] : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    }
+    if (n >= a.G) return;
+    const float inv = 1.f / l;
+    uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)(g * a.G + n) * a.o_sh;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        u32x2 pk;
+        pk.x = (uint32_t)f32_to_bf16_rne(acc[t][0] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][1] * inv) << 16);
+        pk.y = (uint32_t)f32_to_bf16_rne(acc[t][2] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][3] * inv) << 16);
+        *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
+    }
+}
+
 // Mark loaded registers as read.  A step reads some of its loads only on some
 // paths (the query only at a segment change, the second page only when the
 // step has one); a register whose load was never waited for on the path taken
@@ -722,22 +788,42 @@ attn_mfma_kernel(AttnArgs a) {
         }
         return sum;
     };
+    // Requests of length 0 attend nothing and get rows of zeros: request b's
+    // rows are written by wave b mod W, all lanes together.
+    auto zero_empty = [&](int b0) {
+#pragma unroll
+        for (int k = 0; k < kPlanPerLane; ++k) {
+            const int b = b0 + kPlanPerLane * lane + k;
+            uint64_t m = __ballot(b < a.B && Lk[k] == 0 && b % a.waves == w);
+            while (m) {
+                const int src = __ffsll((unsigned long long)m) - 1;
+                m &= m - 1;
+                const int bz = b0 + kPlanPerLane * src + k;
+                // each head row is D bf16 = D / 4 8-byte units (rows are 8-byte aligned)
+                for (int u = lane; u < a.H_q * (D / 4); u += kWaveSize) {
+                    const int h = u / (D / 4), c = u - h * (D / 4);
+                    *(u32x2*)(a.out + (int64_t)bz * a.o_sb + (int64_t)h * a.o_sh + 4 * c) = u32x2{0u, 0u};
+                }
+            }
+        }
+    };
     int lsum = load_lens(0);
+    zero_empty(0);
     int incl = wave_incl_scan(lsum, lane);
     int P = __builtin_amdgcn_readlane(incl, kWaveSize - 1);
-    for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch)
+    for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch) {
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
+        zero_empty(b0);
+    }
     const int skew = share_skew(a.skew, P, a.waves);
     const int r0 = share_bound(w, P, a.waves, skew);
     const int r1 = share_bound(w + 1, P, a.waves, skew);
-    // wave 0 also writes each request's (first unit, pages, length, steps per
-    // head) and P for the merge kernel, and raises the length flag
-    const bool lead = w == 0;
-    if (lead) {
-        if (__any(bad_len) && lane == 0) atomicOr(a.err, kErrLength);
-        if (lane == 0) a.hdr->total_units = P;
+    // wave 0 raises the length flag
+    if (w == 0 && __any(bad_len) && lane == 0) atomicOr(a.err, kErrLength);
+    if (r0 >= r1) {
+        if (lane == 0) a.cuts[w] = make_int4(-1, 0, 0, 0);
+        return;
     }
-    if (r0 >= r1 && !lead) return;
     int sb = -1, sg = 0, sp = 0, sL = 0;   // request, KV head, page, length at unit r0
     int carry = 0;                         // units of the requests before this batch
     for (int b0 = 0; b0 < a.B; b0 += kPlanBatch) {
@@ -749,17 +835,8 @@ attn_mfma_kernel(AttnArgs a) {
             incl = wave_incl_scan(lsum, lane);
         }
         const int excl = carry + incl - lsum;
-        if (lead) {
-            int f = excl;
-#pragma unroll
-            for (int k = 0; k < kPlanPerLane; ++k) {
-                const int b = b0 + kPlanPerLane * lane + k;
-                if (b < a.B) a.b_info[b] = make_int4(f, (Lk[k] + kPage - 1) / kPage, Lk[k], uk[k] / a.H_kv);
-                f += uk[k];
-            }
-        }
         const uint64_t hit = __ballot(lsum > 0 && excl <= r0 && r0 < excl + lsum);
-        if (sb < 0 && hit != 0 && r0 < r1) {
+        if (sb < 0 && hit != 0) {
             // walk the 16 requests of the lane that holds unit r0
             const int src = __ffsll((unsigned long long)hit) - 1;
             int x = __builtin_amdgcn_readlane(excl, src);
@@ -778,9 +855,8 @@ attn_mfma_kernel(AttnArgs a) {
             }
         }
         carry += __builtin_amdgcn_readlane(incl, kWaveSize - 1);
-        if (sb >= 0 && !lead) break;
+        if (sb >= 0) break;
     }
-    if (r0 >= r1) return;
 
     const size_t tile_bytes = (size_t)D * kPage * EB;
     const size_t page_stride = (size_t)a.H_kv * tile_bytes;
@@ -789,12 +865,16 @@ attn_mfma_kernel(AttnArgs a) {
     // DEPTH + 2 cursors walk the wave's stream: cur[0] is computed,
     // cur[1..DEPTH] have their pages (and query rows) in flight, and
     // cur[DEPTH+1] has its block-table entries in flight.
+    sb = __builtin_amdgcn_readfirstlane(sb);
+    sg = __builtin_amdgcn_readfirstlane(sg);
+    sp = __builtin_amdgcn_readfirstlane(sp);
+    sL = __builtin_amdgcn_readfirstlane(sL);
     Cursor cur[DEPTH + 2];
     {
-        cur[0].b = __builtin_amdgcn_readfirstlane(sb);
-        cur[0].g = __builtin_amdgcn_readfirstlane(sg);
-        cur[0].p = __builtin_amdgcn_readfirstlane(sp);
-        cur[0].L = __builtin_amdgcn_readfirstlane(sL);
+        cur[0].b = sb;
+        cur[0].g = sg;
+        cur[0].p = sp;
+        cur[0].L = sL;
         cur[0].np = (cur[0].L + kPage - 1) / kPage;
         cur[0].x = r0;
         cur[0].live = true;
@@ -872,11 +952,15 @@ attn_mfma_kernel(AttnArgs a) {
     bool seg_bad = false;
 
     // Write the finished piece of C's (request, head): the whole output if the
-    // request's head lies entirely in this wave's range, else a partial.
+    // request's head lies entirely in this wave's range, else a partial in
+    // the wave's slot of its kind.  A range cuts at most two: the (request,
+    // head) it starts in, if that began before it (kind 0), and the one it
+    // ends in, if that began inside it and runs past its end (kind 1).
     auto finish = [&](const Cursor& c, float vs) {
         const float l_tot = group_sum4(st.l);
         const int seg_x0 = c.x - c.p / PP;
         const bool whole = seg_x0 >= r0 && seg_x0 + (c.np + PP - 1) / PP <= r1;
+        const int kind = seg_x0 < r0 ? 0 : 1;
         if (hv) {
             const int h = c.g * a.G + n;
             if (whole) {
@@ -890,7 +974,7 @@ attn_mfma_kernel(AttnArgs a) {
                     *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
                 }
             } else {
-                const int64_t slot = ((int64_t)c.b * a.H_kv + c.g + w) * a.G + n;
+                const int64_t slot = (int64_t)(2 * w + kind) * a.G + n;
                 float* po = a.part_o + slot * D;
                 const float f = seg_bad ? NAN : vs;
 #pragma unroll
@@ -993,87 +1077,31 @@ attn_mfma_kernel(AttnArgs a) {
         if (!cur[0].live) break;
     }
     if (bad_pages) atomicOr(a.err, kErrPage);
+    // The request this wave's range ends in, if it began inside the range and
+    // runs past it (its kind-1 piece; the dead cursors stopped at the last
+    // unit): the merge kernel's wave w combines it with the later waves'
+    // pieces.
+    const Cursor& e = cur[0];
+    const int ex0 = e.x - e.p / PP;
+    const int en = (e.np + PP - 1) / PP;
+    if (lane == 0) {
+        const bool cut = ex0 >= r0 && ex0 + en > r1;
+        a.cuts[w] = cut ? make_int4(e.b, e.g, wave_of(ex0 + en - 1, P, a.waves, skew), P) : make_int4(-1, 0, 0, 0);
+    }
 }
 
-// ----------------------------------------------------------------- merge ---
-// One wave per (request, query head) whose KV head was cut by a wave boundary:
-// combine the pieces of the waves that covered it, in wave order
-// (deterministic):
-//   M = max_i m_i,  l = sum_i 2^(m_i - M) l_i,  out = sum_i 2^(m_i - M) o_i / l
-// A request's head that one wave covered whole was written by that wave;
-// requests of length 0 get zeros.
+// One wave per attention wave w: if w's range ended inside a (request, head)
+// that began in it, combine that request's pieces (merge_pieces).
 template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
-    const int wid = blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6);
+    const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6));
+    if (w >= a.waves) return;
+    const int4 c = a.cuts[w];
+    if (c.x < 0) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
-    if (wid >= a.B * a.H_q) return;
-    const int b = wid / a.H_q, h = wid - b * a.H_q;
-    const int g = h / a.G, n = h - g * a.G;
-    const int4 bi = a.b_info[b];
-    const int np = bi.y;
-    uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
-    if (np == 0) {
-        for (int d = lane; d < D; d += kWaveSize) orow[d] = 0;
-        return;
-    }
-    const int P = a.hdr->total_units;
-    const int W = a.waves;
-    const int ns = bi.w;                 // steps per KV head
-    const int x0 = bi.x + g * ns;
-    const int skew = share_skew(a.skew, P, W);
-    const int wf = wave_of(x0, P, W, skew);
-    const int wl = wave_of(x0 + ns - 1, P, W, skew);
-    if (wf == wl) return;
-    const int64_t seg = (int64_t)b * a.H_kv + g;
-    auto has_units = [&](int v) {
-        return share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew);
-    };
-    // Online merge over batches of kBatch pieces: every load of a batch is
-    // issued before any is used (indices past wl are clamped to wl, so every
-    // read is of a written slot range), and a piece of a wave that has no
-    // units gets weight 0 after the load.  Wave wf holds unit x0, so the
-    // first batch sets a finite M.
-    constexpr int kBatch = 4;
-    float M = -INFINITY, l = 0.f;
-    float acc[D / kWaveSize];
-#pragma unroll
-    for (int k = 0; k < D / kWaveSize; ++k) acc[k] = 0.f;
-    for (int v0 = wf; v0 <= wl; v0 += kBatch) {
-        float2 ml[kBatch];
-        float o[kBatch][D / kWaveSize];
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const int64_t slot = (seg + min(v0 + j, wl)) * a.G + n;
-            ml[j] = a.part_ml[slot];
-#pragma unroll
-            for (int k = 0; k < D / kWaveSize; ++k) o[j][k] = a.part_o[slot * D + lane + kWaveSize * k];
-        }
-        float Mb = M;
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const bool live = v0 + j <= wl && has_units(v0 + j);
-            if (!live) ml[j] = make_float2(-INFINITY, 0.f);
-            Mb = fmaxf(Mb, ml[j].x);
-        }
-        if (Mb > M) {             // exact: otherwise the factor is 1
-            const float r = fast_exp2(M - Mb);
-            l *= r;
-#pragma unroll
-            for (int k = 0; k < D / kWaveSize; ++k) acc[k] *= r;
-            M = Mb;
-        }
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const bool live = ml[j].x != -INFINITY;
-            const float wt = live ? fast_exp2(ml[j].x - M) : 0.f;
-            l += live ? wt * ml[j].y : 0.f;
-#pragma unroll
-            for (int k = 0; k < D / kWaveSize; ++k) acc[k] += live ? wt * o[j][k] : 0.f;
-        }
-    }
-    const float inv = 1.f / l;
-#pragma unroll
-    for (int k = 0; k < D / kWaveSize; ++k) orow[lane + kWaveSize * k] = f32_to_bf16_rne(acc[k] * inv);
+    const int P = __builtin_amdgcn_readfirstlane(c.w);
+    merge_pieces<D>(a, __builtin_amdgcn_readfirstlane(c.x), __builtin_amdgcn_readfirstlane(c.y), w,
+                    __builtin_amdgcn_readfirstlane(c.z), P, share_skew(a.skew, P, a.waves), lane >> 4, lane & 15);
 }
 
 }  // namespace
@@ -1139,9 +1167,7 @@ int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D) {
 }
 
 void launch_merge(const AttnArgs& a, hipStream_t s) {
-    const int pairs = a.B * a.H_q;
-    if (pairs == 0) return;
-    const dim3 g((pairs + 3) / 4), blk(256);
+    const dim3 g((a.waves + 3) / 4), blk(256);
     if (a.D == 128)
         hipLaunchKernelGGL(merge_kernel<128>, g, blk, 0, s, a);
     else

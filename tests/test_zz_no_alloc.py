@@ -81,14 +81,23 @@ def test_noalloc_matches_allocating_entry_point_twice():
 
 
 def test_noalloc_rejects_calls_beyond_the_array():
-    # 8192 requests x 16 KV heads x G 16: about a gigabyte of partial slots
-    B, H_kv, G_, D = 8192, 16, 16, 128
-    q = torch.zeros((B, H_kv * G_, D), dtype=torch.bfloat16, device="cuda")
-    k = torch.zeros((4, H_kv, D // 8, 16, 8), dtype=torch.bfloat16, device="cuda")
-    v = torch.zeros((4, H_kv, D, 16), dtype=torch.bfloat16, device="cuda")
-    bt = torch.zeros((B, 1), dtype=torch.int32, device="cuda")
-    sl = torch.ones((B,), dtype=torch.int32, device="cuda")
-    out = torch.empty_like(q)
+    # fp8 pools with 16 query heads per KV head at head_dim 128: two partial
+    # slots of 520 bytes per wave and head come to 34 MB over the 2048 waves
+    # of a whole MI355X, more than the 32 MiB array; capping the waves fits
+    rng = np.random.default_rng(778)
+    B, H_kv, G_, D = 3, 8, 16, 128
+    case = dn.random_case(rng, B, H_kv * G_, H_kv, D, [5000, 70, 1], "fp8")
+    case["k_scale"] = (rng.uniform(0.5, 1.5, size=(B, H_kv)) / 40.0).astype(np.float32)
+    case["v_scale"] = (rng.uniform(0.5, 1.5, size=(B, H_kv)) / 40.0).astype(np.float32)
+    d = _dev(case, "fp8")
+    scale = float(np.float32(1.0 / np.sqrt(D)))
+    waves = torch.cuda.get_device_properties(0).multi_processor_count * 8
+    need = 256 + 16 * waves + 2 * waves * G_ * 8 + 2 * waves * G_ * D * 4
+    if need <= bl.FIXED_SCRATCH_BYTES:
+        pytest.skip(f"{waves} waves fit the fixed array on this device")
     with pytest.raises(bl.BellmanError) as ei:
-        bl.decode_attention_noalloc(q, k, v, bt, sl, 0.1, out)
+        _run(bl.decode_attention_noalloc, d, scale)
     assert ei.value.code == -2 and "fixed scratch array" in str(ei.value)
+    got = _run(bl.decode_attention_noalloc, d, scale, max_waves=1900)
+    want = _run(bl.decode_attention, d, scale, max_waves=1900)
+    assert torch.equal(got.view(torch.int16), want.view(torch.int16))
