@@ -43,11 +43,25 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_sanitized(out: str) -> str:
+    """``oracle.c`` under AddressSanitizer and UndefinedBehaviorSanitizer, at
+    `out` (ROCm's clang, so that one sanitizer runtime serves it and the
+    library's host build)."""
+    clang = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "llvm", "bin", "clang")
+    subprocess.check_call(
+        [clang, "-O1", "-g", "-fopenmp", "-std=c99", "-Wall", "-shared", "-fPIC", "-fsanitize=address,undefined",
+         "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-shared-libsan", _SRC, "-o", out, "-lm"])
+    return out
+
+
 def load(path: str | None = None):
     """Load the oracle library, building it only if no build exists."""
     global _lib
     if path is not None:
         return _bind(ctypes.CDLL(path))
+    if _lib is None and os.environ.get("ORACLE_LIBRARY"):
+        # another build of oracle.c (the host sanitizer build)
+        _lib = _bind(ctypes.CDLL(os.environ["ORACLE_LIBRARY"]))
     if _lib is None:
         if not os.path.exists(_LIB):
             build(force=True)

@@ -8,7 +8,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "libbellman.so")
+# BELLMAN_LIBRARY selects another build of the same library (the host
+# sanitizer build of paper_2510_15330_amd/build.py --sanitize)
+_LIB_PATH = os.environ.get("BELLMAN_LIBRARY") or os.path.join(_HERE, "libbellman.so")
 
 BF16, FP8_E4M3FN, INT32, FP32 = 1, 2, 3, 4
 MAX_DIMS = 5
