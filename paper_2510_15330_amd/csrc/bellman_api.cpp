@@ -34,6 +34,7 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr int kXcdSkew = 10;          // share weights 266 : 246, even : odd XCDs (measured best of 0-28)
 constexpr int kMaxAttnBatch = 8192;  // lengths every attention wave reads to find its share
+constexpr double kShortSharePages = 512;   // below this many table pages a wave: one page per step
 
 // The growable per-device workspace.  Growing it allocates a larger block
 // and keeps the old one alive until bellman_shutdown, so kernels already
@@ -238,7 +239,8 @@ int launch_status(const char* what) {
 // instead of the growable library workspace.
 int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
                      const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
-                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed) {
+                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed,
+                     const bellman_tensor_t* k_new = nullptr, const bellman_tensor_t* v_new = nullptr) {
     g_last_error[0] = 0;
     int rc;
     PoolShape ps;
@@ -250,6 +252,16 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     if ((rc = check_rows(out, "out", BELLMAN_BF16, B, H_q, ps.D, 8))) return rc;
     if ((rc = check_block_table(block_table, B))) return rc;
     if ((rc = check_seq_lens(seq_lens, B))) return rc;
+    // a fused step: the new rows, in the pools' type or bf16 for fp8 pools
+    const bool fused = k_new != nullptr || v_new != nullptr;
+    bool quant = false;
+    if (fused) {
+        if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
+        quant = ps.fp8 && k_new->dtype == BELLMAN_BF16;
+        const int32_t row_dtype = quant ? (int32_t)BELLMAN_BF16 : k_pages->dtype;
+        if ((rc = check_rows(k_new, "k_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
+        if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
+    }
     if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
     if (H_q < 1 || H_q % ps.H_kv != 0)
         return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
@@ -273,7 +285,6 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
             return fail(BELLMAN_ERR_INVALID_ARG, "xcd_skew %d not in [-1, %d]", skew_opt, kMaxSkew);
     }
     if (pps == 4 && !ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step 4 is built for fp8 pools only");
-    if (pps == 0) pps = ps.fp8 ? 4 : 2;
     if (depth == 0) depth = ps.fp8 ? 1 : 2;  // measured: fp8 steps compute more per byte
     if (B == 0) return BELLMAN_OK;
 
@@ -284,6 +295,17 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
         if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
         g_cu_count[dev] = cu;
+    }
+    if (pps == 0) {
+        // bf16: two pages per step, or one when the block table leaves room
+        // for few pages per wave (short shares: the finer step shortens the
+        // ramp and the tail; measured 121 against 126 us on 64 requests of
+        // 1-4k tokens, while 256 requests of 6-13.5k tokens run faster with
+        // two).  Decided from the table's width, so no device read is needed.
+        int64_t w_est = (int64_t)g_cu_count[dev] * (kAttnBlock / kWaveSize) * (depth == 2 ? 1 : 2);
+        if (max_waves > 0 && w_est > max_waves) w_est = max_waves;
+        const double table_pages_per_wave = (double)B * ps.H_kv * (double)max_pages / (double)w_est;
+        pps = ps.fp8 ? 4 : (table_pages_per_wave < kShortSharePages ? 1 : 2);
     }
     int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][pps][depth];
     if (bpc == 0) {
@@ -302,7 +324,12 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     const size_t off_ml = off_cuts + align256(sizeof(int4) * (size_t)waves);
     const size_t slots = 2 * (size_t)waves * (size_t)G;
     const size_t off_o = off_ml + align256(sizeof(float2) * slots);
-    const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
+    // a fused step also keeps a piece of every (request, KV head)
+    const size_t seg_slots = fused ? (size_t)B * ps.H_kv * (size_t)G : 0;
+    const size_t off_rec = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
+    const size_t off_sml = off_rec + align256(sizeof(int4) * (size_t)B * (fused ? ps.H_kv : 0));
+    const size_t off_so = off_sml + align256(sizeof(float2) * seg_slots);
+    const size_t total = off_so + align256(sizeof(float) * seg_slots * (size_t)ps.D);
     hipStream_t s = (hipStream_t)stream;
     char* base;
     if (fixed) {
@@ -349,6 +376,18 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     else a.skew = skew_opt < 0 ? 0 : skew_opt;
     a.err = err;
     a.cuts = (int4*)(base + off_cuts);
+    a.fused = fused ? 1 : 0;
+    a.quant = quant ? 1 : 0;
+    a.k_new = fused ? k_new->data : nullptr;
+    a.v_new = fused ? v_new->data : nullptr;
+    a.new_sb = fused ? k_new->stride[0] : 0;
+    a.new_sh = fused ? k_new->stride[1] : 0;
+    a.vnew_sb = fused ? v_new->stride[0] : 0;
+    a.vnew_sh = fused ? v_new->stride[1] : 0;
+    a.seq_lens_w = (int32_t*)seq_lens->data;
+    a.seg_rec = (int4*)(base + off_rec);
+    a.seg_ml = (float2*)(base + off_sml);
+    a.seg_o = (float*)(base + off_so);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
 
@@ -364,7 +403,8 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         hipError_t e = hipEventRecord(ev1, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    launch_merge(a, s);
+    if (fused) launch_step_merge(a, ps.fp8, s);
+    else launch_merge(a, s);
     return launch_status("merge");
 }
 
@@ -497,6 +537,17 @@ int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* 
                              const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
                              bellman_tensor_t* out, void* stream) {
     return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream, false);
+}
+
+int bellman_decode_step(const bellman_tensor_t* q, const bellman_tensor_t* k_new, const bellman_tensor_t* v_new,
+                        bellman_tensor_t* k_pages, bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                        bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
+                        const bellman_attn_opts_t* opts, void* stream) {
+    if (!k_new || !v_new) {
+        g_last_error[0] = 0;
+        return fail(BELLMAN_ERR_INVALID_ARG, "%s: null descriptor", k_new ? "v_new" : "k_new");
+    }
+    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, false, k_new, v_new);
 }
 
 int bellman_decode_attention_noalloc(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,

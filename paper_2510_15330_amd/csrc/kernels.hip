@@ -621,41 +621,26 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
 }
 
 // ----------------------------------------------------------------- merge ---
-// The pieces of one cut (request b, KV head g), covered by attention waves
-// wf .. wl:
-// wave wf's piece is its kind-1 slot (the request starts inside its range),
-// every later wave's its kind-0 slot; waves with no units left none.  Lane
-// (qg, n) combines head g G + n at dims 16 t + 4 qg .. + 3, online in wave
-// order, two pieces per round trip:
+// Online merge of partial pieces (m_i, l_i, o_i) of one (request, head):
 //   M = max_i m_i,  l = sum_i 2^(m_i - M) l_i,  out = sum_i 2^(m_i - M) o_i / l
+// Lane (qg, n) holds head n at dims 16 t + 4 qg .. + 3.  Pieces come in
+// batches whose loads are all issued before any is used; a piece marked dead
+// gets weight 0.
 template <int D>
-__device__ __forceinline__ void merge_pieces(const AttnArgs& a, int b, int g, int wf, int wl, int P, int skew, int qg,
-                                             int n) {
-    constexpr int NT = D / 16;
-    constexpr int kBatch = 2;
-    const int W = a.waves;
-    const int nh = min(n, a.G - 1);   // padding lanes repeat the last head and write nothing
+struct MergeAcc {
+    static constexpr int NT = D / 16;
     float M = -INFINITY, l = 0.f;
     f32x4 acc[NT];
+    __device__ __forceinline__ MergeAcc() {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int v0 = wf; v0 <= wl; v0 += kBatch) {
-        float2 ml[kBatch];
-        f32x4 o[kBatch][NT];
-#pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const int v = min(v0 + j, wl);          // past wl: a re-read of wl's piece, weight 0 below
-            const int64_t slot = (int64_t)(2 * v + (v == wf ? 1 : 0)) * a.G + nh;
-            ml[j] = a.part_ml[slot];
-#pragma unroll
-            for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
-        }
+        for (int t = 0; t < NT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    template <int K>
+    __device__ __forceinline__ void fold(float2 (&ml)[K], const f32x4 (&o)[K][NT], const bool (&live)[K]) {
         float Mb = M;
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const int v = v0 + j;
-            const bool live = v <= wl && share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew);
-            if (!live) ml[j] = make_float2(-INFINITY, 0.f);
+        for (int j = 0; j < K; ++j) {
+            if (!live[j]) ml[j] = make_float2(-INFINITY, 0.f);
             Mb = fmaxf(Mb, ml[j].x);
         }
         if (Mb > M) {             // exact: otherwise the factor is 1
@@ -666,25 +651,51 @@ __device__ __forceinline__ void merge_pieces(const AttnArgs& a, int b, int g, in
             M = Mb;
         }
 #pragma unroll
-        for (int j = 0; j < kBatch; ++j) {
-            const bool live = ml[j].x != -INFINITY;
-            const float wt = live ? fast_exp2(ml[j].x - M) : 0.f;
-            l += live ? wt * ml[j].y : 0.f;
+        for (int j = 0; j < K; ++j) {
+            const bool ok = ml[j].x != -INFINITY;
+            const float wt = ok ? fast_exp2(ml[j].x - M) : 0.f;
+            l += ok ? wt * ml[j].y : 0.f;
 #pragma unroll
-            for (int t = 0; t < NT; ++t) acc[t] += live ? wt * o[j][t] : f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < NT; ++t) acc[t] += ok ? wt * o[j][t] : f32x4{0.f, 0.f, 0.f, 0.f};
         }
     }
-    if (n >= a.G) return;
-    const float inv = 1.f / l;
-    uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)(g * a.G + n) * a.o_sh;
+    // the pieces of waves wf .. wl: wave wf's is its kind-1 slot (the request
+    // starts inside its range), every later wave's its kind-0 slot; waves
+    // with no units left none.  Two pieces per round trip, in wave order.
+    __device__ __forceinline__ void fold_waves(const AttnArgs& a, int wf, int wl, int P, int skew, int nh, int qg) {
+        constexpr int kBatch = 2;
+        const int W = a.waves;
+        for (int v0 = wf; v0 <= wl; v0 += kBatch) {
+            float2 ml[kBatch];
+            f32x4 o[kBatch][NT];
+            bool live[kBatch];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        u32x2 pk;
-        pk.x = (uint32_t)f32_to_bf16_rne(acc[t][0] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][1] * inv) << 16);
-        pk.y = (uint32_t)f32_to_bf16_rne(acc[t][2] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][3] * inv) << 16);
-        *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
+            for (int j = 0; j < kBatch; ++j) {
+                const int v = min(v0 + j, wl);          // past wl: a re-read of wl's piece, dead below
+                const int64_t slot = (int64_t)(2 * v + (v == wf ? 1 : 0)) * a.G + nh;
+                ml[j] = a.part_ml[slot];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
+            }
+#pragma unroll
+            for (int j = 0; j < kBatch; ++j)
+                live[j] = v0 + j <= wl && share_bound(v0 + j, P, W, skew) < share_bound(v0 + j + 1, P, W, skew);
+            fold<kBatch>(ml, o, live);
+        }
     }
-}
+    // out[b, g G + n, dims of this lane] = acc / l, rounded to bf16
+    __device__ __forceinline__ void store(const AttnArgs& a, int b, int h, int qg) const {
+        const float inv = 1.f / l;
+        uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)h * a.o_sh;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            u32x2 pk;
+            pk.x = (uint32_t)f32_to_bf16_rne(acc[t][0] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][1] * inv) << 16);
+            pk.y = (uint32_t)f32_to_bf16_rne(acc[t][2] * inv) | ((uint32_t)f32_to_bf16_rne(acc[t][3] * inv) << 16);
+            *(u32x2*)(orow + 16 * t + 4 * qg) = pk;
+        }
+    }
+};
 
 // Mark loaded registers as read.  A step reads some of its loads only on some
 // paths (the query only at a segment change, the second page only when the
@@ -808,12 +819,12 @@ attn_mfma_kernel(AttnArgs a) {
         }
     };
     int lsum = load_lens(0);
-    zero_empty(0);
+    if (!a.fused) zero_empty(0);   // a fused step's merge pass writes every row
     int incl = wave_incl_scan(lsum, lane);
     int P = __builtin_amdgcn_readlane(incl, kWaveSize - 1);
     for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch) {
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
-        zero_empty(b0);
+        if (!a.fused) zero_empty(b0);
     }
     const int skew = share_skew(a.skew, P, a.waves);
     const int r0 = share_bound(w, P, a.waves, skew);
@@ -961,7 +972,18 @@ attn_mfma_kernel(AttnArgs a) {
         const int seg_x0 = c.x - c.p / PP;
         const bool whole = seg_x0 >= r0 && seg_x0 + (c.np + PP - 1) / PP <= r1;
         const int kind = seg_x0 < r0 ? 0 : 1;
-        if (hv) {
+        if (whole && a.fused) {
+            // the merge pass adds the new token: leave a piece here too
+            const int64_t seg = (int64_t)c.b * a.H_kv + c.g;
+            if (hv) {
+                const int64_t slot = seg * a.G + n;
+                const float f = seg_bad ? NAN : vs;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) *(f32x4*)(a.seg_o + slot * D + 16 * t + 4 * qg) = st.o[t] * f;
+                if (qg == 0) a.seg_ml[slot] = make_float2(seg_bad ? NAN : st.m, l_tot);
+            }
+            if (lane == 0) a.seg_rec[seg] = make_int4(w, w, 0, 0);
+        } else if (hv) {
             const int h = c.g * a.G + n;
             if (whole) {
                 const float f = seg_bad ? NAN : vs / l_tot;
@@ -1086,12 +1108,14 @@ attn_mfma_kernel(AttnArgs a) {
     const int en = (e.np + PP - 1) / PP;
     if (lane == 0) {
         const bool cut = ex0 >= r0 && ex0 + en > r1;
-        a.cuts[w] = cut ? make_int4(e.b, e.g, wave_of(ex0 + en - 1, P, a.waves, skew), P) : make_int4(-1, 0, 0, 0);
+        const int wl = cut ? wave_of(ex0 + en - 1, P, a.waves, skew) : 0;
+        a.cuts[w] = cut ? make_int4(e.b, e.g, wl, P) : make_int4(-1, 0, 0, 0);
+        if (cut && a.fused) a.seg_rec[(int64_t)e.b * a.H_kv + e.g] = make_int4(w, wl, P, 0);
     }
 }
 
 // One wave per attention wave w: if w's range ended inside a (request, head)
-// that began in it, combine that request's pieces (merge_pieces).
+// that began in it, combine that request's pieces.
 template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6));
@@ -1099,9 +1123,154 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int4 c = a.cuts[w];
     if (c.x < 0) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
-    const int P = __builtin_amdgcn_readfirstlane(c.w);
-    merge_pieces<D>(a, __builtin_amdgcn_readfirstlane(c.x), __builtin_amdgcn_readfirstlane(c.y), w,
-                    __builtin_amdgcn_readfirstlane(c.z), P, share_skew(a.skew, P, a.waves), lane >> 4, lane & 15);
+    const int qg = lane >> 4, n = lane & 15;
+    const int b = __builtin_amdgcn_readfirstlane(c.x), g = __builtin_amdgcn_readfirstlane(c.y);
+    const int wl = __builtin_amdgcn_readfirstlane(c.z), P = __builtin_amdgcn_readfirstlane(c.w);
+    MergeAcc<D> m;
+    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), min(n, a.G - 1), qg);
+    if (n < a.G) m.store(a, b, g * a.G + n, qg);
+}
+
+// The merge pass of a fused decode step: one workgroup per request b, one
+// wave per KV head g (strided over the workgroup's waves).  With L the
+// length before the step, each wave combines (request, head)'s pieces of the
+// attention over the first L tokens with the new token at position L (one
+// more piece: its score, weight 1 and V row), writes the output rows of the
+// G query heads, and writes the new K/V row into slot L of the request's
+// page (a byte copy, or the quantisation of bf16 rows into fp8 pools); then
+// the length becomes L + 1.  This is the append followed by attention over
+// L + 1 tokens.  A request whose slot L lies outside its table or the pool
+// gets no append, keeps its length, and attends its L tokens (flag 1).
+constexpr int kStepMergeWaves = 8;   // waves per request in the fused step's merge pass
+template <int D, bool FP8>
+__global__ void __launch_bounds__(kStepMergeWaves * kWaveSize) step_merge_kernel(AttnArgs a) {
+    constexpr int NT = D / 16;
+    constexpr int EB = FP8 ? 1 : 2;
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x & (kWaveSize - 1);
+    const int wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int qg = lane >> 4, n = lane & 15, nh = min(n, a.G - 1);
+    const int L = a.seq_lens_w[b];
+    const int maxL = a.max_pages * kPage;
+    const int Lc = L < 0 ? 0 : min(L, maxL);
+    int pg = -1;
+    if (L >= 0 && L / kPage < a.max_pages) pg = a.block_table[(int64_t)b * a.bt_stride + L / kPage];
+    const bool ok = pg >= 0 && (int64_t)pg < a.num_pages;
+    const int slot = L & (kPage - 1);
+    for (int g = wv; g < a.H_kv; g += nw) {
+        const int64_t seg = (int64_t)b * a.H_kv + g;
+        MergeAcc<D> m;
+        if (Lc > 0) {
+            const int4 r = a.seg_rec[seg];
+            if (r.x == r.y) {
+                const int64_t sl = seg * a.G + nh;
+                float2 ml[1] = {a.seg_ml[sl]};
+                f32x4 o[1][NT];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) o[0][t] = *(const f32x4*)(a.seg_o + sl * D + 16 * t + 4 * qg);
+                const bool live[1] = {true};
+                m.template fold<1>(ml, o, live);
+            } else {
+                m.fold_waves(a, r.x, r.y, r.z, share_skew(a.skew, r.z, a.waves), nh, qg);
+            }
+        }
+        if (ok) {
+            // the new K and V at this lane's dims 16 t + 4 qg .. + 3, as the pool holds them
+            const float ks = FP8 ? a.k_scale[seg] : 1.f, vsc = FP8 ? a.v_scale[seg] : 1.f;
+            const char* kn = (const char*)a.k_new + (b * a.new_sb + g * a.new_sh) * (a.quant ? 2 : EB);
+            const char* vn = (const char*)a.v_new + (b * a.vnew_sb + g * a.vnew_sh) * (a.quant ? 2 : EB);
+            const uint16_t* qrow = a.q + (int64_t)b * a.q_sb + (int64_t)(g * a.G + nh) * a.q_sh;
+            auto row4 = [&](const char* base, int d0, float sc, float (&x)[4]) {
+                if (!FP8 || a.quant) {
+                    const u32x2 w2 = *(const u32x2*)(base + d0 * 2);
+                    x[0] = __uint_as_float(w2.x << 16);
+                    x[1] = __uint_as_float(w2.x & 0xffff0000u);
+                    x[2] = __uint_as_float(w2.y << 16);
+                    x[3] = __uint_as_float(w2.y & 0xffff0000u);
+                    if (FP8) {   // quantised as the append stores it, then decoded
+                        uint32_t c4 = 0;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) c4 |= quantize_e4m3fn(x[i], sc) << (8 * i);
+                        const f32x2 lo = fp8x2_to_f32(c4, false), hi = fp8x2_to_f32(c4, true);
+                        x[0] = lo.x; x[1] = lo.y; x[2] = hi.x; x[3] = hi.y;
+                    }
+                } else {
+                    const uint32_t c4 = *(const uint32_t*)(base + d0);
+                    const f32x2 lo = fp8x2_to_f32(c4, false), hi = fp8x2_to_f32(c4, true);
+                    x[0] = lo.x; x[1] = lo.y; x[2] = hi.x; x[3] = hi.y;
+                }
+            };
+            float dot = 0.f;
+            f32x4 o[1][NT];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int d0 = 16 * t + 4 * qg;
+                float kx[4], vx[4];
+                row4(kn, d0, ks, kx);
+                row4(vn, d0, vsc, vx);
+                const u32x2 qw = *(const u32x2*)(qrow + d0);
+                const float q4[4] = {__uint_as_float(qw.x << 16), __uint_as_float(qw.x & 0xffff0000u),
+                                     __uint_as_float(qw.y << 16), __uint_as_float(qw.y & 0xffff0000u)};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) dot = fmaf(q4[i], kx[i], dot);
+                o[0][t] = f32x4{vx[0] * vsc, vx[1] * vsc, vx[2] * vsc, vx[3] * vsc};
+            }
+            dot = group_sum4(dot);
+            float2 ml[1] = {make_float2(dot * (a.scale_log2 * ks), 1.f)};
+            const bool live[1] = {true};
+            m.template fold<1>(ml, o, live);
+
+            // the append: K chunks of 16 bytes, V elements into their dim rows
+            constexpr int X = 16 / EB;
+            constexpr int CH = D / X;
+            char* kp = (char*)a.k_pages + (((int64_t)pg * a.H_kv + g) * CH) * kPage * 16;
+            char* vp = (char*)a.v_pages + ((int64_t)pg * a.H_kv + g) * (int64_t)D * kPage * EB;
+            if (lane < CH) {
+                u32x4 w4;
+                if (!a.quant) {
+                    w4 = *(const u32x4*)(kn + lane * 16);
+                } else {   // 16 bf16 -> 16 e4m3fn codes
+                    const u32x4 w0 = *(const u32x4*)(kn + lane * 32), w1 = *(const u32x4*)(kn + lane * 32 + 16);
+                    const uint32_t in[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+                    uint32_t ow[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint32_t lo = in[2 * k], hi = in[2 * k + 1];
+                        ow[k] = quantize_e4m3fn(__uint_as_float(lo << 16), ks) |
+                                (quantize_e4m3fn(__uint_as_float(lo & 0xffff0000u), ks) << 8) |
+                                (quantize_e4m3fn(__uint_as_float(hi << 16), ks) << 16) |
+                                (quantize_e4m3fn(__uint_as_float(hi & 0xffff0000u), ks) << 24);
+                    }
+                    w4 = u32x4{ow[0], ow[1], ow[2], ow[3]};
+                }
+                *(u32x4*)(kp + ((int64_t)lane * kPage + slot) * 16) = w4;
+            }
+            for (int d = lane; d < D; d += kWaveSize) {
+                if (!FP8) {
+                    *(uint16_t*)(vp + ((int64_t)d * kPage + slot) * 2) = *(const uint16_t*)(vn + d * 2);
+                } else if (!a.quant) {
+                    *(uint8_t*)(vp + (int64_t)d * kPage + slot) = *(const uint8_t*)(vn + d);
+                } else {
+                    const uint32_t bits = *(const uint16_t*)(vn + d * 2);
+                    *(uint8_t*)(vp + (int64_t)d * kPage + slot) = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), vsc);
+                }
+            }
+        }
+        if (n < a.G) {
+            if (Lc > 0 || ok) {
+                m.store(a, b, g * a.G + n, qg);
+            } else {   // nothing to attend
+                uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)(g * a.G + n) * a.o_sh;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) *(u32x2*)(orow + 16 * t + 4 * qg) = u32x2{0u, 0u};
+            }
+        }
+    }
+    __syncthreads();   // every wave has read the length
+    if (threadIdx.x == 0) {
+        if (ok) a.seq_lens_w[b] = L + 1;
+        else atomicOr(a.err, kErrAppendSlot);
+    }
 }
 
 }  // namespace
@@ -1164,6 +1333,17 @@ void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8
 
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D) {
     return dispatch(D, fp8, pages_per_step, depth, true, nullptr, 0, nullptr);
+}
+
+void launch_step_merge(const AttnArgs& a, bool fp8, hipStream_t s) {
+    const dim3 g(a.B), blk(kWaveSize * min(a.H_kv, kStepMergeWaves));
+    if (a.D == 128) {
+        if (fp8) hipLaunchKernelGGL((step_merge_kernel<128, true>), g, blk, 0, s, a);
+        else hipLaunchKernelGGL((step_merge_kernel<128, false>), g, blk, 0, s, a);
+    } else {
+        if (fp8) hipLaunchKernelGGL((step_merge_kernel<64, true>), g, blk, 0, s, a);
+        else hipLaunchKernelGGL((step_merge_kernel<64, false>), g, blk, 0, s, a);
+    }
 }
 
 void launch_merge(const AttnArgs& a, hipStream_t s) {
