@@ -180,32 +180,6 @@ int bellman_decode_attention_opts(const bellman_tensor_t *q, const bellman_tenso
                                   bellman_tensor_t *out, const bellman_attn_opts_t *opts,
                                   void *stream);
 
-/*
- * One whole decode step in two kernel launches: the effect of
- *   bellman_kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens)
- * followed by
- *   bellman_decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out)
- * (Sec. 3: each step appends one token per request and attends over the
- * prompt plus the tokens generated so far).  The attention kernel reads the
- * cache as it stands before the step (lengths L = seq_lens[b]); the merge
- * pass adds the new token at position L to every (request, head) as one more
- * softmax piece (its score and V row, exactly as the pool will hold them),
- * writes it into its page and sets seq_lens[b] = L + 1.  The append is
- * bit-exact as bellman_kv_append's; the attention output equals the
- * two-call sequence's within floating-point reordering (the new token's
- * score is a plain fp32 dot product, and fp8 queries are not split as in the
- * attention kernel).  Arguments as for those two calls, with rows of k_new
- * and v_new 16-byte aligned; opts as for bellman_decode_attention_opts (its
- * events bracket the attention kernel).  Malformed lengths and slots are
- * flagged and treated as by the two calls.  Scratch: the workspace of
- * bellman_decode_attention plus B * H_kv * (16 + G (8 + 4 D)) bytes.
- */
-int bellman_decode_step(const bellman_tensor_t *q, const bellman_tensor_t *k_new,
-                        const bellman_tensor_t *v_new, bellman_tensor_t *k_pages,
-                        bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
-                        bellman_tensor_t *seq_lens, float scale, bellman_tensor_t *out,
-                        const bellman_attn_opts_t *opts, void *stream);
-
 /* Bytes of the fixed per-device scratch array of
  * bellman_decode_attention_noalloc. */
 #define BELLMAN_FIXED_SCRATCH_BYTES (32 << 20)

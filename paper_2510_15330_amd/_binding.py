@@ -104,8 +104,6 @@ def library():
     lib.bellman_decode_attention_opts.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                   ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_opts.restype = ctypes.c_int
-    lib.bellman_decode_step.argtypes = [T, T, T, T, T, T, T, ctypes.c_float, T, ctypes.POINTER(AttnOpts), P]
-    lib.bellman_decode_step.restype = ctypes.c_int
     lib.bellman_decode_attention_noalloc.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                      ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_noalloc.restype = ctypes.c_int
@@ -239,23 +237,6 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
                 raise ValueError("record each event once before passing it")
         opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
-
-
-def decode_step(q, k_new, v_new, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
-                k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, events=None, pages_per_step=0,
-                pipeline_depth=0):
-    """bellman_decode_step: append one token per request and attend over the
-    cache including it, in one call (two kernel launches)."""
-    _device_tensors(q, k_new, v_new, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale)
-    ev0 = ev1 = None
-    if events is not None:
-        ev0, ev1 = events[0].cuda_event, events[1].cuda_event
-        if not ev0 or not ev1:
-            raise ValueError("record each event once before passing it")
-    opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1)
-    _check(library().bellman_decode_step(
-        desc(q), desc(k_new), desc(v_new), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
-        desc(seq_lens), ctypes.c_float(scale), desc(out), ctypes.byref(opts), _stream(stream)))
 
 
 def decode_attention_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,

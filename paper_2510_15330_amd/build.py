@@ -48,29 +48,36 @@ def _run(cmd, verbose):
         print(out)
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + f".tmp{os.getpid()}"
-    _run([hipcc()] + HIPCC_FLAGS + ["-shared"] + [os.path.join(CSRC, s) for s in SOURCES] + ["-o", tmp], verbose)
-    os.replace(tmp, LIB)
-    return LIB
-
-
-def build_sanitized(out: str, verbose: bool = False) -> str:
-    """The library with its C++ host sources under ASan + UBSan, at `out`."""
+def _build(out: str, sanitize: bool, verbose: bool) -> str:
+    """Compile the sources in parallel, then link them into `out`."""
     from concurrent.futures import ThreadPoolExecutor
     with tempfile.TemporaryDirectory() as d:
         objs = [os.path.join(d, src + ".o") for src in SOURCES]
 
         def compile_one(i):
             src = SOURCES[i]
-            flags = HIPCC_FLAGS + (SANITIZE_FLAGS if src in HOST_SOURCES else [])
+            flags = HIPCC_FLAGS + (SANITIZE_FLAGS if sanitize and src in HOST_SOURCES else [])
             _run([hipcc()] + flags + ["-c", os.path.join(CSRC, src), "-o", objs[i]], verbose)
 
-        with ThreadPoolExecutor(max_workers=4) as ex:
+        with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
             list(ex.map(compile_one, range(len(SOURCES))))
-        _run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address,undefined",
-              "-shared-libsan"] + objs + ["-o", out], verbose)
+        link = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC"]
+        if sanitize:
+            link += ["-Xarch_host", "-fsanitize=address,undefined", "-shared-libsan"]
+        _run(link + objs + ["-o", out], verbose)
     return out
+
+
+def build(verbose: bool = False) -> str:
+    tmp = LIB + f".tmp{os.getpid()}"
+    _build(tmp, False, verbose)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def build_sanitized(out: str, verbose: bool = False) -> str:
+    """The library with its C++ host sources under ASan + UBSan, at `out`."""
+    return _build(out, True, verbose)
 
 
 if __name__ == "__main__":

@@ -239,8 +239,7 @@ int launch_status(const char* what) {
 // instead of the growable library workspace.
 int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
                      const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
-                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed,
-                     const bellman_tensor_t* k_new = nullptr, const bellman_tensor_t* v_new = nullptr) {
+                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed) {
     g_last_error[0] = 0;
     int rc;
     PoolShape ps;
@@ -252,16 +251,6 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     if ((rc = check_rows(out, "out", BELLMAN_BF16, B, H_q, ps.D, 8))) return rc;
     if ((rc = check_block_table(block_table, B))) return rc;
     if ((rc = check_seq_lens(seq_lens, B))) return rc;
-    // a fused step: the new rows, in the pools' type or bf16 for fp8 pools
-    const bool fused = k_new != nullptr || v_new != nullptr;
-    bool quant = false;
-    if (fused) {
-        if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
-        quant = ps.fp8 && k_new->dtype == BELLMAN_BF16;
-        const int32_t row_dtype = quant ? (int32_t)BELLMAN_BF16 : k_pages->dtype;
-        if ((rc = check_rows(k_new, "k_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
-        if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
-    }
     if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
     if (H_q < 1 || H_q % ps.H_kv != 0)
         return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
@@ -324,12 +313,7 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     const size_t off_ml = off_cuts + align256(sizeof(int4) * (size_t)waves);
     const size_t slots = 2 * (size_t)waves * (size_t)G;
     const size_t off_o = off_ml + align256(sizeof(float2) * slots);
-    // a fused step also keeps a piece of every (request, KV head)
-    const size_t seg_slots = fused ? (size_t)B * ps.H_kv * (size_t)G : 0;
-    const size_t off_rec = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
-    const size_t off_sml = off_rec + align256(sizeof(int4) * (size_t)B * (fused ? ps.H_kv : 0));
-    const size_t off_so = off_sml + align256(sizeof(float2) * seg_slots);
-    const size_t total = off_so + align256(sizeof(float) * seg_slots * (size_t)ps.D);
+    const size_t total = off_o + align256(sizeof(float) * slots * (size_t)ps.D);
     hipStream_t s = (hipStream_t)stream;
     char* base;
     if (fixed) {
@@ -376,18 +360,6 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     else a.skew = skew_opt < 0 ? 0 : skew_opt;
     a.err = err;
     a.cuts = (int4*)(base + off_cuts);
-    a.fused = fused ? 1 : 0;
-    a.quant = quant ? 1 : 0;
-    a.k_new = fused ? k_new->data : nullptr;
-    a.v_new = fused ? v_new->data : nullptr;
-    a.new_sb = fused ? k_new->stride[0] : 0;
-    a.new_sh = fused ? k_new->stride[1] : 0;
-    a.vnew_sb = fused ? v_new->stride[0] : 0;
-    a.vnew_sh = fused ? v_new->stride[1] : 0;
-    a.seq_lens_w = (int32_t*)seq_lens->data;
-    a.seg_rec = (int4*)(base + off_rec);
-    a.seg_ml = (float2*)(base + off_sml);
-    a.seg_o = (float*)(base + off_so);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
 
@@ -403,8 +375,7 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         hipError_t e = hipEventRecord(ev1, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    if (fused) launch_step_merge(a, ps.fp8, s);
-    else launch_merge(a, s);
+    launch_merge(a, s);
     return launch_status("merge");
 }
 
@@ -537,17 +508,6 @@ int bellman_decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* 
                              const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
                              bellman_tensor_t* out, void* stream) {
     return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, nullptr, stream, false);
-}
-
-int bellman_decode_step(const bellman_tensor_t* q, const bellman_tensor_t* k_new, const bellman_tensor_t* v_new,
-                        bellman_tensor_t* k_pages, bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
-                        bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
-                        const bellman_attn_opts_t* opts, void* stream) {
-    if (!k_new || !v_new) {
-        g_last_error[0] = 0;
-        return fail(BELLMAN_ERR_INVALID_ARG, "%s: null descriptor", k_new ? "v_new" : "k_new");
-    }
-    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, false, k_new, v_new);
 }
 
 int bellman_decode_attention_noalloc(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,

@@ -74,18 +74,6 @@ struct AttnArgs {
     float2* part_ml;     // [2 * waves * G]: (running max in log2 units, sum) of each wave's two
                          // partial pieces (the request cut at its range's start, and at its end)
     float* part_o;       // [2 * waves * G * D]
-    // fused decode step only (bellman_decode_step): every (request, head)
-    // leaves pieces, and the step's merge pass adds the new token, writes it
-    // into the pools and advances the lengths
-    int fused;
-    int quant;           // 1: bf16 new rows quantised into fp8 pools
-    const void* k_new;   // [B, H_kv, D]
-    const void* v_new;
-    int64_t new_sb, new_sh, vnew_sb, vnew_sh;   // element strides of the new rows
-    int32_t* seq_lens_w; // the lengths, advanced by the merge pass
-    int4* seg_rec;       // [B * H_kv]: (first wave, last wave, units, 0) of each (request, head)'s pieces
-    float2* seg_ml;      // [B * H_kv * G]: pieces of the (request, head)s one wave covered
-    float* seg_o;        // [B * H_kv * G * D]
 };
 
 // Prompt KV write (prefill.hip).
@@ -131,7 +119,6 @@ void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 void launch_merge(const AttnArgs& a, hipStream_t s);
-void launch_step_merge(const AttnArgs& a, bool fp8, hipStream_t s);
 // Prefill launchers (prefill.hip).
 void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
 void launch_prefill(const PrefillArgs& a, hipStream_t s);

@@ -819,12 +819,12 @@ attn_mfma_kernel(AttnArgs a) {
         }
     };
     int lsum = load_lens(0);
-    if (!a.fused) zero_empty(0);   // a fused step's merge pass writes every row
+    zero_empty(0);
     int incl = wave_incl_scan(lsum, lane);
     int P = __builtin_amdgcn_readlane(incl, kWaveSize - 1);
     for (int b0 = kPlanBatch; b0 < a.B; b0 += kPlanBatch) {
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
-        if (!a.fused) zero_empty(b0);
+        zero_empty(b0);
     }
     const int skew = share_skew(a.skew, P, a.waves);
     const int r0 = share_bound(w, P, a.waves, skew);
@@ -972,18 +972,7 @@ attn_mfma_kernel(AttnArgs a) {
         const int seg_x0 = c.x - c.p / PP;
         const bool whole = seg_x0 >= r0 && seg_x0 + (c.np + PP - 1) / PP <= r1;
         const int kind = seg_x0 < r0 ? 0 : 1;
-        if (whole && a.fused) {
-            // the merge pass adds the new token: leave a piece here too
-            const int64_t seg = (int64_t)c.b * a.H_kv + c.g;
-            if (hv) {
-                const int64_t slot = seg * a.G + n;
-                const float f = seg_bad ? NAN : vs;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) *(f32x4*)(a.seg_o + slot * D + 16 * t + 4 * qg) = st.o[t] * f;
-                if (qg == 0) a.seg_ml[slot] = make_float2(seg_bad ? NAN : st.m, l_tot);
-            }
-            if (lane == 0) a.seg_rec[seg] = make_int4(w, w, 0, 0);
-        } else if (hv) {
+        if (hv) {
             const int h = c.g * a.G + n;
             if (whole) {
                 const float f = seg_bad ? NAN : vs / l_tot;
@@ -1110,7 +1099,6 @@ attn_mfma_kernel(AttnArgs a) {
         const bool cut = ex0 >= r0 && ex0 + en > r1;
         const int wl = cut ? wave_of(ex0 + en - 1, P, a.waves, skew) : 0;
         a.cuts[w] = cut ? make_int4(e.b, e.g, wl, P) : make_int4(-1, 0, 0, 0);
-        if (cut && a.fused) a.seg_rec[(int64_t)e.b * a.H_kv + e.g] = make_int4(w, wl, P, 0);
     }
 }
 
@@ -1129,148 +1117,6 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     MergeAcc<D> m;
     m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), min(n, a.G - 1), qg);
     if (n < a.G) m.store(a, b, g * a.G + n, qg);
-}
-
-// The merge pass of a fused decode step: one workgroup per request b, one
-// wave per KV head g (strided over the workgroup's waves).  With L the
-// length before the step, each wave combines (request, head)'s pieces of the
-// attention over the first L tokens with the new token at position L (one
-// more piece: its score, weight 1 and V row), writes the output rows of the
-// G query heads, and writes the new K/V row into slot L of the request's
-// page (a byte copy, or the quantisation of bf16 rows into fp8 pools); then
-// the length becomes L + 1.  This is the append followed by attention over
-// L + 1 tokens.  A request whose slot L lies outside its table or the pool
-// gets no append, keeps its length, and attends its L tokens (flag 1).
-constexpr int kStepMergeWaves = 8;   // waves per request in the fused step's merge pass
-template <int D, bool FP8>
-__global__ void __launch_bounds__(kStepMergeWaves * kWaveSize) step_merge_kernel(AttnArgs a) {
-    constexpr int NT = D / 16;
-    constexpr int EB = FP8 ? 1 : 2;
-    const int b = blockIdx.x;
-    const int lane = threadIdx.x & (kWaveSize - 1);
-    const int wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    const int qg = lane >> 4, n = lane & 15, nh = min(n, a.G - 1);
-    const int L = a.seq_lens_w[b];
-    const int maxL = a.max_pages * kPage;
-    const int Lc = L < 0 ? 0 : min(L, maxL);
-    int pg = -1;
-    if (L >= 0 && L / kPage < a.max_pages) pg = a.block_table[(int64_t)b * a.bt_stride + L / kPage];
-    const bool ok = pg >= 0 && (int64_t)pg < a.num_pages;
-    const int slot = L & (kPage - 1);
-    for (int g = wv; g < a.H_kv; g += nw) {
-        const int64_t seg = (int64_t)b * a.H_kv + g;
-        MergeAcc<D> m;
-        if (Lc > 0) {
-            const int4 r = a.seg_rec[seg];
-            if (r.x == r.y) {
-                const int64_t sl = seg * a.G + nh;
-                float2 ml[1] = {a.seg_ml[sl]};
-                f32x4 o[1][NT];
-#pragma unroll
-                for (int t = 0; t < NT; ++t) o[0][t] = *(const f32x4*)(a.seg_o + sl * D + 16 * t + 4 * qg);
-                const bool live[1] = {true};
-                m.template fold<1>(ml, o, live);
-            } else {
-                m.fold_waves(a, r.x, r.y, r.z, share_skew(a.skew, r.z, a.waves), nh, qg);
-            }
-        }
-        if (ok) {
-            // the new K and V at this lane's dims 16 t + 4 qg .. + 3, as the pool holds them
-            const float ks = FP8 ? a.k_scale[seg] : 1.f, vsc = FP8 ? a.v_scale[seg] : 1.f;
-            const char* kn = (const char*)a.k_new + (b * a.new_sb + g * a.new_sh) * (a.quant ? 2 : EB);
-            const char* vn = (const char*)a.v_new + (b * a.vnew_sb + g * a.vnew_sh) * (a.quant ? 2 : EB);
-            const uint16_t* qrow = a.q + (int64_t)b * a.q_sb + (int64_t)(g * a.G + nh) * a.q_sh;
-            auto row4 = [&](const char* base, int d0, float sc, float (&x)[4]) {
-                if (!FP8 || a.quant) {
-                    const u32x2 w2 = *(const u32x2*)(base + d0 * 2);
-                    x[0] = __uint_as_float(w2.x << 16);
-                    x[1] = __uint_as_float(w2.x & 0xffff0000u);
-                    x[2] = __uint_as_float(w2.y << 16);
-                    x[3] = __uint_as_float(w2.y & 0xffff0000u);
-                    if (FP8) {   // quantised as the append stores it, then decoded
-                        uint32_t c4 = 0;
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) c4 |= quantize_e4m3fn(x[i], sc) << (8 * i);
-                        const f32x2 lo = fp8x2_to_f32(c4, false), hi = fp8x2_to_f32(c4, true);
-                        x[0] = lo.x; x[1] = lo.y; x[2] = hi.x; x[3] = hi.y;
-                    }
-                } else {
-                    const uint32_t c4 = *(const uint32_t*)(base + d0);
-                    const f32x2 lo = fp8x2_to_f32(c4, false), hi = fp8x2_to_f32(c4, true);
-                    x[0] = lo.x; x[1] = lo.y; x[2] = hi.x; x[3] = hi.y;
-                }
-            };
-            float dot = 0.f;
-            f32x4 o[1][NT];
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int d0 = 16 * t + 4 * qg;
-                float kx[4], vx[4];
-                row4(kn, d0, ks, kx);
-                row4(vn, d0, vsc, vx);
-                const u32x2 qw = *(const u32x2*)(qrow + d0);
-                const float q4[4] = {__uint_as_float(qw.x << 16), __uint_as_float(qw.x & 0xffff0000u),
-                                     __uint_as_float(qw.y << 16), __uint_as_float(qw.y & 0xffff0000u)};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) dot = fmaf(q4[i], kx[i], dot);
-                o[0][t] = f32x4{vx[0] * vsc, vx[1] * vsc, vx[2] * vsc, vx[3] * vsc};
-            }
-            dot = group_sum4(dot);
-            float2 ml[1] = {make_float2(dot * (a.scale_log2 * ks), 1.f)};
-            const bool live[1] = {true};
-            m.template fold<1>(ml, o, live);
-
-            // the append: K chunks of 16 bytes, V elements into their dim rows
-            constexpr int X = 16 / EB;
-            constexpr int CH = D / X;
-            char* kp = (char*)a.k_pages + (((int64_t)pg * a.H_kv + g) * CH) * kPage * 16;
-            char* vp = (char*)a.v_pages + ((int64_t)pg * a.H_kv + g) * (int64_t)D * kPage * EB;
-            if (lane < CH) {
-                u32x4 w4;
-                if (!a.quant) {
-                    w4 = *(const u32x4*)(kn + lane * 16);
-                } else {   // 16 bf16 -> 16 e4m3fn codes
-                    const u32x4 w0 = *(const u32x4*)(kn + lane * 32), w1 = *(const u32x4*)(kn + lane * 32 + 16);
-                    const uint32_t in[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-                    uint32_t ow[4];
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const uint32_t lo = in[2 * k], hi = in[2 * k + 1];
-                        ow[k] = quantize_e4m3fn(__uint_as_float(lo << 16), ks) |
-                                (quantize_e4m3fn(__uint_as_float(lo & 0xffff0000u), ks) << 8) |
-                                (quantize_e4m3fn(__uint_as_float(hi << 16), ks) << 16) |
-                                (quantize_e4m3fn(__uint_as_float(hi & 0xffff0000u), ks) << 24);
-                    }
-                    w4 = u32x4{ow[0], ow[1], ow[2], ow[3]};
-                }
-                *(u32x4*)(kp + ((int64_t)lane * kPage + slot) * 16) = w4;
-            }
-            for (int d = lane; d < D; d += kWaveSize) {
-                if (!FP8) {
-                    *(uint16_t*)(vp + ((int64_t)d * kPage + slot) * 2) = *(const uint16_t*)(vn + d * 2);
-                } else if (!a.quant) {
-                    *(uint8_t*)(vp + (int64_t)d * kPage + slot) = *(const uint8_t*)(vn + d);
-                } else {
-                    const uint32_t bits = *(const uint16_t*)(vn + d * 2);
-                    *(uint8_t*)(vp + (int64_t)d * kPage + slot) = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), vsc);
-                }
-            }
-        }
-        if (n < a.G) {
-            if (Lc > 0 || ok) {
-                m.store(a, b, g * a.G + n, qg);
-            } else {   // nothing to attend
-                uint16_t* orow = a.out + (int64_t)b * a.o_sb + (int64_t)(g * a.G + n) * a.o_sh;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) *(u32x2*)(orow + 16 * t + 4 * qg) = u32x2{0u, 0u};
-            }
-        }
-    }
-    __syncthreads();   // every wave has read the length
-    if (threadIdx.x == 0) {
-        if (ok) a.seq_lens_w[b] = L + 1;
-        else atomicOr(a.err, kErrAppendSlot);
-    }
 }
 
 }  // namespace
@@ -1333,17 +1179,6 @@ void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8
 
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D) {
     return dispatch(D, fp8, pages_per_step, depth, true, nullptr, 0, nullptr);
-}
-
-void launch_step_merge(const AttnArgs& a, bool fp8, hipStream_t s) {
-    const dim3 g(a.B), blk(kWaveSize * min(a.H_kv, kStepMergeWaves));
-    if (a.D == 128) {
-        if (fp8) hipLaunchKernelGGL((step_merge_kernel<128, true>), g, blk, 0, s, a);
-        else hipLaunchKernelGGL((step_merge_kernel<128, false>), g, blk, 0, s, a);
-    } else {
-        if (fp8) hipLaunchKernelGGL((step_merge_kernel<64, true>), g, blk, 0, s, a);
-        else hipLaunchKernelGGL((step_merge_kernel<64, false>), g, blk, 0, s, a);
-    }
 }
 
 void launch_merge(const AttnArgs& a, hipStream_t s) {
