@@ -661,26 +661,41 @@ struct MergeAcc {
     }
     // the pieces of waves wf .. wl: wave wf's is its kind-1 slot (the request
     // starts inside its range), every later wave's its kind-0 slot; waves
-    // with no units left none.  Two pieces per round trip, in wave order.
-    __device__ __forceinline__ void fold_waves(const AttnArgs& a, int wf, int wl, int P, int skew, int nh, int qg) {
-        constexpr int kBatch = 2;
+    // with no units left none.  Two pieces per round trip, in wave order;
+    // the first batch may already be in `ml0`, `o0` (loaded with the record).
+    static __device__ __forceinline__ int64_t slot_of(const AttnArgs& a, int v, int wf, int nh) {
+        return (int64_t)(2 * v + (v == wf ? 1 : 0)) * a.G + nh;
+    }
+    static __device__ __forceinline__ void load2(const AttnArgs& a, int v0, int wf, int wl, int nh, int qg,
+                                                 float2 (&ml)[2], f32x4 (&o)[2][NT]) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int v = min(v0 + j, wl);          // past wl: a re-read of wl's piece, dead below
+            const int64_t slot = slot_of(a, v, wf, nh);
+            ml[j] = a.part_ml[slot];
+#pragma unroll
+            for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
+        }
+    }
+    __device__ __forceinline__ void fold_waves(const AttnArgs& a, int wf, int wl, int P, int skew, int nh, int qg,
+                                               float2 (&ml0)[2], f32x4 (&o0)[2][NT]) {
         const int W = a.waves;
-        for (int v0 = wf; v0 <= wl; v0 += kBatch) {
-            float2 ml[kBatch];
-            f32x4 o[kBatch][NT];
-            bool live[kBatch];
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j) {
-                const int v = min(v0 + j, wl);          // past wl: a re-read of wl's piece, dead below
-                const int64_t slot = (int64_t)(2 * v + (v == wf ? 1 : 0)) * a.G + nh;
-                ml[j] = a.part_ml[slot];
-#pragma unroll
-                for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
-            }
-#pragma unroll
-            for (int j = 0; j < kBatch; ++j)
-                live[j] = v0 + j <= wl && share_bound(v0 + j, P, W, skew) < share_bound(v0 + j + 1, P, W, skew);
-            fold<kBatch>(ml, o, live);
+        // every wave holds units when the lightest weight's share of P is
+        // above one unit: (256 - k) P > C(W), C(W) <= (256 + k) W
+        const bool all_units = (int64_t)(256 - skew) * P > (int64_t)(256 + skew) * W;
+        auto has_units = [&](int v) {
+            return v <= wl && (all_units || share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew));
+        };
+        {
+            const bool live[2] = {has_units(wf), has_units(wf + 1)};
+            fold<2>(ml0, o0, live);
+        }
+        for (int v0 = wf + 2; v0 <= wl; v0 += 2) {
+            float2 ml[2];
+            f32x4 o[2][NT];
+            load2(a, v0, wf, wl, nh, qg, ml, o);
+            const bool live[2] = {has_units(v0), has_units(v0 + 1)};
+            fold<2>(ml, o, live);
         }
     }
     // out[b, g G + n, dims of this lane] = acc / l, rounded to bf16
@@ -1108,14 +1123,20 @@ template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6));
     if (w >= a.waves) return;
-    const int4 c = a.cuts[w];
-    if (c.x < 0) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
-    const int qg = lane >> 4, n = lane & 15;
+    const int qg = lane >> 4, n = lane & 15, nh = min(n, a.G - 1);
+    // the record and, in the same round trip, the first two pieces a cut
+    // starting in wave w would have (slots 2w + 1 and 2w + 2; past the
+    // workspace's last wave a re-read of 2w + 1)
+    const int4 c = a.cuts[w];
+    float2 ml0[2];
+    f32x4 o0[2][D / 16];
+    MergeAcc<D>::load2(a, w, w, min(w + 1, a.waves - 1), nh, qg, ml0, o0);
+    if (c.x < 0) return;
     const int b = __builtin_amdgcn_readfirstlane(c.x), g = __builtin_amdgcn_readfirstlane(c.y);
     const int wl = __builtin_amdgcn_readfirstlane(c.z), P = __builtin_amdgcn_readfirstlane(c.w);
     MergeAcc<D> m;
-    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), min(n, a.G - 1), qg);
+    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), nh, qg, ml0, o0);
     if (n < a.G) m.store(a, b, g * a.G + n, qg);
 }
 
