@@ -82,7 +82,8 @@ typedef struct bellman_tensor {
 /*
  * Append one token per request to the paged KV cache (the step that grows
  * each request's KV length by one token per decode step, Sec. 3).
- *   k_new, v_new  [B, H_kv, D], innermost dim contiguous.  Either the
+ *   k_new, v_new  [B, H_kv, D], innermost dim contiguous, rows 16-byte
+ *                 aligned.  Either the
  *                 pools' element type (codes copied as they are), or bf16
  *                 rows for fp8 pools: then each value x of KV head g is
  *                 stored as e4m3fn(x / scale[b, g]) with the pool's

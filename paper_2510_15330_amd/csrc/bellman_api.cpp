@@ -456,9 +456,8 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     // bf16 rows into fp8 pools are quantised with the pools' dequant scales
     const bool quant = ps.fp8 && k_new->dtype == BELLMAN_BF16;
     const int32_t row_dtype = quant ? (int32_t)BELLMAN_BF16 : k_pages->dtype;
-    const size_t row_eb = (size_t)elem_size(row_dtype);
     if ((rc = check_rows(k_new, "k_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
-    if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, row_eb))) return rc;
+    if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
     if ((rc = check_block_table(block_table, B))) return rc;
     if ((rc = check_seq_lens(seq_lens, B))) return rc;
     if (quant && (!k_pages->dequant_scale || !v_pages->dequant_scale))

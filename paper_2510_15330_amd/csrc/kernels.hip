@@ -67,75 +67,105 @@ __device__ __forceinline__ uint32_t quantize_e4m3fn(float x, float scale) {
 
 // One workgroup per request: write the new K row into its 16-byte chunks and
 // the new V row into its slot column (copying codes, or quantising bf16 rows
-// into fp8 pools), then advance the request's length.
+// into fp8 pools), then advance the request's length.  Work items are K
+// chunks (16 bytes of the pool) and groups of V dims (one 16-byte load of the
+// source row, then one store per dim); each thread issues the loads of up to
+// kAppendPer items before any store, and the loads do not wait for the
+// length and block-table reads that decide where they go.
+constexpr int kAppendPer = 4;
+
+template <int EB, bool QUANT>
+__device__ __forceinline__ void append_rows(const AppendArgs& a, int b, int pg, int slot, bool ok) {
+    constexpr int X = 16 / EB;                  // pool elements per 16-byte K chunk
+    constexpr int GV = QUANT ? 8 : 16 / EB;     // V dims per 16-byte source load
+    const int chunks = a.D / X;
+    const int nk = a.H_kv * chunks, nv = a.H_kv * (a.D / GV);
+    const int64_t tile_elems = (int64_t)a.D * kPage;
+    char* kp = (char*)a.k_pages;
+    char* vp = (char*)a.v_pages;
+    const char* kn = (const char*)a.k_new;
+    const char* vn = (const char*)a.v_new;
+    constexpr int SB = QUANT ? 2 : EB;          // source element bytes
+    for (int base = 0; base < nk + nv; base += kAppendPer * (int)blockDim.x) {
+        u32x4 lo[kAppendPer], hi[kAppendPer];
+#pragma unroll
+        for (int j = 0; j < kAppendPer; ++j) {
+            const int it = base + j * (int)blockDim.x + (int)threadIdx.x;
+            if (it < nk) {
+                const int g = it / chunks, c = it - g * chunks;
+                const char* src = kn + ((int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * X) * SB;
+                lo[j] = *(const u32x4*)src;
+                if (QUANT) hi[j] = *(const u32x4*)(src + 16);
+            } else if (it < nk + nv) {
+                const int iv = it - nk;
+                const int per = a.D / GV;
+                const int g = iv / per, d0 = (iv - g * per) * GV;
+                lo[j] = *(const u32x4*)(vn + ((int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d0) * SB);
+            }
+        }
+        if (!ok) return;
+#pragma unroll
+        for (int j = 0; j < kAppendPer; ++j) {
+            const int it = base + j * (int)blockDim.x + (int)threadIdx.x;
+            if (it < nk) {
+                const int g = it / chunks, c = it - g * chunks;
+                const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;   // 16-byte units
+                u32x4 w = lo[j];
+                if (QUANT) {   // 16 bf16 -> 16 e4m3fn codes with the (request, head)'s K scale
+                    const float ks = a.k_scale[(int64_t)b * a.H_kv + g];
+                    const uint32_t in[8] = {lo[j].x, lo[j].y, lo[j].z, lo[j].w, hi[j].x, hi[j].y, hi[j].z, hi[j].w};
+                    uint32_t ow[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint32_t l2 = in[2 * k], h2 = in[2 * k + 1];
+                        ow[k] = quantize_e4m3fn(__uint_as_float(l2 << 16), ks) |
+                                (quantize_e4m3fn(__uint_as_float(l2 & 0xffff0000u), ks) << 8) |
+                                (quantize_e4m3fn(__uint_as_float(h2 << 16), ks) << 16) |
+                                (quantize_e4m3fn(__uint_as_float(h2 & 0xffff0000u), ks) << 24);
+                    }
+                    w = u32x4{ow[0], ow[1], ow[2], ow[3]};
+                }
+                *(u32x4*)(kp + dst * 16) = w;
+            } else if (it < nk + nv) {
+                const int iv = it - nk;
+                const int per = a.D / GV;
+                const int g = iv / per, d0 = (iv - g * per) * GV;
+                char* col = vp + (((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d0 * kPage + slot) * EB;
+                const uint32_t wd[4] = {lo[j].x, lo[j].y, lo[j].z, lo[j].w};
+                if (QUANT) {
+                    const float vs = a.v_scale[(int64_t)b * a.H_kv + g];
+#pragma unroll
+                    for (int e = 0; e < GV; ++e) {
+                        const uint32_t bits = (wd[e >> 1] >> (16 * (e & 1))) & 0xffffu;
+                        *(uint8_t*)(col + (int64_t)e * kPage) = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), vs);
+                    }
+                } else if (EB == 2) {
+#pragma unroll
+                    for (int e = 0; e < GV; ++e)
+                        *(uint16_t*)(col + (int64_t)e * kPage * 2) = (uint16_t)(wd[e >> 1] >> (16 * (e & 1)));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < GV; ++e)
+                        *(uint8_t*)(col + (int64_t)e * kPage) = (uint8_t)(wd[e >> 2] >> (8 * (e & 3)));
+                }
+            }
+        }
+    }
+}
+
 __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
     const int b = blockIdx.x;
     const int L = a.seq_lens[b];
     const int pi = L >> 4;
-    bool ok = L >= 0 && pi < a.max_pages;
-    int pg = ok ? a.block_table[(int64_t)b * a.bt_stride + pi] : -1;
-    ok = ok && pg >= 0 && (int64_t)pg < a.num_pages;
-    if (!ok) {
-        if (threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
-        return;
-    }
+    const bool in_table = L >= 0 && pi < a.max_pages;
+    const int pg = in_table ? a.block_table[(int64_t)b * a.bt_stride + pi] : -1;
+    const bool ok = pg >= 0 && (int64_t)pg < a.num_pages;
+    if (!ok && threadIdx.x == 0) atomicOr(a.err, kErrAppendSlot);
     const int slot = L & (kPage - 1);
-    const int eb = a.elem_bytes;
-    const int x = 16 / eb;
-    const int chunks = a.D / x;
-    const int64_t tile_elems = (int64_t)a.D * kPage;
-
-    char* kp = (char*)a.k_pages;
-    char* vp = (char*)a.v_pages;
-    if (!a.quant) {
-        const char* kn = (const char*)a.k_new;
-        for (int i = threadIdx.x; i < a.H_kv * chunks; i += blockDim.x) {
-            const int g = i / chunks, c = i - g * chunks;
-            const int64_t src = (int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * x;
-            const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;  // 16-byte units
-            *(u32x4*)(kp + dst * 16) = *(const u32x4*)(kn + src * eb);
-        }
-        const char* vn = (const char*)a.v_new;
-        for (int i = threadIdx.x; i < a.H_kv * a.D; i += blockDim.x) {
-            const int g = i / a.D, d = i - g * a.D;
-            const int64_t src = (int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d;
-            const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d * kPage + slot;
-            if (eb == 2)
-                *(uint16_t*)(vp + dst * 2) = *(const uint16_t*)(vn + src * 2);
-            else
-                *(uint8_t*)(vp + dst) = *(const uint8_t*)(vn + src);
-        }
-    } else {
-        // bf16 rows -> e4m3fn codes; fp8 pools hold 16 dims per 16-byte chunk
-        const uint16_t* kn = (const uint16_t*)a.k_new;
-        for (int i = threadIdx.x; i < a.H_kv * chunks; i += blockDim.x) {
-            const int g = i / chunks, c = i - g * chunks;
-            const float ks = a.k_scale[(int64_t)b * a.H_kv + g];
-            const uint16_t* src = kn + (int64_t)b * a.new_sb + (int64_t)g * a.new_sh + (int64_t)c * 16;
-            const u32x4 w0 = *(const u32x4*)src;
-            const u32x4 w1 = *(const u32x4*)(src + 8);
-            const uint32_t in[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-            uint32_t outw[4];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint32_t lo = in[2 * k], hi = in[2 * k + 1];
-                outw[k] = quantize_e4m3fn(__uint_as_float(lo << 16), ks) |
-                          (quantize_e4m3fn(__uint_as_float(lo & 0xffff0000u), ks) << 8) |
-                          (quantize_e4m3fn(__uint_as_float(hi << 16), ks) << 16) |
-                          (quantize_e4m3fn(__uint_as_float(hi & 0xffff0000u), ks) << 24);
-            }
-            const int64_t dst = (((int64_t)pg * a.H_kv + g) * chunks + c) * kPage + slot;
-            *(u32x4*)(kp + dst * 16) = u32x4{outw[0], outw[1], outw[2], outw[3]};
-        }
-        const uint16_t* vn = (const uint16_t*)a.v_new;
-        for (int i = threadIdx.x; i < a.H_kv * a.D; i += blockDim.x) {
-            const int g = i / a.D, d = i - g * a.D;
-            const float vs = a.v_scale[(int64_t)b * a.H_kv + g];
-            const uint32_t bits = vn[(int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh + d];
-            const int64_t dst = ((int64_t)pg * a.H_kv + g) * tile_elems + (int64_t)d * kPage + slot;
-            *(uint8_t*)(vp + dst) = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), vs);
-        }
-    }
+    if (a.quant) append_rows<1, true>(a, b, pg, slot, ok);
+    else if (a.elem_bytes == 2) append_rows<2, false>(a, b, pg, slot, ok);
+    else append_rows<1, false>(a, b, pg, slot, ok);
+    if (!ok) return;
     __syncthreads();  // every thread has read seq_lens[b]
     if (threadIdx.x == 0) a.seq_lens[b] = L + 1;
 }

@@ -131,6 +131,7 @@ APPEND_CASES = [
     ("v_new batch", lambda B_, g: g.update(vn=t(B_.BF16, [3, 8, 128])), ERR_INVALID, "v_new: shape"),
     ("seq_lens null", lambda B_, g: g.update(sl=t(B_.INT32, [4], data=None)), ERR_INVALID, "null data"),
     ("misaligned k_new", lambda B_, g: g.update(kn=t(B_.BF16, [4, 8, 128], data=FAKE + 4)), ERR_UNSUPPORTED, "aligned"),
+    ("misaligned v_new", lambda B_, g: g.update(vn=t(B_.BF16, [4, 8, 128], data=FAKE + 2)), ERR_UNSUPPORTED, "aligned"),
     ("quantising without scales", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 8, 16, 16]),
                                                          v=t(B_.FP8_E4M3FN, [100, 8, 128, 16])),
      ERR_INVALID, "needs dequant_scale"),
