@@ -1,9 +1,15 @@
-"""ctypes binding of the closed-loop serving model (bellman_sim_run).
+"""The closed-loop serving model (bellman_sim_run) from Python.
 
-Argument marshalling only: the model runs in libbellman.  ``run`` takes a
-``traces.Trace`` and configuration keywords (the fields of
-bellman_sim_config_t) and returns the per-request and per-tick records as
-numpy structured arrays plus the run's totals.
+``run`` is the binding: it marshals a ``traces.Trace`` and configuration
+keywords (the fields of bellman_sim_config_t) into the library, where the
+model runs, and returns the per-request and per-tick records as numpy
+structured arrays plus the run's totals.  The rest of the module is the
+experiment driver on top of those records, computed on the host:
+calibrating the controller's thresholds from an unbounded run
+(``thresholds``), the paper's bounded-versus-unbounded experiment
+(``paper_experiment``, ``summarize``), per-run latency and throughput
+metrics (``run_metrics``) and the comparison of controller variants
+(``compare_controllers``).
 """
 from __future__ import annotations
 
