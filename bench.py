@@ -170,6 +170,33 @@ def summary(w, r, steps):
     }
 
 
+def gather_probe(tile_bytes, pool_bytes=4 << 30, reps=5, waves=(768, 1024, 1536)):
+    """The library's page-pattern gather probe over a pool of `pool_bytes`
+    (tiles of `tile_bytes` read once each, scattered), at a few wave counts
+    around one wave per SIMD (more waves than that read slower): GB/s of the
+    best launch, and its wave count; each count gets one warmup and `reps`
+    launches timed with events on the stream."""
+    import torch
+
+    import paper_2510_15330_amd as bl
+
+    pool = torch.empty(pool_bytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    best = (0.0, 0)
+    for mw in waves:
+        bl.probe_gather(pool, tile_bytes, sink, max_waves=mw)
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            bl.probe_gather(pool, tile_bytes, sink, max_waves=mw)
+            b.record()
+            torch.cuda.synchronize()
+            best = max(best, (pool_bytes / (a.elapsed_time(b) * 1e-3) / 1e9, mw))
+    del pool, sink
+    free_cuda()
+    return best
+
+
 def cpu_baseline(w, target_s=12.0, min_s=10.0):
     """The binary64 oracle on the first requests of the workload's first step,
     timed on this host; pages of the sampled requests are gathered on the
@@ -563,6 +590,20 @@ def main():
             f"-> {rs['kernel_gbs']:.1f} GB/s")
         del ws, rs
         free_cuda()
+
+        # the page pattern's ceiling on this machine: the same scattered 16-byte
+        # non-temporal loads with no arithmetic, bf16 (4 KiB) and fp8 (2 KiB)
+        # page tiles
+        (g4, w4), (g2, w2) = gather_probe(4096), gather_probe(2048)
+        result["gather_probe"] = {
+            "tile_4096_gbs": round(g4, 1), "tile_4096_waves": w4,
+            "tile_2048_gbs": round(g2, 1), "tile_2048_waves": w2,
+            "summarization_kernel_vs_probe": round(result["roofline"]["achieved"] / g4, 4),
+            "stress_fp8_kernel_vs_probe": round(result["stress_fp8"]["kernel_gbs"] / g2, 4),
+            "llama3_8b_kernel_vs_probe": round(result["llama3_8b"]["kernel_gbs"] / g4, 4),
+        }
+        result["roofline"]["frac_of_gather_probe"] = result["gather_probe"]["summarization_kernel_vs_probe"]
+        log(f"[bench] gather probe: {g4:.1f} GB/s (4 KiB tiles), {g2:.1f} GB/s (2 KiB tiles)")
 
         rp = measure_prefill("prefill_summarization", 20, 5)
         result["prefill_summarization"] = {

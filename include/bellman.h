@@ -569,6 +569,24 @@ int bellman_reserve_workspace(int64_t bytes);
  * outside the pool (page skipped). */
 int bellman_device_errors(void *stream, int32_t *flags);
 
+/*
+ * Diagnostic: the page-pattern ceiling.  Reads every tile of a device pool
+ * of pool_bytes once, n = pool_bytes / tile_bytes tiles (n a power of two,
+ * tile_bytes 2048, 4096 or 8192: an fp8 or bf16 KV page of one head at
+ * head_dim 128, or two), in a fixed scrambled order (a bijection of the
+ * tile indices built from odd multiplications and xor-shifts) that spreads
+ * each wave's consecutive tiles, and the tiles all waves read at one time,
+ * over the pool, as a batch's random pages are.  The loads are the decode kernel's (16 bytes a
+ * lane, non-temporal), with no arithmetic but an XOR of every 32-bit word
+ * into *sink, which the caller clears beforehand (the result is the XOR of
+ * the whole pool).  max_waves caps the waves (0 = every resident wave).  The
+ * bytes read over the kernel's time are the rate the attention kernel's page
+ * stream can reach on this device.  pool 16-byte aligned, sink 4-byte
+ * aligned; enqueues one kernel on `stream`.
+ */
+int bellman_probe_gather(const void *pool, int64_t pool_bytes, int32_t tile_bytes, int32_t max_waves,
+                         uint32_t *sink, void *stream);
+
 /* Synchronise every device that holds a workspace and free its blocks
  * (current and retired).  No call may be in flight, and graphs captured
  * with library calls must not be replayed afterwards. */

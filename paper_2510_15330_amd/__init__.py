@@ -21,6 +21,7 @@ from ._binding import (  # noqa: F401
     library,
     library_path,
     prefill_attention,
+    probe_gather,
     reserve_workspace,
     shutdown,
     version,

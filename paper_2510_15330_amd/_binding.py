@@ -107,6 +107,8 @@ def library():
     lib.bellman_decode_attention_noalloc.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                      ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_noalloc.restype = ctypes.c_int
+    lib.bellman_probe_gather.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P]
+    lib.bellman_probe_gather.restype = ctypes.c_int
     lib.bellman_kv_write.argtypes = [T, T, T, T, T, T, T, P]
     lib.bellman_kv_write.restype = ctypes.c_int
     lib.bellman_prefill_attention.argtypes = [T, T, T, T, T, T, ctypes.c_float, T, P]
@@ -249,6 +251,16 @@ def decode_attention_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, 
     _check(library().bellman_decode_attention_noalloc(
         desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table), desc(seq_lens),
         ctypes.c_float(scale), desc(out), ctypes.byref(opts), _stream(stream)))
+
+
+def probe_gather(pool, tile_bytes, sink, max_waves=0, stream=None):
+    """bellman_probe_gather: read every tile of the device buffer ``pool``
+    once in the decode kernels' scattered page pattern and XOR its words into
+    ``sink`` (a cleared device int32/uint32 tensor of one element)."""
+    _device_tensors(pool, sink)
+    _check(library().bellman_probe_gather(ctypes.c_void_p(pool.data_ptr()), pool.numel() * pool.element_size(),
+                                          int(tile_bytes), int(max_waves), ctypes.c_void_p(sink.data_ptr()),
+                                          _stream(stream)))
 
 
 def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, stream=None):

@@ -16,7 +16,7 @@ import tempfile
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libbellman.so")
-DEVICE_SOURCES = ["kernels.hip", "prefill.hip", "device_state.hip"]
+DEVICE_SOURCES = ["kernels.hip", "prefill.hip", "device_state.hip", "probe.hip"]
 HOST_SOURCES = ["bellman_api.cpp", "controller.cpp", "serve_sim.cpp"]
 SOURCES = DEVICE_SOURCES + HOST_SOURCES
 

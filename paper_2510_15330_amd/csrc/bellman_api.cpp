@@ -496,6 +496,33 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     return launch_status("kv_append");
 }
 
+int bellman_probe_gather(const void* pool, int64_t pool_bytes, int32_t tile_bytes, int32_t max_waves, uint32_t* sink,
+                         void* stream) {
+    g_last_error[0] = 0;
+    if (!pool || !sink) return fail(BELLMAN_ERR_INVALID_ARG, "pool and sink must be device pointers");
+    if (tile_bytes != 2048 && tile_bytes != 4096 && tile_bytes != 8192)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "tile_bytes %d not in {2048, 4096, 8192}", tile_bytes);
+    if (pool_bytes < tile_bytes || pool_bytes % tile_bytes)
+        return fail(BELLMAN_ERR_INVALID_ARG, "pool_bytes %lld is not a positive multiple of tile_bytes",
+                    (long long)pool_bytes);
+    const int64_t n = pool_bytes / tile_bytes;
+    if (n & (n - 1)) return fail(BELLMAN_ERR_INVALID_ARG, "pool_bytes / tile_bytes = %lld is not a power of two",
+                                 (long long)n);
+    if (!aligned(pool, 16) || !aligned(sink, 4))
+        return fail(BELLMAN_ERR_UNSUPPORTED, "pool must be 16-byte and sink 4-byte aligned");
+    if (max_waves < 0) return fail(BELLMAN_ERR_INVALID_ARG, "max_waves %d < 0", max_waves);
+    int dev, rc;
+    if ((rc = current_device(&dev))) return rc;
+    int cu = 0;
+    hipError_t e = hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess || cu < 1) return fail(BELLMAN_ERR_HIP, "multiprocessor count: %s", hipGetErrorString(e));
+    int64_t waves = (int64_t)cu * gather_probe_blocks_per_cu(tile_bytes) * 4;
+    if (max_waves > 0 && waves > max_waves) waves = max_waves;
+    if (waves > n) waves = n;
+    launch_gather_probe(pool, n, tile_bytes, (int)waves, sink, (hipStream_t)stream);
+    return launch_status("gather probe");
+}
+
 int bellman_decode_attention_opts(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
                                   const bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
                                   const bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,

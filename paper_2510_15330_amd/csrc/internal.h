@@ -123,6 +123,11 @@ void launch_merge(const AttnArgs& a, hipStream_t s);
 void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
 void launch_prefill(const PrefillArgs& a, hipStream_t s);
 
+// Page-pattern gather probe (probe.hip): n tiles of tile_bytes, n a power of
+// two; nonzero if tile_bytes is not a built size.
+int launch_gather_probe(const void* pool, int64_t n, int tile_bytes, int waves, uint32_t* sink, hipStream_t s);
+int gather_probe_blocks_per_cu(int tile_bytes);
+
 // Addresses of the current device's error word and fixed scratch array
 // (device_state.hip); dev must be the current device.  0 or a negative
 // bellman status.

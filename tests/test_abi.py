@@ -202,6 +202,26 @@ def test_prompt_write_rejects(B, name, mut, code, msg):
     assert msg in B.last_error()
 
 
+PROBE_CASES = [
+    ("null pool", dict(pool=None), ERR_INVALID, "device pointers"),
+    ("null sink", dict(sink=None), ERR_INVALID, "device pointers"),
+    ("tile size", dict(tile=1024), ERR_UNSUPPORTED, "tile_bytes"),
+    ("not a multiple", dict(nbytes=4096 * 3 + 8), ERR_INVALID, "multiple"),
+    ("not a power of two", dict(nbytes=4096 * 3), ERR_INVALID, "power of two"),
+    ("misaligned pool", dict(pool=FAKE + 8), ERR_UNSUPPORTED, "aligned"),
+    ("negative waves", dict(waves=-1), ERR_INVALID, "max_waves"),
+]
+
+
+@pytest.mark.parametrize("name,kw,code,msg", PROBE_CASES, ids=[c[0] for c in PROBE_CASES])
+def test_probe_rejects(B, name, kw, code, msg):
+    a = dict(pool=FAKE, nbytes=4096 * 4, tile=4096, waves=0, sink=FAKE)
+    a.update(kw)
+    rc = B.library().bellman_probe_gather(a["pool"], a["nbytes"], a["tile"], a["waves"], a["sink"], None)
+    assert rc == code
+    assert msg in B.last_error()
+
+
 def test_option_ranges(B):
     g = good(B)
     lib = B.library()
