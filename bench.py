@@ -170,7 +170,7 @@ def summary(w, r, steps):
     }
 
 
-def gather_probe(tile_bytes, pool_bytes=4 << 30, reps=5, waves=(768, 1024, 1536)):
+def gather_probe(tile_bytes, pool_bytes=4 << 30, reps=5, waves=(768, 1024, 2048)):
     """The library's page-pattern gather probe over a pool of `pool_bytes`
     (tiles of `tile_bytes` read once each, scattered), at a few wave counts
     around one wave per SIMD (more waves than that read slower): GB/s of the

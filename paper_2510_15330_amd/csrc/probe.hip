@@ -16,7 +16,7 @@ namespace {
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kProbeBlock = 256;
-constexpr int kProbeDepth = 2;          // tiles in flight per wave while it folds the previous two
+constexpr int kProbeDepth = 4;          // tiles in flight per wave while it folds the previous four
 constexpr uint64_t kProbeMul1 = 0x9E3779B97F4A7C15ull;   // odd multipliers: bijections mod 2^k
 constexpr uint64_t kProbeMul2 = 0xD6E8FEB86659FD93ull;
 
