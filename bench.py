@@ -114,6 +114,43 @@ def decode_run(w, steps, warmup, **kw):
                 kernel_gbs=attn_bytes.mean() / kt.mean() / 1e9, call_gbs=attn_bytes.mean() / ct.mean() / 1e9)
 
 
+def wave_times_run(w, step=0, **kw):
+    """One decode-attention call of `w` at its current lengths with the
+    library's per-wave timing records (the traced kernel): the span of the
+    kernel, how busy its waves keep it, and, per XCD (the id each wave read
+    from the hardware), the waves' mean busy time and mean and last end,
+    all in microseconds from the first wave's start."""
+    import torch
+
+    import paper_2510_15330_amd as bl
+
+    out = torch.empty((w.B, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
+    rec = torch.full((3 * 16384,), -1, dtype=torch.int64, device="cuda")
+    bl.decode_attention(w.q[step], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
+                        k_scale=w.k_scale, v_scale=w.v_scale, wave_times=rec, **kw)
+    torch.cuda.synchronize()
+    r = rec.view(-1, 3).cpu().numpy()
+    r = r[r[:, 0] >= 0]
+    W = len(r)
+    t0 = r[:, 0].min()
+    start, end = (r[:, 0] - t0) / 100.0, (r[:, 1] - t0) / 100.0      # 100 MHz clock -> us
+    xcc = (r[:, 2] >> 32) & 15
+    span = float(end.max())
+    per_xcd = {}
+    for x in sorted(set(int(v) for v in xcc)):
+        m = xcc == x
+        per_xcd[str(x)] = {"waves": int(m.sum()), "busy_us": round(float((end[m] - start[m]).mean()), 1),
+                           "end_us_mean": round(float(end[m].mean()), 1), "end_us_max": round(float(end[m].max()), 1)}
+    wave = np.arange(W)
+    return {
+        "waves": W, "span_us": round(span, 1),
+        "busy_frac": round(float((end - start).sum() / (W * span)), 4),
+        "last_start_us": round(float(start.max()), 1), "first_end_us": round(float(end.min()), 1),
+        "xcd_is_workgroup_mod_8": round(float((xcc == (wave // 4) % 8).mean()), 4),
+        "per_xcd": per_xcd,
+    }
+
+
 def graph_run(w, steps, reps=3):
     """The same `steps` decode steps captured in one HIP graph (after an
     eager run has grown the workspace) and replayed `reps` times from the
@@ -541,6 +578,12 @@ def main():
         }
         log(f"[bench] equal shares: attention kernel {e['kt'].mean() * 1e6:.1f} us avg")
         del e
+        # per-wave timing records of one call each way: with equal shares the
+        # waves of slower XCDs end later; the weighting evens the ends out
+        result["wave_times"] = {"equal_shares": wave_times_run(w, xcd_skew=-1), "default": wave_times_run(w)}
+        wt = result["wave_times"]
+        log(f"[bench] wave times: span {wt['equal_shares']['span_us']} us equal shares, "
+            f"{wt['default']['span_us']} us default; busy {wt['default']['busy_frac']}")
 
     if full:
         lens_u, info_u = wl.sample_lengths("summarization", 0)

@@ -170,6 +170,16 @@ typedef struct bellman_attn_opts {
                              the main attention kernel (profiling); NULL = none */
     void *event_end;      /* optional hipEvent_t recorded right after it (before the
                              merge of the cut requests) */
+    int64_t *wave_times;  /* optional device array of 3 * W int64 (W = the waves the
+                             call uses: every resident wave, or max_waves): wave w
+                             writes [3w] = the 100 MHz real-time clock when it
+                             starts, [3w+1] = the clock when it has written its
+                             last result, [3w+2] = (XCD id << 32) | HW_ID of its
+                             SIMD.  A timing record: the results are those of the
+                             untraced call.  Built for head_dim 128 at the default
+                             steps (bf16: pages_per_step 1 or 2 with
+                             pipeline_depth 2; fp8: 4 pages, depth 1); other
+                             shapes return BELLMAN_ERR_UNSUPPORTED.  NULL = none */
 } bellman_attn_opts_t;
 
 /* bellman_decode_attention with explicit tuning options (NULL = defaults).

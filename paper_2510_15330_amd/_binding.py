@@ -37,7 +37,8 @@ class Tensor(ctypes.Structure):
 class AttnOpts(ctypes.Structure):
     _fields_ = [("max_waves", ctypes.c_int32), ("xcd_skew", ctypes.c_int32),
                 ("pages_per_step", ctypes.c_int32), ("pipeline_depth", ctypes.c_int32),
-                ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p)]
+                ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p),
+                ("wave_times", ctypes.c_void_p)]
 
 
 class PrefillOpts(ctypes.Structure):
@@ -219,17 +220,20 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None
 
 def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
                      k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, events=None,
-                     pages_per_step=0, pipeline_depth=0):
+                     pages_per_step=0, pipeline_depth=0, wave_times=None):
     """bellman_decode_attention(_opts): one decode step over the paged cache.
 
     ``events`` is an optional pair of recorded-once torch.cuda.Event objects
     that the library records around its main attention kernel; ``xcd_skew``
-    is 0 (the library's choice), -1 (equal shares) or 1..255."""
-    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale)
+    is 0 (the library's choice), -1 (equal shares) or 1..255; ``wave_times``
+    an optional device int64 tensor of 3 entries per wave for the per-wave
+    timing records."""
+    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale, wave_times)
     lib = library()
     args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
             desc(seq_lens), ctypes.c_float(scale), desc(out))
-    if max_waves == 0 and xcd_skew == 0 and events is None and pages_per_step == 0 and pipeline_depth == 0:
+    if (max_waves == 0 and xcd_skew == 0 and events is None and pages_per_step == 0 and pipeline_depth == 0
+            and wave_times is None):
         _check(lib.bellman_decode_attention(*args, _stream(stream)))
     else:
         ev0 = ev1 = None
@@ -237,7 +241,8 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
             ev0, ev1 = events[0].cuda_event, events[1].cuda_event
             if not ev0 or not ev1:
                 raise ValueError("record each event once before passing it")
-        opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1)
+        wt = None if wave_times is None else wave_times.data_ptr()
+        opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1, wt)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 

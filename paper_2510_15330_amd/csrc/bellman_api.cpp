@@ -296,6 +296,11 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         const double table_pages_per_wave = (double)B * ps.H_kv * (double)max_pages / (double)w_est;
         pps = ps.fp8 ? 4 : (table_pages_per_wave < kShortSharePages ? 1 : 2);
     }
+    int64_t* wave_times = opts ? opts->wave_times : nullptr;
+    if (wave_times && !attention_traced(pps, depth, ps.fp8, ps.D))
+        return fail(BELLMAN_ERR_UNSUPPORTED,
+                    "wave_times: traced kernels are built for head_dim 128 at the default steps only");
+    if (wave_times && !aligned(wave_times, 8)) return fail(BELLMAN_ERR_UNSUPPORTED, "wave_times must be 8-byte aligned");
     int& bpc = g_blocks_per_cu[dev][ps.fp8][ps.D == 128][pps][depth];
     if (bpc == 0) {
         bpc = attention_blocks_per_cu(pps, depth, ps.fp8, ps.D);
@@ -362,6 +367,7 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     a.cuts = (int4*)(base + off_cuts);
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
+    a.wave_times = wave_times;
 
     hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
     hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;

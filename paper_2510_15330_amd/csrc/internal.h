@@ -74,6 +74,7 @@ struct AttnArgs {
     float2* part_ml;     // [2 * waves * G]: (running max in log2 units, sum) of each wave's two
                          // partial pieces (the request cut at its range's start, and at its end)
     float* part_o;       // [2 * waves * G * D]
+    int64_t* wave_times; // optional [3 * waves] per-wave timing records (traced kernel), else null
 };
 
 // Prompt KV write (prefill.hip).
@@ -116,6 +117,8 @@ struct PrefillArgs {
 // hipGetLastError in the caller.
 void launch_kv_append(const AppendArgs& a, hipStream_t s);
 void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s);
+// Whether the attention kernel variant has a traced twin (wave_times).
+bool attention_traced(int pages_per_step, int depth, bool fp8, int D);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 void launch_merge(const AttnArgs& a, hipStream_t s);

@@ -805,11 +805,22 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1
     cursor_len<PP>(c);
 }
 
+// The hardware registers a traced wave records (s_getreg_b32 operands:
+// register id, bit offset 0, field width): the XCD it runs on, and its
+// wave / SIMD / CU / shader-engine ids.
+constexpr int kHwRegXccId = 20 | (3 << 11);    // XCC_ID, bits 3:0
+constexpr int kHwRegHwId = 4 | (31 << 11);     // HW_ID, bits 31:0
+
 // DEPTH steps of PP pages are in flight per wave while it computes one.  With
 // DEPTH = 1 two waves share each SIMD; with DEPTH = 2 each SIMD runs one wave
 // (its issue is not arbitrated against a second, older wave, which otherwise
 // runs ahead and leaves the younger one to finish alone).
-template <int D, bool FP8, int PP, int DEPTH>
+//
+// TRACE: each wave also records, in a.wave_times[3w .. 3w + 2], the
+// real-time clock (100 MHz) when it starts and when it has written its last
+// result, and (XCD id << 32) | HW_ID: a timing record, not a change of the
+// computation.
+template <int D, bool FP8, int PP, int DEPTH, bool TRACE>
 __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu(DEPTH == 1 ? 2 : 1, DEPTH == 1 ? 2 : 1)))
 attn_mfma_kernel(AttnArgs a) {
     constexpr int NT = D / 16;
@@ -821,6 +832,20 @@ attn_mfma_kernel(AttnArgs a) {
     // wave index, made provably uniform so that all stream bookkeeping is scalar
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kAttnBlock / kWaveSize) + (threadIdx.x >> 6));
     if (w >= a.waves) return;
+    uint64_t t_start = 0;
+    if constexpr (TRACE) t_start = __builtin_amdgcn_s_memrealtime();
+    auto trace_end = [&]() {
+        if constexpr (TRACE) {
+            const uint64_t t_end = __builtin_amdgcn_s_memrealtime();
+            const uint64_t ids = ((uint64_t)(__builtin_amdgcn_s_getreg(kHwRegXccId) & 15) << 32) |
+                                 (uint32_t)__builtin_amdgcn_s_getreg(kHwRegHwId);
+            if (lane == 0) {
+                a.wave_times[3 * (int64_t)w] = (int64_t)t_start;
+                a.wave_times[3 * (int64_t)w + 1] = (int64_t)t_end;
+                a.wave_times[3 * (int64_t)w + 2] = (int64_t)ids;
+            }
+        }
+    };
 
     // This wave's range of the P units (see the work split above).  Lane l
     // holds requests b0 + 16 l .. b0 + 16 l + 15 of each batch of lengths, so
@@ -878,6 +903,7 @@ attn_mfma_kernel(AttnArgs a) {
     if (w == 0 && __any(bad_len) && lane == 0) atomicOr(a.err, kErrLength);
     if (r0 >= r1) {
         if (lane == 0) a.cuts[w] = make_int4(-1, 0, 0, 0);
+        trace_end();
         return;
     }
     int sb = -1, sg = 0, sp = 0, sL = 0;   // request, KV head, page, length at unit r0
@@ -1145,6 +1171,7 @@ attn_mfma_kernel(AttnArgs a) {
         const int wl = cut ? wave_of(ex0 + en - 1, P, a.waves, skew) : 0;
         a.cuts[w] = cut ? make_int4(e.b, e.g, wl, P) : make_int4(-1, 0, 0, 0);
     }
+    trace_end();
 }
 
 // One wave per attention wave w: if w's range ended inside a (request, head)
@@ -1179,15 +1206,26 @@ void launch_kv_append(const AppendArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(kv_append_kernel, dim3(a.B), dim3(256), 0, s, a);
 }
 
+// The shapes built with a traced twin: head_dim 128 at the library's default
+// steps (bf16: one or two pages, depth 2; fp8: four pages, depth 1).
+template <int D, bool FP8, int PP, int DEPTH>
+constexpr bool kTraced = D == 128 && (FP8 ? (PP == 4 && DEPTH == 1) : (PP <= 2 && DEPTH == 2));
+
 template <int D, bool FP8, int PP, int DEPTH>
 struct Variant {
     static void launch(const AttnArgs& a, int grid, hipStream_t s) {
-        hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH>), dim3(grid), dim3(kAttnBlock), 0, s, a);
+        if constexpr (kTraced<D, FP8, PP, DEPTH>) {
+            if (a.wave_times) {
+                hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, true>), dim3(grid), dim3(kAttnBlock), 0, s, a);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, false>), dim3(grid), dim3(kAttnBlock), 0, s, a);
     }
     static int occupancy() {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<D, FP8, PP, DEPTH>, kAttnBlock, 0) !=
-                hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<D, FP8, PP, DEPTH, false>, kAttnBlock,
+                                                         0) != hipSuccess ||
             nb < 1)
             nb = 1;
         return nb;
@@ -1226,6 +1264,11 @@ static int dispatch(int D, bool fp8, int pp, int depth, bool occ, const AttnArgs
 void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s) {
     if (a.B == 0 || a.H_q == 0) return;
     dispatch(a.D, fp8, pages_per_step, depth, false, &a, grid, s);
+}
+
+bool attention_traced(int pages_per_step, int depth, bool fp8, int D) {
+    if (D != 128) return false;
+    return fp8 ? (pages_per_step == 4 && depth == 1) : (pages_per_step <= 2 && depth == 2);
 }
 
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D) {
