@@ -131,7 +131,6 @@ def wave_times_run(w, step=0, **kw):
     torch.cuda.synchronize()
     r = rec.view(-1, 3).cpu().numpy()
     r = r[r[:, 0] >= 0]
-    records = r.copy()
     W = len(r)
     t0 = r[:, 0].min()
     start, end = (r[:, 0] - t0) / 100.0, (r[:, 1] - t0) / 100.0      # 100 MHz clock -> us
@@ -149,7 +148,7 @@ def wave_times_run(w, step=0, **kw):
         "last_start_us": round(float(start.max()), 1), "first_end_us": round(float(end.min()), 1),
         "xcd_is_workgroup_mod_8": round(float((xcc == (wave // 4) % 8).mean()), 4),
         "per_xcd": per_xcd,
-    }, records
+    }
 
 
 def graph_run(w, steps, reps=3):
@@ -581,22 +580,10 @@ def main():
         del e
         # per-wave timing records of one call each way: with equal shares the
         # waves of slower XCDs end later; the weighting evens the ends out
-        eq_stats, eq_records = wave_times_run(w, xcd_skew=-1)
-        result["wave_times"] = {"equal_shares": eq_stats, "default": wave_times_run(w)[0]}
+        result["wave_times"] = {"equal_shares": wave_times_run(w, xcd_skew=-1), "default": wave_times_run(w)}
         wt = result["wave_times"]
         log(f"[bench] wave times: span {wt['equal_shares']['span_us']} us equal shares, "
             f"{wt['default']['span_us']} us default; busy {wt['default']['busy_frac']}")
-        # per-XCD weights calibrated from the equal-shares records, then timed
-        # like the default run (the library's calibration entry point)
-        xw = [int(v) for v in bl.xcd_weights_from_times(eq_records)]
-        cw = decode_run(w, steps, args.warmup, **dict(knobs, xcd_weights=xw))
-        result["xcd_calibrated"] = {
-            "weights": xw, "kernel_us_mean": round(cw["kt"].mean() * 1e6, 2),
-            "vs_default": round(float(cw["kt"].mean() / r["kt"].mean()), 4),
-            "wave_times": wave_times_run(w, xcd_weights=xw)[0],
-        }
-        log(f"[bench] calibrated XCD weights {xw}: attention kernel {cw['kt'].mean() * 1e6:.1f} us avg")
-        del cw
 
     if full:
         lens_u, info_u = wl.sample_lengths("summarization", 0)

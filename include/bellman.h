@@ -180,13 +180,6 @@ typedef struct bellman_attn_opts {
                              steps (bf16: pages_per_step 1 or 2 with
                              pipeline_depth 2; fp8: 4 pages, depth 1); other
                              shapes return BELLMAN_ERR_UNSUPPORTED.  NULL = none */
-    const int32_t *xcd_weights; /* optional host array of 8 share weights, 1..1023,
-                                   one per XCD (workgroup i runs on XCD i mod 8):
-                                   on long shares (every wave at least 256 steps)
-                                   the waves of XCD x take shares proportional
-                                   to xcd_weights[x]; replaces xcd_skew.  From
-                                   bellman_xcd_weights_from_times.  NULL = none.
-                                   Results agree within rounding. */
 } bellman_attn_opts_t;
 
 /* bellman_decode_attention with explicit tuning options (NULL = defaults).
@@ -585,17 +578,6 @@ int bellman_reserve_workspace(int64_t bytes);
  * range, 4 = a block-table entry
  * outside the pool (page skipped). */
 int bellman_device_errors(void *stream, int32_t *flags);
-
-/*
- * Per-XCD share weights from the timing records (opts.wave_times, copied to
- * the host) of one decode-attention call made with equal shares
- * (xcd_skew = -1): each XCD's weight is 256 times the mean busy time over
- * all XCDs divided by its own waves' mean busy time (end - start), clamped
- * to 128..512, so that on a call of the same shape every XCD's waves would
- * end together.  XCDs with no record get 256.  records: 3 * waves int64 as
- * the traced kernel writes them; weights: 8 int32 out.
- */
-int bellman_xcd_weights_from_times(const int64_t *records, int32_t waves, int32_t *weights);
 
 /*
  * Diagnostic: the page-pattern ceiling.  Reads every tile of a device pool

@@ -25,5 +25,4 @@ from ._binding import (  # noqa: F401
     reserve_workspace,
     shutdown,
     version,
-    xcd_weights_from_times,
 )

@@ -38,7 +38,7 @@ class AttnOpts(ctypes.Structure):
     _fields_ = [("max_waves", ctypes.c_int32), ("xcd_skew", ctypes.c_int32),
                 ("pages_per_step", ctypes.c_int32), ("pipeline_depth", ctypes.c_int32),
                 ("event_begin", ctypes.c_void_p), ("event_end", ctypes.c_void_p),
-                ("wave_times", ctypes.c_void_p), ("xcd_weights", ctypes.POINTER(ctypes.c_int32))]
+                ("wave_times", ctypes.c_void_p)]
 
 
 class PrefillOpts(ctypes.Structure):
@@ -108,8 +108,6 @@ def library():
     lib.bellman_decode_attention_noalloc.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                      ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_noalloc.restype = ctypes.c_int
-    lib.bellman_xcd_weights_from_times.argtypes = [P, ctypes.c_int32, P]
-    lib.bellman_xcd_weights_from_times.restype = ctypes.c_int
     lib.bellman_probe_gather.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P]
     lib.bellman_probe_gather.restype = ctypes.c_int
     lib.bellman_kv_write.argtypes = [T, T, T, T, T, T, T, P]
@@ -220,19 +218,9 @@ def kv_append(k_new, v_new, k_pages, v_pages, block_table, seq_lens, stream=None
                                  desc(block_table), desc(seq_lens), _stream(stream)))
 
 
-def xcd_weights_from_times(records):
-    """bellman_xcd_weights_from_times: eight share weights from the host copy
-    (int64 numpy array of 3 per wave) of an equal-shares call's records."""
-    import numpy as np
-    r = np.ascontiguousarray(records, dtype=np.int64)
-    out = np.zeros(8, dtype=np.int32)
-    _check(library().bellman_xcd_weights_from_times(r.ctypes.data, len(r) // 3, out.ctypes.data))
-    return out
-
-
 def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
                      k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, events=None,
-                     pages_per_step=0, pipeline_depth=0, wave_times=None, xcd_weights=None):
+                     pages_per_step=0, pipeline_depth=0, wave_times=None):
     """bellman_decode_attention(_opts): one decode step over the paged cache.
 
     ``events`` is an optional pair of recorded-once torch.cuda.Event objects
@@ -245,7 +233,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
     args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
             desc(seq_lens), ctypes.c_float(scale), desc(out))
     if (max_waves == 0 and xcd_skew == 0 and events is None and pages_per_step == 0 and pipeline_depth == 0
-            and wave_times is None and xcd_weights is None):
+            and wave_times is None):
         _check(lib.bellman_decode_attention(*args, _stream(stream)))
     else:
         ev0 = ev1 = None
@@ -254,11 +242,7 @@ def decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, str
             if not ev0 or not ev1:
                 raise ValueError("record each event once before passing it")
         wt = None if wave_times is None else wave_times.data_ptr()
-        xw = None
-        if xcd_weights is not None:
-            xw = (ctypes.c_int32 * 8)(*[int(v) for v in xcd_weights])
-        opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1, wt,
-                        None if xw is None else ctypes.cast(xw, ctypes.POINTER(ctypes.c_int32)))
+        opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1, wt)
         _check(lib.bellman_decode_attention_opts(*args, ctypes.byref(opts), _stream(stream)))
 
 

@@ -272,11 +272,6 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
             return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step %d not in {0, 1, 2, 4}", pps);
         if (skew_opt < -1 || skew_opt > kMaxSkew)
             return fail(BELLMAN_ERR_INVALID_ARG, "xcd_skew %d not in [-1, %d]", skew_opt, kMaxSkew);
-        if (opts->xcd_weights)
-            for (int i = 0; i < kNumXcds; ++i)
-                if (opts->xcd_weights[i] < 1 || opts->xcd_weights[i] > kMaxXcdWeight)
-                    return fail(BELLMAN_ERR_INVALID_ARG, "xcd_weights[%d] = %d not in [1, %d]", i,
-                                opts->xcd_weights[i], kMaxXcdWeight);
     }
     if (pps == 4 && !ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "pages_per_step 4 is built for fp8 pools only");
     if (depth == 0) depth = ps.fp8 ? 1 : 2;  // measured: fp8 steps compute more per byte
@@ -366,13 +361,8 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     // The default XCD weights were measured on a whole MI355X (256 CUs,
     // workgroup i on XCD i mod 8) with one workgroup per CU; partitioned
     // devices and two workgroups per CU (depth 1) keep equal shares.
-    if (opts && opts->xcd_weights) {
-        for (int i = 0; i < kNumXcds; ++i) a.xw.w[i] = opts->xcd_weights[i];
-    } else if (skew_opt == 0) {
-        a.xw = skew_weights((bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0);
-    } else {
-        a.xw = skew_weights(skew_opt < 0 ? 0 : skew_opt);
-    }
+    if (skew_opt == 0) a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
+    else a.skew = skew_opt < 0 ? 0 : skew_opt;
     a.err = err;
     a.cuts = (int4*)(base + off_cuts);
     a.part_ml = (float2*)(base + off_ml);
@@ -510,37 +500,6 @@ int bellman_kv_append(const bellman_tensor_t* k_new, const bellman_tensor_t* v_n
     a.quant = quant ? 1 : 0;
     launch_kv_append(a, (hipStream_t)stream);
     return launch_status("kv_append");
-}
-
-int bellman_xcd_weights_from_times(const int64_t* records, int32_t waves, int32_t* weights) {
-    g_last_error[0] = 0;
-    if (!records || !weights) return fail(BELLMAN_ERR_INVALID_ARG, "records and weights must be host arrays");
-    if (waves < 1) return fail(BELLMAN_ERR_INVALID_ARG, "waves %d < 1", waves);
-    double busy[kNumXcds] = {0};
-    int64_t count[kNumXcds] = {0};
-    for (int32_t w = 0; w < waves; ++w) {
-        const int64_t t0 = records[3 * (int64_t)w], t1 = records[3 * (int64_t)w + 1];
-        const int x = (int)((records[3 * (int64_t)w + 2] >> 32) & 15);
-        if (t0 < 0 || t1 < t0 || x >= kNumXcds) return fail(BELLMAN_ERR_INVALID_ARG, "record %d is not a timing record", w);
-        busy[x] += (double)(t1 - t0);
-        ++count[x];
-    }
-    double mean_all = 0;
-    int seen = 0;
-    for (int x = 0; x < kNumXcds; ++x)
-        if (count[x] > 0 && busy[x] > 0) {
-            busy[x] /= (double)count[x];
-            mean_all += busy[x];
-            ++seen;
-        }
-    if (seen == 0) return fail(BELLMAN_ERR_INVALID_ARG, "no wave was busy");
-    mean_all /= seen;
-    for (int x = 0; x < kNumXcds; ++x) {
-        double v = (count[x] > 0 && busy[x] > 0) ? 256.0 * mean_all / busy[x] : 256.0;
-        v = v < 128.0 ? 128.0 : (v > 512.0 ? 512.0 : v);
-        weights[x] = (int32_t)lround(v);
-    }
-    return BELLMAN_OK;
 }
 
 int bellman_probe_gather(const void* pool, int64_t pool_bytes, int32_t tile_bytes, int32_t max_waves, uint32_t* sink,

@@ -5,7 +5,6 @@
 #include <stdint.h>
 
 #include "../../include/bellman.h"
-#include "work_split.h"
 
 namespace bellman {
 
@@ -65,7 +64,8 @@ struct AttnArgs {
     int B, H_q, H_kv, G, D, max_pages;
     int waves;           // waves sharing the flattened step stream (the grid's waves)
     int pp;              // pages per step of the launched attention kernel
-    XcdWeights xw;       // share weights of each XCD's waves on long shares (work_split.h)
+    int skew;            // share weights 256 + skew (even-XCD workgroups) / 256 - skew on long shares; 0..255
+                         // (work_split.h)
     int32_t* err;        // the device's error word
     // workspace
     int4* cuts;          // [waves]: (request, KV head, last wave, units) of the (request, head) in

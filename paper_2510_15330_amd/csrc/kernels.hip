@@ -707,14 +707,14 @@ struct MergeAcc {
             for (int t = 0; t < NT; ++t) o[j][t] = *(const f32x4*)(a.part_o + slot * D + 16 * t + 4 * qg);
         }
     }
-    __device__ __forceinline__ void fold_waves(const AttnArgs& a, int wf, int wl, int P, const XcdWeights& xw, int nh, int qg,
+    __device__ __forceinline__ void fold_waves(const AttnArgs& a, int wf, int wl, int P, int skew, int nh, int qg,
                                                float2 (&ml0)[2], f32x4 (&o0)[2][NT]) {
         const int W = a.waves;
         // every wave holds units when the lightest weight's share of P is
         // above one unit: (256 - k) P > C(W), C(W) <= (256 + k) W
-        const bool all_units = every_wave_holds_units(P, W, xw);
+        const bool all_units = (int64_t)(256 - skew) * P > (int64_t)(256 + skew) * W;
         auto has_units = [&](int v) {
-            return v <= wl && (all_units || share_bound(v, P, W, xw) < share_bound(v + 1, P, W, xw));
+            return v <= wl && (all_units || share_bound(v, P, W, skew) < share_bound(v + 1, P, W, skew));
         };
         {
             const bool live[2] = {has_units(wf), has_units(wf + 1)};
@@ -896,9 +896,9 @@ attn_mfma_kernel(AttnArgs a) {
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
         zero_empty(b0);
     }
-    const XcdWeights xw = weights_in_force(a.xw, P, a.waves);
-    const int r0 = share_bound(w, P, a.waves, xw);
-    const int r1 = share_bound(w + 1, P, a.waves, xw);
+    const int skew = share_skew(a.skew, P, a.waves);
+    const int r0 = share_bound(w, P, a.waves, skew);
+    const int r1 = share_bound(w + 1, P, a.waves, skew);
     // wave 0 raises the length flag
     if (w == 0 && __any(bad_len) && lane == 0) atomicOr(a.err, kErrLength);
     if (r0 >= r1) {
@@ -1168,7 +1168,7 @@ attn_mfma_kernel(AttnArgs a) {
     const int en = (e.np + PP - 1) / PP;
     if (lane == 0) {
         const bool cut = ex0 >= r0 && ex0 + en > r1;
-        const int wl = cut ? wave_of(ex0 + en - 1, P, a.waves, xw) : 0;
+        const int wl = cut ? wave_of(ex0 + en - 1, P, a.waves, skew) : 0;
         a.cuts[w] = cut ? make_int4(e.b, e.g, wl, P) : make_int4(-1, 0, 0, 0);
     }
     trace_end();
@@ -1193,7 +1193,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int b = __builtin_amdgcn_readfirstlane(c.x), g = __builtin_amdgcn_readfirstlane(c.y);
     const int wl = __builtin_amdgcn_readfirstlane(c.z), P = __builtin_amdgcn_readfirstlane(c.w);
     MergeAcc<D> m;
-    m.fold_waves(a, w, wl, P, weights_in_force(a.xw, P, a.waves), nh, qg, ml0, o0);
+    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), nh, qg, ml0, o0);
     if (n < a.G) m.store(a, b, g * a.G + n, qg);
 }
 

@@ -11,13 +11,14 @@
 // (request, head) covers its pages [j*PP, min((j+1)*PP, pages)).  Wave w of
 // W takes units [share_bound(w), share_bound(w + 1)).
 //
-// Shares by weight.  Workgroup i runs on XCD i mod 8 (four waves a
-// workgroup), and the XCDs stream at measurably different rates.  Wave w
-// weighs the weight of its XCD, x(w) = (w / 4) mod 8, and its range starts at
-// unit floor(C(w) P / C(W)), C the cumulative weight (equal weights:
-// [floor(w P / W), floor((w + 1) P / W))).  Weights apply only to long shares
-// (at least kSkewMinSteps steps a wave), where the rate difference, not the
-// ramp, sets the finish.
+// Shares by weight.  Workgroup i runs on XCD i mod 8, and waves on the
+// odd-numbered XCDs were measured to stream 4-5% slower than those on the
+// even ones; with skew k the waves of even-XCD workgroups (w / 4 even) weigh
+// 256 + k and the others 256 - k, and wave w's range starts at unit
+// floor(C(w) P / C(W)), C the cumulative weight (k = 0: equal shares
+// [floor(w P / W), floor((w + 1) P / W))).  The skew applies only to long
+// shares (at least kSkewMinSteps steps a wave), where the rate difference,
+// not the ramp, sets the finish.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -25,89 +26,37 @@
 
 namespace bellman {
 
-constexpr int kSkewMinSteps = 256;   // steps a wave from which the weights apply
-constexpr int kMaxSkew = 255;        // even/odd weights 256 +- k stay positive
-constexpr int kNumXcds = 8;
-constexpr int kMaxXcdWeight = 1023;  // weights 1 .. 1023: C(W) P stays below 2^63
+constexpr int kSkewMinSteps = 256;   // steps a wave from which the skew applies
+constexpr int kMaxSkew = 255;        // weights stay positive
 
-// The share weight of each XCD's waves.
-struct XcdWeights {
-    int w[kNumXcds];
-};
-
-// Even-numbered XCDs 256 + k, odd-numbered 256 - k (k = 0: equal shares).
-__host__ __device__ inline XcdWeights skew_weights(int k) {
-    XcdWeights x;
-    for (int i = 0; i < kNumXcds; ++i) x.w[i] = (i & 1) ? 256 - k : 256 + k;
-    return x;
+// The skew in force for P units over W waves.
+__host__ __device__ inline int share_skew(int skew, int P, int W) {
+    return (int64_t)P >= (int64_t)kSkewMinSteps * W ? skew : 0;
 }
 
-// The weights in force for P units over W waves: `x` on long shares, equal
-// ones otherwise.
-__host__ __device__ inline XcdWeights weights_in_force(const XcdWeights& x, int P, int W) {
-    return (int64_t)P >= (int64_t)kSkewMinSteps * W ? x : skew_weights(0);
+// C(w): summed weight of waves 0 .. w-1 (period of 8 waves: 4 of an
+// even-XCD workgroup, then 4 of an odd one).
+__host__ __device__ inline int64_t share_weight(int w, int skew) {
+    const int64_t a = 256 + skew, b = 256 - skew;
+    const int r = w & 7;
+    return (int64_t)(w >> 3) * 4 * (a + b) + (r <= 4 ? r * a : 4 * a + (r - 4) * b);
 }
 
-// Sum of the weights of XCDs 0 .. n-1 (constant indices only, so that device
-// code keeps the weights in scalar registers).
-__host__ __device__ inline int64_t weight_prefix(const XcdWeights& x, int n) {
-    int64_t s = 0;
-#pragma unroll
-    for (int i = 0; i < kNumXcds; ++i) s += i < n ? x.w[i] : 0;
-    return s;
-}
-__host__ __device__ inline int weight_of(const XcdWeights& x, int i) {
-    int v = x.w[0];
-#pragma unroll
-    for (int j = 1; j < kNumXcds; ++j) v = i == j ? x.w[j] : v;
-    return v;
-}
-
-// C(w): summed weight of waves 0 .. w-1.  A period of 32 waves (eight
-// workgroups of four) weighs 4 S, S the sum of the weights.
-__host__ __device__ inline int64_t share_weight(int w, const XcdWeights& x) {
-    const int q = w >> 5, r = w & 31, i = r >> 2, j = r & 3;
-    return (int64_t)q * 4 * weight_prefix(x, kNumXcds) + 4 * weight_prefix(x, i) + (int64_t)j * weight_of(x, i);
-}
-
-// First unit of wave w (w = W gives P).  C(W) <= 1023 W and P < 2^31, so the
+// First unit of wave w (w = W gives P).  C(W) <= 2^9 W and P < 2^31, so the
 // product stays below 2^63 for any W < 2^22.
-__host__ __device__ inline int share_bound(int w, int P, int W, const XcdWeights& x) {
-    return (int)(share_weight(w, x) * P / share_weight(W, x));
+__host__ __device__ inline int share_bound(int w, int P, int W, int skew) {
+    return (int)(share_weight(w, skew) * P / share_weight(W, skew));
 }
 
-// The wave v with share_bound(v) <= u < share_bound(v + 1), for 0 <= u < P:
-// the largest v whose start is at most u, i.e. the largest v with
-// C(v) P < (u + 1) C(W), i.e. C(v) <= c = floor(((u + 1) C(W) - 1) / P).
-__host__ __device__ inline int wave_of(int u, int P, int W, const XcdWeights& x) {
-    const int64_t c = ((int64_t)(u + 1) * share_weight(W, x) - 1) / P;   // largest admissible C(v)
-    const int64_t period = 4 * weight_prefix(x, kNumXcds);
-    const int64_t q = c / period;
-    int64_t rem = c - q * period;
-    int64_t v = 32 * q + 31;
-    bool found = false;
-#pragma unroll
-    for (int i = 0; i < kNumXcds; ++i) {
-        const int64_t seg = 4 * (int64_t)x.w[i];
-        if (!found && rem < seg) {
-            v = 32 * q + 4 * i + rem / x.w[i];
-            found = true;
-        }
-        if (!found) rem -= seg;
-    }
+// The wave v with share_bound(v) <= x < share_bound(v + 1), for 0 <= x < P:
+// the largest v whose start is at most x, i.e. the largest v with
+// C(v) P < (x + 1) C(W).
+__host__ __device__ inline int wave_of(int x, int P, int W, int skew) {
+    const int64_t a = 256 + skew, b = 256 - skew;
+    const int64_t c = ((int64_t)(x + 1) * share_weight(W, skew) - 1) / P;   // largest admissible C(v)
+    const int64_t q = c / (4 * (a + b)), rem = c - q * 4 * (a + b);
+    const int64_t v = 8 * q + (rem <= 4 * a ? rem / a : 4 + (rem - 4 * a) / b);
     return (int)(v < (int64_t)W - 1 ? v : (int64_t)W - 1);
-}
-
-// Whether every wave holds at least one unit: the lightest wave's share
-// exceeds one unit, since C(W) <= (heaviest weight) W.
-__host__ __device__ inline bool every_wave_holds_units(int P, int W, const XcdWeights& x) {
-    int lo = x.w[0], hi = x.w[0];
-#pragma unroll
-    for (int i = 1; i < kNumXcds; ++i) {
-        lo = x.w[i] < lo ? x.w[i] : lo;
-        hi = x.w[i] > hi ? x.w[i] : hi;
-    }
-    return (int64_t)lo * P > (int64_t)hi * W;
 }
 
 }  // namespace bellman

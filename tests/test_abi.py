@@ -243,38 +243,6 @@ def test_option_ranges(B):
     rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
                                            ctypes.byref(opts), None)
     assert rc == ERR_UNSUPPORTED and "pipeline_depth" in B.last_error()
-    for bad in ([0] + [256] * 7, [256] * 7 + [1024]):
-        xw = (ctypes.c_int32 * 8)(*bad)
-        opts = B.AttnOpts(0, 0, 0, 0, None, None, None, ctypes.cast(xw, ctypes.POINTER(ctypes.c_int32)))
-        rc = lib.bellman_decode_attention_opts(g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
-                                               ctypes.byref(opts), None)
-        assert rc == ERR_INVALID and "xcd_weights" in B.last_error()
-
-
-def test_xcd_weights_from_times(B):
-    """Weights that even out the XCDs' ends: inversely proportional to each
-    XCD's mean busy time, 256 at the mean, clamped to 128..512."""
-    import numpy as np
-    busy = [1400, 1466, 1427, 1514, 1425, 1517, 1384, 1464]     # per XCD, one equal-shares call
-    rec = []
-    for w in range(1024):
-        x = (w // 4) % 8
-        start = 1000 + (w % 3)
-        rec += [start, start + busy[x] * 100 + (w % 5), (x << 32) | 0x1234]
-    got = B.xcd_weights_from_times(np.array(rec, dtype=np.int64))
-    mean = np.mean([np.mean([busy[x] * 100 + (w % 5) for w in range(1024) if (w // 4) % 8 == x]) for x in range(8)])
-    for x in range(8):
-        mb = np.mean([busy[x] * 100 + (w % 5) for w in range(1024) if (w // 4) % 8 == x])
-        assert got[x] == int(np.floor(256 * mean / mb + 0.5))
-    assert got[6] > got[0] > got[1] > got[5]
-    # clamping, an XCD with no record, and malformed records
-    rec = np.array([0, 100, 0 << 32, 0, 1000, 1 << 32, 0, 10, 2 << 32], dtype=np.int64)
-    got = B.xcd_weights_from_times(rec)
-    assert got[0] == 256 * 370 // 100 or got[0] > 0
-    assert list(got[3:]) == [256] * 5
-    assert got[1] == 128 and got[2] == 512
-    with pytest.raises(B.BellmanError):
-        B.xcd_weights_from_times(np.array([5, 3, 0], dtype=np.int64))
 
 
 def test_controller_rejects(B):
