@@ -303,16 +303,16 @@ def cpu_baseline(w, target_s=12.0, min_s=10.0):
     }
 
 
-def measure_prefill(name, steps, warmup, seed=0):
+def measure_prefill(name, steps, warmup, seed=0, kv="bf16"):
     """Prompt path: a step restores the cached lengths (one small copy), writes
     the batch's keys and values into their pages and runs causal prompt
-    attention over the cache."""
+    attention over the cache (bf16 pools, or fp8 codes with their scales)."""
     import torch
 
     import paper_2510_15330_amd as bl
     from paper_2510_15330_amd import workloads as wl
 
-    w = wl.build_prefill(name, seed=seed, device="cuda")
+    w = wl.build_prefill(name, seed=seed, device="cuda", kv=kv)
     out = torch.empty((w.T, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
     lens0 = w.seq_lens.clone()
     stream = torch.cuda.current_stream()
@@ -321,7 +321,7 @@ def measure_prefill(name, steps, warmup, seed=0):
         w.seq_lens.copy_(lens0)
         bl.kv_write(w.k_new, w.v_new, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, stream=stream)
         bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out,
-                             stream=stream, events=events)
+                             stream=stream, events=events, k_scale=w.k_scale, v_scale=w.v_scale)
 
     for _ in range(warmup):
         step()
@@ -357,8 +357,13 @@ def cpu_baseline_prefill(w, target_s=12.0):
     import oracle
 
     lib = oracle.load()
-    kp = w.k_pages.cpu().view(torch.int16).numpy().view(np.uint16)
-    vp = w.v_pages.cpu().view(torch.int16).numpy().view(np.uint16)
+    fp8 = w.kv == "fp8"
+    if fp8:
+        kp, vp = w.k_pages.cpu().numpy(), w.v_pages.cpu().numpy()
+        ks0, vs0 = w.k_scale[:1].cpu().numpy(), w.v_scale[:1].cpu().numpy()
+    else:
+        kp = w.k_pages.cpu().view(torch.int16).numpy().view(np.uint16)
+        vp = w.v_pages.cpu().view(torch.int16).numpy().view(np.uint16)
     bt0 = w.block_table[:1].cpu().numpy()
     rng = np.random.default_rng(0)
     n0 = int(w.new[0])
@@ -369,7 +374,10 @@ def cpu_baseline_prefill(w, target_s=12.0):
         qb = w.q[torch.from_numpy(rows).cuda()].cpu().view(torch.int16).numpy().view(np.uint16)
         bt = np.repeat(bt0, k, axis=0)
         t = time.perf_counter()
-        oracle.prefill_attention(qb, kp, vp, bt, lens, np.arange(k + 1, dtype=np.int32), w.scale, lib=lib)
+        kw = {}
+        if fp8:
+            kw = dict(kv_dtype=oracle.FP8_E4M3FN, k_scale=np.repeat(ks0, k, axis=0), v_scale=np.repeat(vs0, k, axis=0))
+        oracle.prefill_attention(qb, kp, vp, bt, lens, np.arange(k + 1, dtype=np.int32), w.scale, lib=lib, **kw)
         return time.perf_counter() - t, int(lens.sum())
 
     dt, _ = run(8)
@@ -389,8 +397,8 @@ def cpu_baseline_prefill(w, target_s=12.0):
 
 def main_prefill(args):
     steps = args.steps if args.steps is not None else 20
-    log(f"[bench] {args.workload}: {steps} steps after {args.warmup} warmup")
-    r = measure_prefill(args.workload, steps, args.warmup)
+    log(f"[bench] {args.workload} ({args.kv} pools): {steps} steps after {args.warmup} warmup")
+    r = measure_prefill(args.workload, steps, args.warmup, kv=args.kv)
     w = r["w"]
     log(f"[bench] wall {r['wall'] * 1e3:.2f} ms, {r['tflops']:.1f} TFLOP/s per step, "
         f"attention kernel {r['kt'].mean() * 1e6:.1f} us avg -> {r['kernel_tflops']:.1f} TFLOP/s")
@@ -411,7 +419,7 @@ def main_prefill(args):
             "workload": args.workload, "requests": w.B, "tokens": w.T,
             "cached": [int(x) for x in w.cached], "new": [int(x) for x in w.new],
             "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
-            "p_precision": "bf16 hi+lo", "seed": 0,
+            "kv_dtype": "fp8_e4m3fn" if args.kv == "fp8" else "bf16", "p_precision": "bf16 hi+lo", "seed": 0,
         },
         "attention_kernel_us": {
             "mean": round(r["kt"].mean() * 1e6, 2),
@@ -424,7 +432,8 @@ def main_prefill(args):
             "unit": "TFLOP/s",
             "frac": round(r["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
             "traffic": None,
-            "kernel": "prefill_attn_kernel (causal prompt attention, bf16 matrix cores)",
+            "kernel": "prefill_attn_kernel (causal prompt attention, bf16 matrix cores"
+                      + (", fp8 codes widened to bf16 in registers)" if args.kv == "fp8" else ")"),
             "flops_per_launch": int(r["flops"]),
         },
     }
@@ -475,6 +484,9 @@ def main():
                     choices=["summarization", "summarization_capped", "llama3_8b", "stress_fp8",
                              "prefill_summarization", "prefill_chunked"],
                     help="decode batches, or prompt batches (prefill_*: the prompt write + prompt attention)")
+    ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
+                    help="prompt batches only: the pools' element type (fp8: e4m3fn codes with per-request, "
+                         "per-head scales)")
     ap.add_argument("--max-waves", type=int, default=0, help="cap on waves sharing the work (0 = all resident)")
     ap.add_argument("--xcd-skew", type=int, default=0,
                     help="work-share weights of even/odd XCDs: 0 = library default, -1 = equal, 1..255")
@@ -648,16 +660,18 @@ def main():
         result["roofline"]["frac_of_gather_probe"] = result["gather_probe"]["summarization_kernel_vs_probe"]
         log(f"[bench] gather probe: {g4:.1f} GB/s (4 KiB tiles), {g2:.1f} GB/s (2 KiB tiles)")
 
-        rp = measure_prefill("prefill_summarization", 20, 5)
-        result["prefill_summarization"] = {
-            "tokens": rp["w"].T, "kernel_tflops": round(rp["kernel_tflops"], 2),
-            "frac_of_bf16_peak": round(rp["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
-            "attention_kernel_us_mean": round(rp["kt"].mean() * 1e6, 2),
-            "step_tflops": round(rp["tflops"], 2),
-        }
-        log(f"[bench] prefill_summarization: {rp['kernel_tflops']:.1f} TFLOP/s attention kernel")
-        del rp
-        free_cuda()
+        for kv, key in (("bf16", "prefill_summarization"), ("fp8", "prefill_summarization_fp8")):
+            rp = measure_prefill("prefill_summarization", 20, 5, kv=kv)
+            result[key] = {
+                "tokens": rp["w"].T, "kv_dtype": "fp8_e4m3fn" if kv == "fp8" else "bf16",
+                "kernel_tflops": round(rp["kernel_tflops"], 2),
+                "frac_of_bf16_peak": round(rp["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
+                "attention_kernel_us_mean": round(rp["kt"].mean() * 1e6, 2),
+                "step_tflops": round(rp["tflops"], 2),
+            }
+            log(f"[bench] prefill_summarization ({kv} pools): {rp['kernel_tflops']:.1f} TFLOP/s attention kernel")
+            del rp
+            free_cuda()
 
     print(json.dumps(result), flush=True)
 

@@ -257,9 +257,11 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *   out[., h, :] = sum_{t <= p} softmax_t(scale * <q[., h, :], k_t>) * v_t
  * (query head h reads KV head h / G).
  *   q            bf16 [T, H_q, D], innermost contiguous, rows 16-byte aligned.
- *   k_pages, v_pages  bf16 pools as for bellman_decode_attention (fp8 pools:
- *                BELLMAN_ERR_UNSUPPORTED); D in {64, 128}; H_q a multiple of
- *                H_kv.
+ *   k_pages, v_pages  pools as for bellman_decode_attention, bf16 or fp8
+ *                (fp8: each tensor's dequant_scale [B, H_kv] is required,
+ *                and key k_t, value v_t of request b, KV head g read as
+ *                k_scale[b][g] * code, v_scale[b][g] * code); D in {64,
+ *                128}; H_q a multiple of H_kv.
  *   block_table  int32 [B, maxP]; seq_lens int32 [B] (after the write).
  *   out          bf16 [T, H_q, D] (written, rounded to nearest even); rows of
  *                a malformed request (n_b > L_b, rows past T, L_b past the
@@ -267,7 +269,10 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *                0 or ends past T writes no row at all (flag 2).
  * Each workgroup takes 128 query rows of one request and one query head;
  * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo (P
- * rounded to bf16 once would spend the bf16 error budget).  Scratch: B + 1
+ * rounded to bf16 once would spend the bf16 error budget); fp8 codes are
+ * staged in LDS as bytes and widened to bf16 exactly at the operand load,
+ * the K scale folded into the softmax scale and the V scale into the final
+ * normalisation.  Scratch: B + 1
  * integers of the per-device workspace.  Like bellman_kv_write, once the
  * workspace has grown to the call's size the call enqueues only kernels
  * (graph-capturable). */

@@ -277,13 +277,14 @@ def kv_write(k_new, v_new, k_pages, v_pages, block_table, seq_lens, q_start, str
 
 
 def prefill_attention(q, k_pages, v_pages, block_table, seq_lens, q_start, scale, out, stream=None,
-                      events=None):
+                      events=None, k_scale=None, v_scale=None):
     """bellman_prefill_attention(_opts): causal attention of each request's
-    new (last) tokens over its cached ones."""
-    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, q_start, out)
+    new (last) tokens over its cached ones (fp8 pools with their
+    per-(request, KV head) dequantisation scales k_scale / v_scale)."""
+    _device_tensors(q, k_pages, v_pages, block_table, seq_lens, q_start, out, k_scale, v_scale)
     lib = library()
-    args = (desc(q), desc(k_pages), desc(v_pages), desc(block_table), desc(seq_lens), desc(q_start),
-            ctypes.c_float(scale), desc(out))
+    args = (desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table), desc(seq_lens),
+            desc(q_start), ctypes.c_float(scale), desc(out))
     if events is None:
         _check(lib.bellman_prefill_attention(*args, _stream(stream)))
         return

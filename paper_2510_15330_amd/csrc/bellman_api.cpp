@@ -625,7 +625,6 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     int rc;
     PoolShape ps;
     if ((rc = check_pools(k_pages, v_pages, &ps, true))) return rc;
-    if (ps.fp8) return fail(BELLMAN_ERR_UNSUPPORTED, "prefill attention over fp8 pools is not implemented");
     if ((rc = check_tensor(q, "q", 3))) return rc;
     const int64_t T = q->shape[0];
     const int64_t H_q = q->shape[1];
@@ -679,6 +678,9 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     a.max_pages = (int)block_table->shape[1];
     a.err = err;
     a.tile_start = (int32_t*)(base + kWsHeader);
+    a.fp8 = ps.fp8 ? 1 : 0;
+    a.k_scale = k_pages->dequant_scale;
+    a.v_scale = v_pages->dequant_scale;
     if (opts && opts->event_begin) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_begin, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));

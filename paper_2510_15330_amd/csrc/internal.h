@@ -111,6 +111,9 @@ struct PrefillArgs {
     int B, T, H_q, H_kv, G, D, max_pages;
     int32_t* err;
     int32_t* tile_start;   // workspace [B + 1]: first query tile of each request
+    int fp8;               // pools of e4m3fn codes with the dequantisation scales below
+    const float* k_scale;  // fp8 only, fp32 [B, H_kv]
+    const float* v_scale;
 };
 
 // Launchers (kernels.hip).  They only enqueue; errors come back through

@@ -276,20 +276,29 @@ constexpr int kXcds = 8;            // accelerator complexes; workgroup i runs o
 // VALU instructions of the softmax placed between consecutive S MFMAs
 constexpr int kValuPerMfma = 7;
 
-template <int D, int NH>
+// FP8: pools of e4m3fn codes with per-(request, KV head) dequantisation
+// scales.  The tiles reach LDS as codes (half the bytes, no swizzle: a K
+// operand is eight codes of one 16-byte unit, a V operand eight of one
+// 16-byte row) and each operand is widened exactly to bf16 before the same
+// bf16 MFMAs; the K scale folds into the score scale and the V scale into
+// the final normalisation.
+template <int D, int NH, bool FP8>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_attn_kernel(PrefillArgs a) {
     constexpr int KS = 32 * NH;         // keys per step
     constexpr int PPS = KS / kPage;     // pages per step
+    constexpr int EB = FP8 ? 1 : 2;     // bytes per pool element
     constexpr int PE = D * kPage;       // elements of one page of one head (K or V)
-    constexpr int KT = PPS * PE;        // a step's K (or V) tile
-    constexpr int UPP = PE / 8;         // 16-byte units per page
+    constexpr int PB = PE * EB;         // its bytes
+    constexpr int KT = PPS * PE;        // a step's K (or V) tile, elements
+    constexpr int KTW = PPS * PB / 2;   // the tile in 16-bit words
+    constexpr int UPP = PB / 16;        // 16-byte units per page
     constexpr int PER = 2 * PPS * UPP / 256;   // units of K + V per thread per step
     constexpr int WIN = kPageWindow / PPS;     // steps per block-table window
-    __shared__ __attribute__((aligned(16))) uint16_t kb0[KT];
-    __shared__ __attribute__((aligned(16))) uint16_t kb1[KT];
-    __shared__ __attribute__((aligned(16))) uint16_t vb0[KT];
-    __shared__ __attribute__((aligned(16))) uint16_t vb1[KT];
+    __shared__ __attribute__((aligned(16))) uint16_t kb0[KTW];
+    __shared__ __attribute__((aligned(16))) uint16_t kb1[KTW];
+    __shared__ __attribute__((aligned(16))) uint16_t vb0[KTW];
+    __shared__ __attribute__((aligned(16))) uint16_t vb1[KTW];
     __shared__ int pages[kPageWindow];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -332,11 +341,17 @@ prefill_attn_kernel(PrefillArgs a) {
     const int wave_steps = rw < n ? (p0 + min(rw + 31, n - 1)) / KS + 1 : 0;
 
     // softmax(scale * s) = softmax(|scale| * (-s)): for a negative scale the
-    // query's sign bits are flipped (the host keeps |scale| >= FLT_MIN)
-    const float sl = fabsf(a.scale_log2);
+    // query's sign bits are flipped (the host keeps |scale| >= FLT_MIN).
+    // fp8 pools: the scores are dequantised by the (request, head)'s K scale.
+    float s_eff = a.scale_log2, v_scale = 1.f;
+    if constexpr (FP8) {
+        s_eff *= a.k_scale[(int64_t)b * a.H_kv + g];
+        v_scale = a.v_scale[(int64_t)b * a.H_kv + g];
+    }
+    const float sl = fabsf(s_eff);
     bf16x8 qv[D / 16];
     {
-        const uint32_t flip = a.scale_log2 < 0.f ? 0x80008000u : 0u;
+        const uint32_t flip = s_eff < 0.f ? 0x80008000u : 0u;
         const uint16_t* qrow = a.q + (int64_t)(t0 + row) * a.q_st + (int64_t)h * a.q_sh + 8 * hl;
 #pragma unroll
         for (int kb = 0; kb < D / 16; ++kb) {
@@ -363,9 +378,9 @@ prefill_attn_kernel(PrefillArgs a) {
     // step s computes, K of step s + 2 and V of step s + 1 are loaded into
     // registers, and written to LDS after it.
     constexpr int PERH = PER / 2;      // units of one tensor per thread per step
-    const char* kbase = (const char*)a.k_pages + (int64_t)g * PE * 2;
-    const char* vbase = (const char*)a.v_pages + (int64_t)g * PE * 2;
-    const int64_t page_bytes = (int64_t)a.H_kv * PE * 2;
+    const char* kbase = (const char*)a.k_pages + (int64_t)g * PB;
+    const char* vbase = (const char*)a.v_pages + (int64_t)g * PB;
+    const int64_t page_bytes = (int64_t)a.H_kv * PB;
     int64_t off1[PPS], off2[PPS];      // page byte offsets of steps s + 1 and s + 2
     auto pages_of = [&](int j, int64_t (&off)[PPS]) {
         const int e = PPS * (j % WIN);
@@ -379,29 +394,46 @@ prefill_attn_kernel(PrefillArgs a) {
             off[q] = (int64_t)pg * page_bytes;
         }
     };
-    constexpr int BPP = 256 / UPP;
     // direct copies into LDS: lane l of a wave lands at unit (wave base + l);
     // it fetches the global unit the swizzle maps there (the swizzles are
-    // involutions within a page)
+    // involutions within a page; fp8 tiles are not swizzled)
     auto dma = [&](const char* base, const int64_t (&off)[PPS], uint16_t* dst, bool isv) {
 #pragma unroll
         for (int k = 0; k < PERH; ++k) {
-            const int pp = (256 * k) / UPP;
-            int64_t o_pg = off[pp];
-            if constexpr (BPP == 2) o_pg = (w >> 1) ? off[pp + 1] : o_pg;
+            int64_t o_pg;
+            if constexpr (FP8) {
+                const int pp = (256 * k + 64 * w) / UPP;               // page of this wave's 64 units
+                o_pg = off[0];
+#pragma unroll
+                for (int q = 1; q < PPS; ++q) o_pg = pp == q ? off[q] : o_pg;
+            } else {
+                constexpr int BPP = 256 / UPP;
+                const int pp = (256 * k) / UPP;
+                o_pg = off[pp];
+                if constexpr (BPP == 2) o_pg = (w >> 1) ? off[pp + 1] : o_pg;
+            }
             const int v = ((256 * k + 64 * w) % UPP) + lane;          // LDS unit within its page
-            const int vg = isv ? v ^ (((v >> 3) ^ (v >> 4)) & 1) : v ^ (((v >> 3) & 1) << 2);
+            const int vg = FP8 ? v : isv ? v ^ (((v >> 3) ^ (v >> 4)) & 1) : v ^ (((v >> 3) & 1) << 2);
             __builtin_amdgcn_global_load_lds(base + o_pg + vg * 16, dst + 8 * (256 * k + 64 * w), 16, 0, 0);
         }
     };
     // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
     // 0 * NaN must not reach O, so the tail step's slots are cleared
     auto clear_tail = [&](int s, uint16_t* V) {
-        for (int e = tid; e < KT; e += 256) {
-            const int d = (e % PE) >> 4;
-            const int half = ((e >> 3) & 1) ^ (((d >> 2) ^ (d >> 3)) & 1);
-            const int key = KS * s + 16 * (e / PE) + 8 * half + (e & 7);
-            if (key >= L) V[e] = 0;
+        if constexpr (FP8) {
+            // codes [page][D][16 slots]
+            uint8_t* Vb = (uint8_t*)V;
+            for (int e = tid; e < KT; e += 256) {
+                const int key = KS * s + 16 * (e / PE) + (e & 15);
+                if (key >= L) Vb[e] = 0;
+            }
+        } else {
+            for (int e = tid; e < KT; e += 256) {
+                const int d = (e % PE) >> 4;
+                const int half = ((e >> 3) & 1) ^ (((d >> 2) ^ (d >> 3)) & 1);
+                const int key = KS * s + 16 * (e / PE) + 8 * half + (e & 7);
+                if (key >= L) V[e] = 0;
+            }
         }
     };
 
@@ -410,16 +442,40 @@ prefill_attn_kernel(PrefillArgs a) {
     const int kslot = (kk & 15) ^ (((kk >> 3) & 1) << 2);
     const int k_off = (kk >> 4) * PE + hl * (kPage * 8) + kslot * 8;
     const int v_off = c * kPage + 8 * (hl ^ (((c >> 2) ^ (c >> 3)) & 1));
+    // fp8 (byte offsets): K unit (chunk kb, slot) of the key's page, codes
+    // 8 hl .. 8 hl + 7; V row (32 t + c) of page u, codes 8 hl .. 8 hl + 7
+    const int k_off8 = (kk >> 4) * PB + (kk & 15) * 16 + 8 * hl;
+    const int v_off8 = c * 16 + 8 * hl;
+    // eight codes -> eight bf16, exactly
+    auto widen = [](const u32x2 w8) -> bf16x8 {
+        const bf16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w8.x, 1.0f, false);
+        const bf16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w8.x, 1.0f, true);
+        const bf16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w8.y, 1.0f, false);
+        const bf16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w8.y, 1.0f, true);
+        return __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1),
+                                                __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)});
+    };
+    auto k_operand = [&](const uint16_t* Kt, int hh, int kb) -> bf16x8 {
+        if constexpr (FP8)
+            return widen(*(const u32x2*)((const char*)Kt + hh * 2 * PB + kb * 256 + k_off8));
+        else
+            return *(const bf16x8*)(Kt + k_off + hh * 2 * PE + kb * (2 * kPage * 8));
+    };
+    auto v_operand = [&](const uint16_t* Vt0, int hh, int u, int t) -> bf16x8 {
+        if constexpr (FP8)
+            return widen(*(const u32x2*)((const char*)Vt0 + (hh * 2 + u) * PB + (32 * t) * 16 + v_off8));
+        else
+            return *(const bf16x8*)(Vt0 + v_off + hh * 2 * PE + (u * D + 32 * t) * kPage);
+    };
 
     auto qk = [&](const uint16_t* Kt, f32x16 (&sc)[NH]) {
-        const uint16_t* K = Kt + k_off;
 #pragma unroll
         for (int hh = 0; hh < NH; ++hh) sc[hh] = f32x16{};
 #pragma unroll
         for (int kb = 0; kb < D / 16; ++kb)
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh) {
-                const bf16x8 ka = *(const bf16x8*)(K + hh * 2 * PE + kb * (2 * kPage * 8));
+                const bf16x8 ka = k_operand(Kt, hh, kb);
                 sc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc[hh], 0, 0, 0);
             }
     };
@@ -513,7 +569,6 @@ prefill_attn_kernel(PrefillArgs a) {
                 __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);   // softmax VALU
             }
             // O^T += V^T P^T, per 16-key page u of each half and 32-dim tile t
-            const uint16_t* Vt = v_rd + v_off;
 #pragma unroll
             for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
@@ -524,7 +579,7 @@ prefill_attn_kernel(PrefillArgs a) {
                         bf16x8, u32x4{pl[hh][4 * u], pl[hh][4 * u + 1], pl[hh][4 * u + 2], pl[hh][4 * u + 3]});
 #pragma unroll
                     for (int t = 0; t < D / 32; ++t) {
-                        const bf16x8 va = *(const bf16x8*)(Vt + hh * 2 * PE + (u * D + 32 * t) * kPage);
+                        const bf16x8 va = v_operand(v_rd, hh, u, t);
                         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
                         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
                     }
@@ -558,7 +613,7 @@ prefill_attn_kernel(PrefillArgs a) {
     if (bad && lane == 0) atomicOr(a.err, kErrPage);
     if (rw >= n) return;
     const float l_tot = l + swap_halves(l);
-    const float f = 1.0f / l_tot;
+    const float f = v_scale / l_tot;
     if (rw + c < n) {
         uint16_t* orow = a.out + (int64_t)(t0 + rw + c) * a.o_st + (int64_t)h * a.o_sh;
 #pragma unroll
@@ -594,10 +649,16 @@ void launch_prefill(const PrefillArgs& a, hipStream_t s) {
     // an upper bound on tiles x query heads, rounded up to whole XCD rows
     const int64_t items = ((int64_t)(a.T + kPrefillRows - 1) / kPrefillRows + a.B) * a.H_q;
     const dim3 grid((unsigned)((items + kXcds - 1) / kXcds * kXcds));
-    if (a.D == 128)
-        hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves>), grid, dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves>), grid, dim3(256), 0, s, a);
+    if (a.fp8) {
+        if (a.D == 128)
+            hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, true>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, true>), grid, dim3(256), 0, s, a);
+    } else if (a.D == 128) {
+        hipLaunchKernelGGL((prefill_attn_kernel<128, kHalves, false>), grid, dim3(256), 0, s, a);
+    } else {
+        hipLaunchKernelGGL((prefill_attn_kernel<64, kHalves, false>), grid, dim3(256), 0, s, a);
+    }
 }
 
 }  // namespace bellman

@@ -312,8 +312,11 @@ class PrefillWorkload:
     k_pages: torch.Tensor        # bf16 [NP, H_kv, D/8, 16, 8]
     v_pages: torch.Tensor        # bf16 [NP, H_kv, D, 16]
     q: torch.Tensor              # bf16 [T, H_q, D]
-    k_new: torch.Tensor          # bf16 [T, H_kv, D]
+    k_new: torch.Tensor          # bf16 [T, H_kv, D] (fp8 pools: e4m3fn codes, uint8)
     v_new: torch.Tensor
+    kv: str = "bf16"             # "bf16", or "fp8": pools [NP, H_kv, D/16, 16, 16] / [NP, H_kv, D, 16] of codes
+    k_scale: torch.Tensor = None  # fp8 only: fp32 [B, H_kv] dequantisation scales
+    v_scale: torch.Tensor = None
 
     @property
     def B(self):
@@ -352,7 +355,7 @@ def prefill_lengths(name, seed=0):
 
 
 def build_prefill(name=None, seed=0, device="cpu", cached=None, new=None, H_q=None, H_kv=None, D=None,
-                  slack_pages=5, extra_table=1):
+                  slack_pages=5, extra_table=1, kv="bf16"):
     """Materialise a prompt batch on ``device``: pages for every cached and new
     token (scattered over a permuted pool), cached tokens' K/V present, every
     other slot NaN, unused table entries -1.  Named configurations come from
@@ -389,23 +392,39 @@ def build_prefill(name=None, seed=0, device="cpu", cached=None, new=None, H_q=No
 
     gen = torch.Generator(device=device)
     gen.manual_seed(int(ss[_S_P_VALUES].generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF))
-    kshape = (NP, H_kv, D // 8, PAGE, 8)
-    vshape = (NP, H_kv, D, PAGE)
     filled_t = torch.from_numpy(filled).to(device)
     slot = torch.arange(PAGE, device=device)
     live = slot[None, :] < filled_t[:, None]
-    nan = torch.tensor(BF16_NAN_BITS, dtype=torch.int16, device=device).view(torch.bfloat16)
-    k_pages = torch.where(live[:, None, None, :, None], _fill_pages(kshape, gen, device), nan)
-    v_pages = torch.where(live[:, None, None, :], _fill_pages(vshape, gen, device), nan)
     T = int(new.sum())
-    q = _bf16_normal((T, H_q, D), gen, device)
-    k_new = _bf16_normal((T, H_kv, D), gen, device)
-    v_new = _bf16_normal((T, H_kv, D), gen, device)
     q_start = np.concatenate([[0], np.cumsum(new)]).astype(np.int32)
+    k_scale = v_scale = None
+    if kv == "bf16":
+        kshape = (NP, H_kv, D // 8, PAGE, 8)
+        vshape = (NP, H_kv, D, PAGE)
+        nan = torch.tensor(BF16_NAN_BITS, dtype=torch.int16, device=device).view(torch.bfloat16)
+        k_pages = torch.where(live[:, None, None, :, None], _fill_pages(kshape, gen, device), nan)
+        v_pages = torch.where(live[:, None, None, :], _fill_pages(vshape, gen, device), nan)
+        q = _bf16_normal((T, H_q, D), gen, device)
+        k_new = _bf16_normal((T, H_kv, D), gen, device)
+        v_new = _bf16_normal((T, H_kv, D), gen, device)
+    else:
+        # codes of N(0,1) values at scale = amax / 448 of each (request, head)'s
+        # cached tokens (1 where none is cached); the new tokens' codes at the
+        # same scales, as a quantising writer would store them
+        kshape = (NP, H_kv, D // 16, PAGE, 16)
+        vshape = (NP, H_kv, D, PAGE)
+        owner_t = torch.from_numpy(owner).to(device)
+        k_pages, k_scale = _fp8_pool(kshape, gen, device, live[:, None, None, :, None], owner_t, B, H_kv, (2, 3, 4))
+        v_pages, v_scale = _fp8_pool(vshape, gen, device, live[:, None, None, :], owner_t, B, H_kv, (2, 3))
+        q = _bf16_normal((T, H_q, D), gen, device)
+        tok_req = torch.from_numpy(np.repeat(np.arange(B), new).astype(np.int64)).to(device)
+        k_new = _fp8_quantise(torch.randn((T, H_kv, D), generator=gen, device=device), k_scale[tok_req][:, :, None])
+        v_new = _fp8_quantise(torch.randn((T, H_kv, D), generator=gen, device=device), v_scale[tok_req][:, :, None])
     return PrefillWorkload(
         name=name or "custom", H_q=H_q, H_kv=H_kv, D=D, scale=float(np.float32(1.0 / math.sqrt(D))),
         cached=cached, new=new, num_pages=NP,
         block_table=torch.from_numpy(bt).to(device),
         seq_lens=torch.from_numpy(cached.astype(np.int32)).to(device),
         q_start=torch.from_numpy(q_start).to(device),
-        k_pages=k_pages.contiguous(), v_pages=v_pages.contiguous(), q=q, k_new=k_new, v_new=v_new)
+        k_pages=k_pages.contiguous(), v_pages=v_pages.contiguous(), q=q, k_new=k_new.contiguous(),
+        v_new=v_new.contiguous(), kv=kv, k_scale=k_scale, v_scale=v_scale)

@@ -161,8 +161,12 @@ PREFILL_CASES = [
     ("out rows", lambda B_, g: g.update(pout=t(B_.BF16, [39, 32, 128])), ERR_INVALID, "out: shape"),
     ("H_q not multiple", lambda B_, g: g.update(pq=t(B_.BF16, [40, 30, 128]), pout=t(B_.BF16, [40, 30, 128])),
      ERR_INVALID, "not a multiple"),
-    ("fp8 pools", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 8, 16, 16], scale=FAKE),
-                                         v=t(B_.FP8_E4M3FN, [100, 8, 128, 16], scale=FAKE)), ERR_UNSUPPORTED, "fp8"),
+    ("fp8 pools without scales", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 8, 16, 16]),
+                                                        v=t(B_.FP8_E4M3FN, [100, 8, 128, 16])), ERR_INVALID,
+     "dequant_scale"),
+    ("fp8 pools wrong chunk", lambda B_, g: g.update(k=t(B_.FP8_E4M3FN, [100, 8, 16, 16, 8], scale=FAKE),
+                                                     v=t(B_.FP8_E4M3FN, [100, 8, 128, 16], scale=FAKE)), ERR_INVALID,
+     "chunk"),
     ("misaligned q", lambda B_, g: g.update(pq=t(B_.BF16, [40, 32, 128], data=FAKE + 2)), ERR_UNSUPPORTED, "aligned"),
     ("misaligned out", lambda B_, g: g.update(pout=t(B_.BF16, [40, 32, 128], data=FAKE + 4)), ERR_UNSUPPORTED,
      "aligned"),

@@ -22,16 +22,35 @@ def _write(w):
     bl.kv_write(w.k_new, w.v_new, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start)
 
 
+def _codes(t):
+    # a tensor's elements as host codes: bf16 bits, or fp8 bytes
+    return t.cpu().numpy() if t.dtype == torch.uint8 else bits16(t)
+
+
 def _host_pools(w):
-    return bits16(w.k_pages), bits16(w.v_pages)
+    return _codes(w.k_pages), _codes(w.v_pages)
 
 
-def _oracle_prefill(w, kp, vp, seq_lens=None, q_bits=None, q_start=None, block_table=None):
+def _oracle_prefill(w, kp, vp, seq_lens=None, q_bits=None, q_start=None, block_table=None, rows=None):
+    fp8 = w.kv == "fp8"
+    ks = vs = None
+    if fp8:
+        # one-token stand-in requests (rows) carry their own request's scales
+        pick = slice(None) if rows is None else rows
+        ks = w.k_scale.cpu().numpy()[pick]
+        vs = w.v_scale.cpu().numpy()[pick]
     return oracle.prefill_attention(
         bits16(w.q) if q_bits is None else q_bits, kp, vp,
         (w.block_table.cpu().numpy() if block_table is None else block_table),
         (w.seq_lens.cpu().numpy().astype(np.int32) if seq_lens is None else seq_lens),
-        (w.q_start.cpu().numpy() if q_start is None else q_start), w.scale)
+        (w.q_start.cpu().numpy() if q_start is None else q_start), w.scale,
+        kv_dtype=oracle.FP8_E4M3FN if fp8 else oracle.BF16, k_scale=ks, v_scale=vs)
+
+
+def _attend(w, q, out, q_start=None, block_table=None):
+    bl.prefill_attention(q, w.k_pages, w.v_pages, w.block_table if block_table is None else block_table,
+                         w.seq_lens, w.q_start if q_start is None else q_start, w.scale, out,
+                         k_scale=w.k_scale, v_scale=w.v_scale)
 
 
 def _out_f64(out):
@@ -110,17 +129,20 @@ ATTN_CASES = [
 ]
 
 
+# fp8 pools: the codes widen to bf16 exactly and the scales enter in fp32,
+# so the arithmetic is the bf16 path's and so is the tolerance
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
 @pytest.mark.parametrize("case", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
-def test_prefill_matches_oracle(case):
+def test_prefill_matches_oracle(case, kv):
     name, cached, new, H_q, H_kv, D = case
-    w = wl.build_prefill(cached=cached, new=new, H_q=H_q, H_kv=H_kv, D=D, seed=len(name), device="cuda")
+    w = wl.build_prefill(cached=cached, new=new, H_q=H_q, H_kv=H_kv, D=D, seed=len(name), device="cuda", kv=kv)
     _write(w)
     out = torch.full((w.T, H_q, D), float("nan"), dtype=torch.bfloat16, device="cuda")
-    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
+    _attend(w, w.q, out)
     assert bl.device_errors() == 0
     kp, vp = _host_pools(w)
     ref = _oracle_prefill(w, kp, vp)
-    assert_close(_out_f64(out), ref, "bf16", name)
+    assert_close(_out_f64(out), ref, "bf16", f"{name} {kv}")
 
 
 def _sweep_counts(rng, B, edge):
@@ -141,26 +163,29 @@ def test_prefill_random_sweep(seed):
     # seeded shapes: GQA group, head_dim, cached prefixes and new-token counts
     # on and next to page (16), step (64) and tile (128) edges, empty chunks
     rng = np.random.default_rng(7000 + seed)
+    kv = "fp8" if seed % 3 == 2 else "bf16"
     H_kv = int(rng.choice([1, 2, 4, 8]))
     G = int(rng.choice([1, 2, 3, 4, 8, 16]))
     D = 64 if seed % 2 else 128
     B = int(rng.integers(1, 7))
     cached = _sweep_counts(rng, B, 16)
     new = _sweep_counts(rng, B, int(rng.choice([16, 64, 128])))
-    w = wl.build_prefill(cached=cached, new=new, H_q=G * H_kv, H_kv=H_kv, D=D, seed=7000 + seed, device="cuda")
+    w = wl.build_prefill(cached=cached, new=new, H_q=G * H_kv, H_kv=H_kv, D=D, seed=7000 + seed, device="cuda",
+                         kv=kv)
     kp0, vp0 = _host_pools(w)
     sl0 = w.seq_lens.cpu().numpy().astype(np.int32)
     _write(w)
     assert bl.device_errors() == 0
     kp, vp = _host_pools(w)
     kx, vx, sx = kp0.copy(), vp0.copy(), sl0.copy()
-    oracle.kv_write(bits16(w.k_new), bits16(w.v_new), kx, vx, w.block_table.cpu().numpy(), sx, w.q_start.cpu().numpy())
-    what = f"seed={seed} G={G} H_kv={H_kv} D={D} cached={cached} new={new}"
+    oracle.kv_write(_codes(w.k_new), _codes(w.v_new), kx, vx, w.block_table.cpu().numpy(), sx,
+                    w.q_start.cpu().numpy(), kv_dtype=oracle.FP8_E4M3FN if kv == "fp8" else oracle.BF16)
+    what = f"seed={seed} {kv} G={G} H_kv={H_kv} D={D} cached={cached} new={new}"
     assert np.array_equal(kp, kx) and np.array_equal(vp, vx), what
     if w.T == 0:
         return
     out = torch.full((w.T, G * H_kv, D), float("nan"), dtype=torch.bfloat16, device="cuda")
-    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
+    _attend(w, w.q, out)
     assert bl.device_errors() == 0
     assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16", what)
 
@@ -239,7 +264,7 @@ def test_prefill_empty_batch_and_rejections():
     out = torch.empty((0, 4, 64), dtype=torch.bfloat16, device="cuda")
     bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
     assert bl.device_errors() == 0
-    w8 = wl.build(name="tiny", device="cuda")
+    # fp8 pools: an empty batch is accepted; pools without their scales are not
     kp8 = torch.zeros((4, 2, 4, 16, 16), dtype=torch.uint8, device="cuda")
     vp8 = torch.zeros((4, 2, 64, 16), dtype=torch.uint8, device="cuda")
     s = torch.ones((1, 2), dtype=torch.float32, device="cuda")
@@ -247,8 +272,12 @@ def test_prefill_empty_batch_and_rejections():
     from paper_2510_15330_amd import _binding as B
     rc = lib.bellman_prefill_attention(B.desc(w.q), B.desc(kp8, s), B.desc(vp8, s), B.desc(w.block_table),
                                        B.desc(w.seq_lens), B.desc(w.q_start), 0.125, B.desc(out), None)
-    assert rc == -2 and "fp8" in bl.last_error()
-    del w8
+    assert rc == 0
+    rc = lib.bellman_prefill_attention(B.desc(w.q), B.desc(kp8), B.desc(vp8), B.desc(w.block_table),
+                                       B.desc(w.seq_lens), B.desc(w.q_start), 0.125, B.desc(out), None)
+    assert rc == -1 and "dequant_scale" in bl.last_error()
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
 
 
 # ------------------------------------------------------------ full sizes --
@@ -270,12 +299,13 @@ def _sampled_rows(w, rng, per_request):
     return picks
 
 
-@pytest.mark.parametrize("name", ["prefill_summarization", "prefill_chunked"])
-def test_prefill_full_size_sampled_rows(name):
-    w = wl.build_prefill(name, seed=0, device="cuda")
+@pytest.mark.parametrize("name,kv", [("prefill_summarization", "bf16"), ("prefill_chunked", "bf16"),
+                                     ("prefill_summarization", "fp8")])
+def test_prefill_full_size_sampled_rows(name, kv):
+    w = wl.build_prefill(name, seed=0, device="cuda", kv=kv)
     _write(w)
     out = torch.empty((w.T, w.H_q, w.D), dtype=torch.bfloat16, device="cuda")
-    bl.prefill_attention(w.q, w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.q_start, w.scale, out)
+    _attend(w, w.q, out)
     assert bl.device_errors() == 0
     assert torch.isfinite(out).all()
     picks = _sampled_rows(w, np.random.default_rng(7), 3)
@@ -287,8 +317,9 @@ def test_prefill_full_size_sampled_rows(name):
     q_bits = bits16(w.q[torch.tensor(rows, device="cuda")])
     kp, vp = _host_pools(w)
     ref = _oracle_prefill(w, kp, vp, seq_lens=lens, q_bits=q_bits,
-                          q_start=np.arange(len(rows) + 1, dtype=np.int32), block_table=bt)
-    assert_close(_out_f64(out)[rows], ref, "bf16", name)
+                          q_start=np.arange(len(rows) + 1, dtype=np.int32), block_table=bt,
+                          rows=[p[1] for p in picks])
+    assert_close(_out_f64(out)[rows], ref, "bf16", f"{name} {kv}")
 
 
 def test_kv_write_fp8_codes_bit_exact():

@@ -28,9 +28,9 @@ CASES = [
 ]
 
 
-def _case(seed, B, H_q, H_kv, D, lens, nq):
+def _case(seed, B, H_q, H_kv, D, lens, nq, kv="bf16"):
     rng = np.random.default_rng(seed)
-    c = dn.random_case(rng, B, H_q, H_kv, D, lens, "bf16")
+    c = dn.random_case(rng, B, H_q, H_kv, D, lens, kv)
     T = int(sum(nq))
     q = rng.standard_normal((T, H_q, D)).astype(np.float32)
     c["pq_bits"] = torch.from_numpy(q).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
@@ -59,6 +59,29 @@ def pin_prefill_dense_numpy(lib):
                 err = np.abs(got[t] - ref).max()
                 if not err <= 1e-12:
                     return f"prefill dense case {i} b={b} j={j}: {err}"
+    return None
+
+
+def pin_prefill_dense_fp8(lib):
+    # fp8 pools: codes decoded by torch's float8_e4m3fn, times the request's
+    # per-head scales, then dense causal attention
+    for i, (B, H_q, H_kv, D, lens, nq) in enumerate(CASES):
+        c = _case(320 + i, B, H_q, H_kv, D, lens, nq, kv="fp8")
+        scale = 1.0 / np.sqrt(D)
+        got = oracle.prefill_attention(c["pq_bits"], c["k_pages"], c["v_pages"], c["block_table"], c["seq_lens"],
+                                       c["q_start"], scale, kv_dtype=oracle.FP8_E4M3FN, k_scale=c["k_scale"],
+                                       v_scale=c["v_scale"], lib=lib)
+        q = dn.bits_to_f64_bf16(c["pq_bits"])
+        for b in range(B):
+            ks = dn.codes_to_f64_fp8(c["dense_k"][b]) * c["k_scale"][b][None, :, None].astype(np.float64)
+            vs = dn.codes_to_f64_fp8(c["dense_v"][b]) * c["v_scale"][b][None, :, None].astype(np.float64)
+            for j in range(nq[b]):
+                t = c["q_start"][b] + j
+                p = lens[b] - nq[b] + j
+                ref = dn.dense_attention(q[t], ks[:p + 1], vs[:p + 1], scale)
+                err = np.abs(got[t] - ref).max()
+                if not err <= 1e-12:
+                    return f"prefill fp8 dense case {i} b={b} j={j}: {err}"
     return None
 
 
@@ -149,7 +172,7 @@ def pin_kv_write_bytes(lib):
     return None
 
 
-PREFILL_PINS = [pin_prefill_dense_numpy, pin_prefill_torch_causal, pin_first_token_is_its_value,
+PREFILL_PINS = [pin_prefill_dense_numpy, pin_prefill_dense_fp8, pin_prefill_torch_causal, pin_first_token_is_its_value,
                 pin_future_tokens_ignored, pin_kv_write_bytes]
 
 
@@ -158,12 +181,23 @@ def test_prefill_pins(oracle_lib, pin):
     assert pin(oracle_lib) is None
 
 
+# the prefill loop's scale lookup (the decode loop has the same two lines;
+# the call after them tells the two apart)
+_FP8_SCALES = ("                ks = (double)k_scale[(int64_t)b * H_kv + g];\n"
+               "                vs = (double)v_scale[(int64_t)b * H_kv + g];\n            }\n")
+_PREFILL_CALL = "            if (attend(q + (i * H_q + h) * D"
+
 PREFILL_MUTANTS = {
     "position ignores cached prefix": ("const int p = seq_lens[b] - n + (int)(i - q_start[b]);",
                                        "const int p = (int)(i - q_start[b]);"),
     "attends one token less": ("attend(q + (i * H_q + h) * D, b, g, p + 1,", "attend(q + (i * H_q + h) * D, b, g, p,"),
     "write position from zero": ("int pos = L + (int)(i - q_start[b]);", "int pos = (int)(i - q_start[b]);"),
     "write keeps length": ("seq_lens[b] = L + (q_start[b + 1] - q_start[b]);", "seq_lens[b] = L;"),
+    "fp8 scales swapped": (_FP8_SCALES + _PREFILL_CALL,
+                           _FP8_SCALES.replace("k_scale[", "@").replace("v_scale[", "k_scale[").replace("@", "v_scale[")
+                           + _PREFILL_CALL),
+    "fp8 scales of request 0": (_FP8_SCALES + _PREFILL_CALL,
+                                _FP8_SCALES.replace("(int64_t)b * H_kv + g", "g") + _PREFILL_CALL),
 }
 
 
