@@ -277,11 +277,22 @@ constexpr int kXcds = 8;            // accelerator complexes; workgroup i runs o
 constexpr int kValuPerMfma = 7;
 
 // FP8: pools of e4m3fn codes with per-(request, KV head) dequantisation
-// scales.  The tiles reach LDS as codes (half the bytes, no swizzle: a K
-// operand is eight codes of one 16-byte unit, a V operand eight of one
-// 16-byte row) and each operand is widened exactly to bf16 before the same
-// bf16 MFMAs; the K scale folds into the score scale and the V scale into
-// the final normalisation.
+// scales.  The tiles reach LDS as codes (half the bytes) and each operand is
+// widened exactly to bf16 before the same bf16 MFMAs; the K scale folds into
+// the score scale and the V scale into the final normalisation.  A lane
+// reads one whole 16-byte unit and feeds two MFMAs with its halves:
+//  * S: A row i holds key pi8(i) = 16 ((i / 4) % 2) + 8 (i / 16) +
+//    4 ((i / 8) % 2) + i % 4, so lane (h, c) of the result holds the keys
+//    16 h + 8 e + 0..7 (e = 0, 1) of each 32-key half: page h of the half.
+//    MFMA pair (2 m, 2 m + 1) reads, in lane (h, c), the unit of chunk
+//    2 m + h of key pi8(c) and takes its codes 8 e .. 8 e + 7 into MFMA
+//    2 m + e; the query operand of MFMA 2 m + e holds dims 32 m + 16 h + 8 e.
+//  * PV: lane (h, c) reads row 32 t + c of page h of the half (16 keys) and
+//    takes keys 8 e .. 8 e + 7 into MFMA e, whose P operand is then exactly
+//    the lane's probabilities of group e.
+// Pages sit PB + 128 bytes apart in LDS and odd pages hold K slot s at
+// s ^ 4, so every 8 (and 16) consecutive lanes of a read touch distinct
+// banks.
 template <int D, int NH, bool FP8>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 prefill_attn_kernel(PrefillArgs a) {
@@ -291,7 +302,8 @@ prefill_attn_kernel(PrefillArgs a) {
     constexpr int PE = D * kPage;       // elements of one page of one head (K or V)
     constexpr int PB = PE * EB;         // its bytes
     constexpr int KT = PPS * PE;        // a step's K (or V) tile, elements
-    constexpr int KTW = PPS * PB / 2;   // the tile in 16-bit words
+    constexpr int PBP = FP8 ? PB + 128 : PB;   // LDS bytes from one page of a tile to the next
+    constexpr int KTW = PPS * PBP / 2;  // the tile in 16-bit words
     constexpr int UPP = PB / 16;        // 16-byte units per page
     constexpr int PER = 2 * PPS * UPP / 256;   // units of K + V per thread per step
     constexpr int WIN = kPageWindow / PPS;     // steps per block-table window
@@ -352,10 +364,11 @@ prefill_attn_kernel(PrefillArgs a) {
     bf16x8 qv[D / 16];
     {
         const uint32_t flip = s_eff < 0.f ? 0x80008000u : 0u;
-        const uint16_t* qrow = a.q + (int64_t)(t0 + row) * a.q_st + (int64_t)h * a.q_sh + 8 * hl;
+        // the B operand of MFMA kb: dims 16 kb + 8 hl (fp8: 32 (kb / 2) + 16 hl + 8 (kb % 2))
+        const uint16_t* qrow = a.q + (int64_t)(t0 + row) * a.q_st + (int64_t)h * a.q_sh + (FP8 ? 16 : 8) * hl;
 #pragma unroll
         for (int kb = 0; kb < D / 16; ++kb) {
-            u32x4 v = *(const u32x4*)(qrow + 16 * kb);
+            u32x4 v = *(const u32x4*)(qrow + (FP8 ? 32 * (kb >> 1) + 8 * (kb & 1) : 16 * kb));
             v ^= flip;
             qv[kb] = __builtin_bit_cast(bf16x8, v);
         }
@@ -402,10 +415,25 @@ prefill_attn_kernel(PrefillArgs a) {
         for (int k = 0; k < PERH; ++k) {
             int64_t o_pg;
             if constexpr (FP8) {
-                const int pp = (256 * k + 64 * w) / UPP;               // page of this wave's 64 units
-                o_pg = off[0];
-#pragma unroll
-                for (int q = 1; q < PPS; ++q) o_pg = pp == q ? off[q] : o_pg;
+                const int u0 = 256 * k + 64 * w;    // this wave's 64 units: one page's units u0 % UPP ..
+                const int pp = u0 / UPP;
+                // page (256 k) / UPP + (w / (4 / BPP)) of the step, chosen by
+                // selects on the wave's bits (no indexed access of off[],
+                // which the compiler would stage through memory)
+                constexpr int BPP = 256 / UPP;  // pages a round of 256 units covers: 2 (D 128) or 4 (D 64)
+                const int p0k = (256 * k) / UPP;
+                if constexpr (BPP == 2) {
+                    o_pg = (w >> 1) ? off[p0k + 1] : off[p0k];
+                } else {
+                    const int64_t lo2 = (w & 1) ? off[p0k + 1] : off[p0k];
+                    const int64_t hi2 = (w & 1) ? off[p0k + 3] : off[p0k + 2];
+                    o_pg = (w & 2) ? hi2 : lo2;
+                }
+                const int v = u0 % UPP + lane;
+                const int vg = (!isv && (pp & 1)) ? v ^ 4 : v;
+                __builtin_amdgcn_global_load_lds(base + o_pg + vg * 16, dst + (pp * PBP + (u0 % UPP) * 16) / 2, 16, 0,
+                                                 0);
+                continue;
             } else {
                 constexpr int BPP = 256 / UPP;
                 const int pp = (256 * k) / UPP;
@@ -421,11 +449,11 @@ prefill_attn_kernel(PrefillArgs a) {
     // 0 * NaN must not reach O, so the tail step's slots are cleared
     auto clear_tail = [&](int s, uint16_t* V) {
         if constexpr (FP8) {
-            // codes [page][D][16 slots]
+            // codes [page][D][16 slots], pages PBP bytes apart
             uint8_t* Vb = (uint8_t*)V;
             for (int e = tid; e < KT; e += 256) {
                 const int key = KS * s + 16 * (e / PE) + (e & 15);
-                if (key >= L) Vb[e] = 0;
+                if (key >= L) Vb[(e / PE) * PBP + e % PE] = 0;
             }
         } else {
             for (int e = tid; e < KT; e += 256) {
@@ -442,10 +470,11 @@ prefill_attn_kernel(PrefillArgs a) {
     const int kslot = (kk & 15) ^ (((kk >> 3) & 1) << 2);
     const int k_off = (kk >> 4) * PE + hl * (kPage * 8) + kslot * 8;
     const int v_off = c * kPage + 8 * (hl ^ (((c >> 2) ^ (c >> 3)) & 1));
-    // fp8 (byte offsets): K unit (chunk kb, slot) of the key's page, codes
-    // 8 hl .. 8 hl + 7; V row (32 t + c) of page u, codes 8 hl .. 8 hl + 7
-    const int k_off8 = (kk >> 4) * PB + (kk & 15) * 16 + 8 * hl;
-    const int v_off8 = c * 16 + 8 * hl;
+    // fp8 (byte offsets): the K unit (chunk 2 m + hl, slot) of key pi8(c),
+    // and row c of V page hl, of each 32-key half
+    const int kk8 = 16 * ((c >> 2) & 1) + 8 * ((c >> 4) & 1) + 4 * ((c >> 3) & 1) + (c & 3);
+    const int k_off8 = (kk8 >> 4) * PBP + hl * 256 + ((kk8 & 15) ^ (4 * (kk8 >> 4))) * 16;
+    const int v_off8 = hl * PBP + c * 16;
     // eight codes -> eight bf16, exactly
     auto widen = [](const u32x2 w8) -> bf16x8 {
         const bf16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w8.x, 1.0f, false);
@@ -456,28 +485,45 @@ prefill_attn_kernel(PrefillArgs a) {
                                                 __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)});
     };
     auto k_operand = [&](const uint16_t* Kt, int hh, int kb) -> bf16x8 {
-        if constexpr (FP8)
-            return widen(*(const u32x2*)((const char*)Kt + hh * 2 * PB + kb * 256 + k_off8));
-        else
-            return *(const bf16x8*)(Kt + k_off + hh * 2 * PE + kb * (2 * kPage * 8));
+        return *(const bf16x8*)(Kt + k_off + hh * 2 * PE + kb * (2 * kPage * 8));
     };
     auto v_operand = [&](const uint16_t* Vt0, int hh, int u, int t) -> bf16x8 {
-        if constexpr (FP8)
-            return widen(*(const u32x2*)((const char*)Vt0 + (hh * 2 + u) * PB + (32 * t) * 16 + v_off8));
-        else
-            return *(const bf16x8*)(Vt0 + v_off + hh * 2 * PE + (u * D + 32 * t) * kPage);
+        return *(const bf16x8*)(Vt0 + v_off + hh * 2 * PE + (u * D + 32 * t) * kPage);
+    };
+    // fp8: the 16-byte unit of K pair m, and row 32 t + c of V, of half hh
+    auto k_unit8 = [&](const uint16_t* Kt, int hh, int m) -> u32x4 {
+        return *(const u32x4*)((const char*)Kt + hh * 2 * PBP + m * 512 + k_off8);
+    };
+    auto v_row8 = [&](const uint16_t* Vt0, int hh, int t) -> u32x4 {
+        return *(const u32x4*)((const char*)Vt0 + hh * 2 * PBP + (32 * t) * 16 + v_off8);
     };
 
     auto qk = [&](const uint16_t* Kt, f32x16 (&sc)[NH]) {
 #pragma unroll
         for (int hh = 0; hh < NH; ++hh) sc[hh] = f32x16{};
+        if constexpr (FP8) {
 #pragma unroll
-        for (int kb = 0; kb < D / 16; ++kb)
+            for (int m = 0; m < D / 32; ++m) {
+                u32x4 ku[NH];
 #pragma unroll
-            for (int hh = 0; hh < NH; ++hh) {
-                const bf16x8 ka = k_operand(Kt, hh, kb);
-                sc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc[hh], 0, 0, 0);
+                for (int hh = 0; hh < NH; ++hh) ku[hh] = k_unit8(Kt, hh, m);
+#pragma unroll
+                for (int e = 0; e < 2; ++e)
+#pragma unroll
+                    for (int hh = 0; hh < NH; ++hh) {
+                        const bf16x8 ka = widen(e ? u32x2{ku[hh].z, ku[hh].w} : u32x2{ku[hh].x, ku[hh].y});
+                        sc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[2 * m + e], sc[hh], 0, 0, 0);
+                    }
             }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < D / 16; ++kb)
+#pragma unroll
+                for (int hh = 0; hh < NH; ++hh) {
+                    const bf16x8 ka = k_operand(Kt, hh, kb);
+                    sc[hh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qv[kb], sc[hh], 0, 0, 0);
+                }
+        }
     };
 
     // prologue: K and V of step 0, K of step 1, S of step 0
@@ -523,7 +569,7 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
                     for (int j = 0; j < 16; ++j) {
-                        const int key = KS * s + 32 * hh + 16 * (j >> 3) + 8 * hl + (j & 7);
+                        const int key = KS * s + 32 * hh + (j & 7) + (FP8 ? 16 * hl + 8 * (j >> 3) : 16 * (j >> 3) + 8 * hl);
                         sc[hh][j] = key <= pos ? sc[hh][j] : -INFINITY;
                     }
             }
@@ -561,37 +607,60 @@ prefill_attn_kernel(PrefillArgs a) {
             l += psum;
             // K reads run two MFMAs ahead of the S MFMAs, with the softmax
             // VALU work spread between them
+            // (fp8: one K read per two MFMAs)
+            constexpr int KR = FP8 ? 2 : 1;
             __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
             for (int i = 0; i < 8 * NH; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // an MFMA of S
-                if (i + 2 < 8 * NH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // a K read
+                if (i % KR == KR - 1 && i / KR + 2 < 8 * NH / KR)
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // a K read
                 __builtin_amdgcn_sched_group_barrier(0x002, kValuPerMfma, 0);   // softmax VALU
             }
-            // O^T += V^T P^T, per 16-key page u of each half and 32-dim tile t
+            // O^T += V^T P^T, per 16-key group u of each half and 32-dim tile t
+            // (bf16: group u is page u; fp8: keys 8 u .. 8 u + 7 of the
+            // lane's page, both groups from one 16-byte V row)
+            auto p_operand = [](const uint32_t (&p)[8], int u) {
+                return __builtin_bit_cast(bf16x8, u32x4{p[4 * u], p[4 * u + 1], p[4 * u + 2], p[4 * u + 3]});
+            };
+            if constexpr (FP8) {
 #pragma unroll
-            for (int hh = 0; hh < NH; ++hh)
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const bf16x8 bh = __builtin_bit_cast(
-                        bf16x8, u32x4{ph[hh][4 * u], ph[hh][4 * u + 1], ph[hh][4 * u + 2], ph[hh][4 * u + 3]});
-                    const bf16x8 bl = __builtin_bit_cast(
-                        bf16x8, u32x4{pl[hh][4 * u], pl[hh][4 * u + 1], pl[hh][4 * u + 2], pl[hh][4 * u + 3]});
+                for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
                     for (int t = 0; t < D / 32; ++t) {
-                        const bf16x8 va = v_operand(v_rd, hh, u, t);
-                        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
-                        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                        const u32x4 vr = v_row8(v_rd, hh, t);
+#pragma unroll
+                        for (int u = 0; u < 2; ++u) {
+                            const bf16x8 va = widen(u ? u32x2{vr.z, vr.w} : u32x2{vr.x, vr.y});
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p_operand(ph[hh], u), o[t], 0, 0, 0);
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p_operand(pl[hh], u), o[t], 0, 0, 0);
+                        }
                     }
-                }
-            // V reads run four MFMAs ahead of the PV MFMAs
-            constexpr int MF = 2;
-            constexpr int NV = 2 * NH * (D / 32);
-            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+            } else {
+#pragma unroll
+                for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const bf16x8 bh = p_operand(ph[hh], u);
+                        const bf16x8 bl = p_operand(pl[hh], u);
+#pragma unroll
+                        for (int t = 0; t < D / 32; ++t) {
+                            const bf16x8 va = v_operand(v_rd, hh, u, t);
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                        }
+                    }
+            }
+            // V reads run four MFMAs ahead of the PV MFMAs (fp8: two reads,
+            // each feeding four)
+            constexpr int MF = FP8 ? 4 : 2;
+            constexpr int NV = (FP8 ? 1 : 2) * NH * (D / 32);
+            constexpr int VA = FP8 ? 2 : 4;
+            __builtin_amdgcn_sched_group_barrier(0x100, VA, 0);
 #pragma unroll
             for (int i = 0; i < NV; ++i) {
                 __builtin_amdgcn_sched_group_barrier(0x008, MF, 0);
-                if (i + 4 < NV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                if (i + VA < NV) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
             }
         }
         if (more_v) {
