@@ -235,6 +235,24 @@ def test_edge_shapes(B, Hq, Hkv, D, lens, kv):
                 assert np.all(got[b] == 0.0)
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_negative_zero_and_sharp_scales(kv):
+    # the softmax scale is any finite number: negative (the scores' order
+    # reverses), zero (uniform weights: the mean of the visible values) and
+    # four times the usual 1/sqrt(D) (peaked weights).  Much sharper weights
+    # make each output one value row, whose own bf16 rounding (half an ulp of
+    # values up to ~11 in the fp8 case) alone reaches the max-abs bound.
+    B, Hq, Hkv, D, lens = 3, 16, 2, 128, [1, 77, 900]
+    rng = np.random.default_rng(4242)
+    case = dn.random_case(rng, B, Hq, Hkv, D, lens, kv)
+    s0 = float(np.float32(1.0 / np.sqrt(D)))
+    for scale in (-s0, 0.0, 4 * s0):
+        ref = oracle_case(case, scale, kv)
+        for waves in (0, 7):
+            got = run_case(dev_case(case, kv), scale, max_waves=waves)
+            G.assert_close(got, ref, kv, f"scale {scale} {kv} waves={waves}")
+
+
 def _sweep_lengths(rng, B):
     """Lengths that land on and next to page (16) and four-page (64) step
     boundaries, plus empty and one-token requests and arbitrary ones."""

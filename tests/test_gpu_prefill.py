@@ -145,6 +145,24 @@ def test_prefill_matches_oracle(case, kv):
     assert_close(_out_f64(out), ref, "bf16", f"{name} {kv}")
 
 
+@pytest.mark.parametrize("kv", ["bf16", "fp8"])
+def test_prefill_negative_zero_and_sharp_scales(kv):
+    # any finite softmax scale: negative (the kernel flips the query's signs),
+    # zero (uniform weights over each row's visible keys) and four times the
+    # usual 1/sqrt(D) (much sharper weights leave single value rows, whose
+    # own bf16 rounding reaches the max-abs bound)
+    cached, new, H_q, H_kv, D = [0, 40], [150, 90], 8, 2, 128
+    for scale in (-0.0884, 0.0, 0.3536):
+        w = wl.build_prefill(cached=cached, new=new, H_q=H_q, H_kv=H_kv, D=D, seed=77, device="cuda", kv=kv)
+        w.scale = scale
+        _write(w)
+        out = torch.full((w.T, H_q, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+        _attend(w, w.q, out)
+        assert bl.device_errors() == 0
+        kp, vp = _host_pools(w)
+        assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16", f"scale {scale} {kv}")
+
+
 def _sweep_counts(rng, B, edge):
     out = []
     for _ in range(B):
