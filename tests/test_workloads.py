@@ -81,3 +81,42 @@ def test_fp8_workload_small_pool():
     finite = vals[torch.isfinite(vals)]
     assert finite.abs().max() <= 448.0
     assert w.k_new.dtype == torch.uint8
+
+
+def test_fp8_prompt_batch():
+    # fp8 prompt batches: code pools in the decode layout, per-(request, head)
+    # scales set by the cached tokens (1 where none is cached), the new rows
+    # quantised at those scales, and empty slots holding the NaN code
+    cached, new = [0, 33, 200], [40, 17, 128]
+    w = wl.build_prefill(cached=cached, new=new, H_q=8, H_kv=2, D=128, seed=3, kv="fp8")
+    assert w.kv == "fp8"
+    assert w.k_pages.dtype == torch.uint8 and w.k_pages.shape[1:] == (2, 8, 16, 16)
+    assert w.v_pages.dtype == torch.uint8 and w.v_pages.shape[1:] == (2, 128, 16)
+    assert w.k_new.dtype == torch.uint8 and w.k_new.shape == (sum(new), 2, 128)
+    assert w.k_scale.shape == (3, 2) and w.v_scale.shape == (3, 2)
+    assert torch.all(w.k_scale[0] == 1.0) and torch.all(w.v_scale[0] == 1.0)
+    assert torch.all(w.k_scale[1:] > 0) and torch.all(w.k_scale[1:] < 1.0)
+    # cached slots of request 1: every code finite, and the amax code of each
+    # head is the largest finite e4m3fn value (scale = amax / 448)
+    bt = w.block_table.cpu().numpy()
+    kp = w.k_pages.view(torch.float8_e4m3fn).float()
+    for g in range(2):
+        vals = torch.cat([kp[bt[1, p], g].permute(1, 0, 2).reshape(16, -1) for p in range(3)])[:33]
+        assert torch.isfinite(vals).all()
+        assert vals.abs().max() == 448.0
+    # slots past every request's cached length hold the NaN code
+    filled = set()
+    for b, c in enumerate(cached):
+        for t in range(c):
+            filled.add((int(bt[b, t // 16]), t % 16))
+    kc = w.k_pages.cpu().numpy()
+    for p in range(w.k_pages.shape[0]):
+        for sl in range(16):
+            if (p, sl) not in filled:
+                assert np.all(kc[p, :, :, sl, :] == wl.FP8_NAN_CODE)
+    # the new rows: codes of N(0,1) values at the request's scale, so the
+    # dequantised rows have unit-order spread
+    kn = w.k_new.view(torch.float8_e4m3fn).float()
+    rows = torch.repeat_interleave(torch.arange(3), torch.tensor(new))
+    deq = kn * w.k_scale[rows][:, :, None]
+    assert torch.isfinite(deq).all() and 0.5 < float(deq.std()) < 2.0
