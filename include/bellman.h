@@ -269,10 +269,11 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *                0 or ends past T writes no row at all (flag 2).
  * Each workgroup takes 128 query rows of one request and one query head;
  * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo (P
- * rounded to bf16 once would spend the bf16 error budget); fp8 codes are
- * staged in LDS as bytes and widened to bf16 exactly at the operand load,
- * the K scale folded into the softmax scale and the V scale into the final
- * normalisation.  Scratch: B + 1
+ * rounded to bf16 once would spend the bf16 error budget).  fp8 codes are
+ * staged in LDS as bytes and widened exactly at the operand load: K to bf16
+ * for QK^T, V to fp16 for a single-pass fp16 PV (P rounded to fp16 keeps 11
+ * significant bits); the K scale folds into the softmax scale and the V
+ * scale into the final normalisation.  Scratch: B + 1
  * integers of the per-device workspace.  Like bellman_kv_write, once the
  * workspace has grown to the call's size the call enqueues only kernels
  * (graph-capturable). */

@@ -25,6 +25,8 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float swap_halves(float x) {  // value of lane l ^ 32
     const unsigned u = __float_as_uint(x);
@@ -289,7 +291,10 @@ constexpr int kValuPerMfma = 7;
 //    2 m + e; the query operand of MFMA 2 m + e holds dims 32 m + 16 h + 8 e.
 //  * PV: lane (h, c) reads row 32 t + c of page h of the half (16 keys) and
 //    takes keys 8 e .. 8 e + 7 into MFMA e, whose P operand is then exactly
-//    the lane's probabilities of group e.
+//    the lane's probabilities of group e.  PV runs in fp16, one pass: the
+//    codes (at most 448 in magnitude, subnormals from 2^-9) are exact in
+//    fp16, and P (below 2^8 with the lazy max) keeps 11 significant bits
+//    there, against the bf16 hi + lo pair's two passes.
 // Pages sit PB + 128 bytes apart in LDS and odd pages hold K slot s at
 // s ^ 4, so every 8 (and 16) consecutive lanes of a read touch distinct
 // banks.
@@ -484,6 +489,15 @@ prefill_attn_kernel(PrefillArgs a) {
         return __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1),
                                                 __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)});
     };
+    // eight codes -> eight fp16, exactly
+    auto widen16 = [](const u32x2 w8) -> f16x8 {
+        const f16x2 p0 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w8.x, 1.0f, false);
+        const f16x2 p1 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w8.x, 1.0f, true);
+        const f16x2 p2 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w8.y, 1.0f, false);
+        const f16x2 p3 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w8.y, 1.0f, true);
+        return __builtin_bit_cast(f16x8, u32x4{__builtin_bit_cast(uint32_t, p0), __builtin_bit_cast(uint32_t, p1),
+                                               __builtin_bit_cast(uint32_t, p2), __builtin_bit_cast(uint32_t, p3)});
+    };
     auto k_operand = [&](const uint16_t* Kt, int hh, int kb) -> bf16x8 {
         return *(const bf16x8*)(Kt + k_off + hh * 2 * PE + kb * (2 * kPage * 8));
     };
@@ -597,12 +611,16 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int j = 0; j < 16; j += 2) {
                     const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j], sl, -m)),
                                       __builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j + 1], sl, -m))};
-                    const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
-                    ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
-                    // the remainder is exact in fp32, then rounded again
                     psum += pq.x + pq.y;
-                    pl[hh][j / 2] = __builtin_bit_cast(
-                        uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
+                    if constexpr (FP8) {
+                        ph[hh][j / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pq, f16x2));
+                    } else {
+                        const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
+                        ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
+                        // the remainder is exact in fp32, then rounded again
+                        pl[hh][j / 2] = __builtin_bit_cast(
+                            uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
+                    }
                 }
             l += psum;
             // K reads run two MFMAs ahead of the S MFMAs, with the softmax
@@ -631,9 +649,10 @@ prefill_attn_kernel(PrefillArgs a) {
                         const u32x4 vr = v_row8(v_rd, hh, t);
 #pragma unroll
                         for (int u = 0; u < 2; ++u) {
-                            const bf16x8 va = widen(u ? u32x2{vr.z, vr.w} : u32x2{vr.x, vr.y});
-                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p_operand(ph[hh], u), o[t], 0, 0, 0);
-                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, p_operand(pl[hh], u), o[t], 0, 0, 0);
+                            const f16x8 va = widen16(u ? u32x2{vr.z, vr.w} : u32x2{vr.x, vr.y});
+                            const f16x8 pa = __builtin_bit_cast(
+                                f16x8, u32x4{ph[hh][4 * u], ph[hh][4 * u + 1], ph[hh][4 * u + 2], ph[hh][4 * u + 3]});
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pa, o[t], 0, 0, 0);
                         }
                     }
             } else {
@@ -652,8 +671,8 @@ prefill_attn_kernel(PrefillArgs a) {
                     }
             }
             // V reads run four MFMAs ahead of the PV MFMAs (fp8: two reads,
-            // each feeding four)
-            constexpr int MF = FP8 ? 4 : 2;
+            // each feeding two)
+            constexpr int MF = 2;
             constexpr int NV = (FP8 ? 1 : 2) * NH * (D / 32);
             constexpr int VA = FP8 ? 2 : 4;
             __builtin_amdgcn_sched_group_barrier(0x100, VA, 0);
