@@ -268,14 +268,20 @@ int bellman_kv_write(const bellman_tensor_t *k_new, const bellman_tensor_t *v_ne
  *                table: flag 2) are not written; a q_start that decreases, starts below
  *                0 or ends past T writes no row at all (flag 2).
  * Each workgroup takes 128 query rows of one request and one query head;
- * QK^T and PV run on the matrix cores with P carried in bf16 hi + lo (P
- * rounded to bf16 once would spend the bf16 error budget).  fp8 codes are
- * staged in LDS as bytes and widened exactly at the operand load: K to bf16
- * for QK^T, V to fp16 for a single-pass fp16 PV (P rounded to fp16 keeps 11
- * significant bits); the K scale folds into the softmax scale and the V
- * scale into the final normalisation.  Scratch: B + 1
- * integers of the per-device workspace.  Like bellman_kv_write, once the
- * workspace has grown to the call's size the call enqueues only kernels
+ * QK^T runs on the bf16 matrix cores and PV on the fp16 ones, in one pass
+ * with P rounded to fp16 (11 significant bits; P rounded to bf16 once would
+ * spend the bf16 error budget).  Over bf16 pools the values the call reads
+ * are first copied into the workspace as fp16, each (request, KV head) at
+ * the power of two 2^e that brings its largest magnitude M into
+ * [2^14, 2^15): every value of at least M 2^-28 converts exactly, none
+ * overflows, and the output is scaled back by 2^-e.  Over fp8 pools the
+ * codes are staged in LDS as bytes and widened exactly at the operand load
+ * (K to bf16, V to fp16); the K scale folds into the softmax scale and the
+ * V scale into the final normalisation.  Scratch in the per-device
+ * workspace: 2 (B + 1) + B H_kv integers, and over bf16 pools B maxP
+ * (4 + 4 H_kv + 32 D H_kv) bytes more for the value copy and its
+ * bookkeeping (maxP = the block table's width).  Like bellman_kv_write, once
+ * the workspace has grown to the call's size the call enqueues only kernels
  * (graph-capturable). */
 int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t *k_pages,
                               const bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
@@ -283,8 +289,9 @@ int bellman_prefill_attention(const bellman_tensor_t *q, const bellman_tensor_t 
                               float scale, bellman_tensor_t *out, void *stream);
 
 typedef struct bellman_prefill_opts {
-    void *event_begin;    /* optional hipEvent_t recorded before the attention kernels */
-    void *event_end;      /* optional hipEvent_t recorded after them */
+    void *event_begin;    /* optional hipEvent_t recorded right before the attention
+                             kernel (after the planning and value-copy kernels) */
+    void *event_end;      /* optional hipEvent_t recorded right after it */
 } bellman_prefill_opts_t;
 
 /* bellman_prefill_attention with options (NULL = defaults). */

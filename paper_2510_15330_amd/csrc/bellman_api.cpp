@@ -9,6 +9,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -644,11 +645,28 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
         return fail(BELLMAN_ERR_UNSUPPORTED, "too many query tiles x heads");
     if (T == 0 || B == 0) return BELLMAN_OK;
 
+    // bf16 pools: the fp16 copy of the values holds at most every table page
+    // of every request (B x maxP pages of H_kv heads)
+    const int64_t max_pages = block_table->shape[1];
+    const size_t page_head_bytes = (size_t)ps.D * 16 * 2;
+    if (!ps.fp8 && (double)B * (double)max_pages >= 2147483647.0)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "batch x block-table width must stay below 2^31 pages");
+    const size_t copy_bytes = ps.fp8 ? 0 : (size_t)B * (size_t)max_pages * (size_t)ps.H_kv * page_head_bytes;
+    if (!ps.fp8 && (double)B * (double)max_pages * ps.H_kv * (double)page_head_bytes > 1099511627776.0)
+        return fail(BELLMAN_ERR_UNSUPPORTED, "the fp16 value copy of B x maxP pages would exceed 1 TiB");
+    const size_t off_tiles = kWsHeader;
+    const size_t off_pages = off_tiles + align256((size_t)(B + 1) * 4);
+    const size_t off_req = off_pages + align256((size_t)(B + 1) * 4);
+    const size_t off_tmax = off_req + align256(ps.fp8 ? 0 : (size_t)B * (size_t)max_pages * 4);
+    const size_t off_vmax = off_tmax + align256(ps.fp8 ? 0 : (size_t)B * (size_t)max_pages * ps.H_kv * 4);
+    const size_t off_copy = off_vmax + align256((size_t)B * ps.H_kv * 4);
+    const size_t total = off_copy + align256(copy_bytes);
+
     int dev;
     if ((rc = current_device(&dev))) return rc;
     hipStream_t s = (hipStream_t)stream;
     char* base;
-    if ((rc = ensure_workspace(dev, kWsHeader + align256((size_t)(B + 1) * 4), s, &base))) return rc;
+    if ((rc = ensure_workspace(dev, total, s, &base))) return rc;
     int32_t* err;
     if ((rc = device_error_word(dev, &err))) return rc;
     PrefillArgs a;
@@ -675,17 +693,27 @@ int bellman_prefill_attention_opts(const bellman_tensor_t* q, const bellman_tens
     a.H_kv = ps.H_kv;
     a.G = (int)(H_q / ps.H_kv);
     a.D = ps.D;
-    a.max_pages = (int)block_table->shape[1];
+    a.max_pages = (int)max_pages;
     a.err = err;
-    a.tile_start = (int32_t*)(base + kWsHeader);
+    a.tile_start = (int32_t*)(base + off_tiles);
     a.fp8 = ps.fp8 ? 1 : 0;
     a.k_scale = k_pages->dequant_scale;
     a.v_scale = v_pages->dequant_scale;
+    a.page_off = (int32_t*)(base + off_pages);
+    a.page_req = (int32_t*)(base + off_req);
+    a.tmax = (float*)(base + off_tmax);
+    a.vmax = (uint32_t*)(base + off_vmax);
+    a.vcopy = (uint16_t*)(base + off_copy);
+    // enough waves for every (page, head) tile of B x maxP pages at most
+    // once, and at most 2048 workgroups
+    a.vgrid = (int)std::max<int64_t>(1, std::min<int64_t>(2048, ((int64_t)B * max_pages * ps.H_kv + 3) / 4));
+    launch_prefill_prep(a, s);
+    if ((rc = launch_status("prefill_attention (planning)"))) return rc;
     if (opts && opts->event_begin) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_begin, s);
         if (e != hipSuccess) return fail(BELLMAN_ERR_HIP, "hipEventRecord: %s", hipGetErrorString(e));
     }
-    launch_prefill(a, s);
+    launch_prefill_attn(a, s);
     if ((rc = launch_status("prefill_attention"))) return rc;
     if (opts && opts->event_end) {
         hipError_t e = hipEventRecord((hipEvent_t)opts->event_end, s);

@@ -114,6 +114,13 @@ struct PrefillArgs {
     int fp8;               // pools of e4m3fn codes with the dequantisation scales below
     const float* k_scale;  // fp8 only, fp32 [B, H_kv]
     const float* v_scale;
+    // bf16 pools: the fp16 copy of the values the attention reads (workspace)
+    int32_t* page_off;     // [B + 1]: first copied page of each request
+    int32_t* page_req;     // [B * maxP]: the request of each copied page
+    float* tmax;           // [copied pages, H_kv]: the largest |v| of each (page, head) tile
+    uint32_t* vmax;        // [B, H_kv]: float bits of the largest |v| of each (request, KV head)
+    uint16_t* vcopy;       // [sum of copied pages, H_kv, D, 16] fp16
+    int vgrid;             // workgroups of the copy passes (4 waves each)
 };
 
 // Launchers (kernels.hip).  They only enqueue; errors come back through
@@ -127,7 +134,10 @@ int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 void launch_merge(const AttnArgs& a, hipStream_t s);
 // Prefill launchers (prefill.hip).
 void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s);
-void launch_prefill(const PrefillArgs& a, hipStream_t s);
+// The prompt attention's planning (and, over bf16 pools, the fp16 value
+// copy), then the attention kernel itself.
+void launch_prefill_prep(const PrefillArgs& a, hipStream_t s);
+void launch_prefill_attn(const PrefillArgs& a, hipStream_t s);
 
 // Page-pattern gather probe (probe.hip): n tiles of tile_bytes, n a power of
 // two; nonzero if tile_bytes is not a built size.

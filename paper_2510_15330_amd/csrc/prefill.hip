@@ -206,9 +206,16 @@ __device__ __forceinline__ int tiles_of(const PrefillArgs& a, int b) {
     return (n + kPrefillRows - 1) / kPrefillRows;
 }
 
+// pages of request b whose values the attention reads: all ceil(L_b / 16)
+// when it has query tiles, none otherwise
+__device__ __forceinline__ int vpages_of(const PrefillArgs& a, int b) {
+    return tiles_of(a, b) > 0 ? (a.seq_lens[b] + kPage - 1) / kPage : 0;
+}
+
 __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs a) {
     __shared__ int part[kPlanThreads];
     __shared__ int malformed;
+    __shared__ int total_pages;
     const int tid = threadIdx.x;
     if (tid == 0) malformed = (a.q_start[0] < 0 || a.q_start[a.B] > a.T) ? 1 : 0;
     __syncthreads();
@@ -225,6 +232,37 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
     }
     if (bad) atomicOr(a.err, kErrLength);
     const int incl = block_scan(sum, part);
+    if (!a.fp8) {
+        // bf16 pools: the pages the value copy holds (every page of a request
+        // with query tiles, none of the others; none at all when malformed)
+        int pages = 0;
+        for (int k = 0; k < per; ++k)
+            if (b0 + k < a.B && !malformed) pages += vpages_of(a, b0 + k);
+        const int pincl = block_scan(pages, part);
+        int prun = pincl - pages;
+        for (int k = 0; k < per; ++k) {
+            const int b = b0 + k;
+            if (b < a.B) {
+                a.page_off[b] = prun;
+                prun += malformed ? 0 : vpages_of(a, b);
+            }
+        }
+        if (tid == kPlanThreads - 1) {
+            a.page_off[a.B] = pincl;
+            total_pages = pincl;
+        }
+        __syncthreads();   // page_off is read back below by every thread
+        // the request of every copied page: the last b with page_off[b] <= p
+        for (int p = tid; p < total_pages; p += kPlanThreads) {
+            int lo = 0, hi = a.B - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (a.page_off[mid] <= p) lo = mid;
+                else hi = mid - 1;
+            }
+            a.page_req[p] = lo;
+        }
+    }
     if (malformed) {
         for (int k = 0; k < per; ++k)
             if (b0 + k < a.B) a.tile_start[b0 + k] = 0;
@@ -243,6 +281,125 @@ __global__ void __launch_bounds__(kPlanThreads) prefill_plan_kernel(PrefillArgs 
         }
     }
     if (tid == kPlanThreads - 1) a.tile_start[a.B] = incl;
+}
+
+// ------------------------------------------------ fp16 copy of bf16 values --
+// Over bf16 pools PV runs in fp16, in one pass (P, below 2^8, keeps 11
+// significant bits in fp16; rounded to bf16 once it would spend the bf16
+// error budget).  Each (request, KV head)'s values are copied into the
+// workspace as fp16 at a power-of-two scale 2^e that puts their largest
+// magnitude M in [2^14, 2^15): bf16's 8 significant bits fit fp16's 11, so
+// every value of at least M 2^-28 converts exactly and none overflows, and
+// the rest keep an absolute error below M 2^-40.  The copy keeps the pool's
+// page layout [page][D][16 slots], a request's pages consecutive from
+// page_off[b], slots past its length zero.  Three passes, none with
+// atomics: vmax_kernel takes the largest magnitude of every (page, head)
+// tile, vreduce_kernel M of every (request, KV head), and vcopy_kernel
+// writes the copy.
+
+// the scale exponent e for a largest magnitude whose float bits are mb
+// (e = 0 when every value is zero or the maximum is not finite)
+__device__ __forceinline__ int vcopy_exp(uint32_t mb) {
+    if (mb == 0u || mb >= 0x7f800000u) return 0;
+    const int E = max((int)(mb >> 23), 1);          // floor(log2 M) + 127
+    return min(max(141 - E, -126), 126);
+}
+__device__ __forceinline__ float pow2f(int e) {   // 2^e, -126 <= e <= 127
+    return __uint_as_float((uint32_t)(e + 127) << 23);
+}
+
+// The copy passes run a fixed grid of waves over the flat (page, KV head)
+// tiles of all requests; page p of the copy belongs to request page_req[p]
+// (written by the planner).  Each lane takes 4 (D = 128) or 2 16-byte units
+// (8 slots of one dim row) of a tile, all loaded before any is used.
+template <int D>
+struct VTile {
+    static constexpr int U = 2 * D / 64;   // units per lane
+    int b, j, g, pg, L;
+    u32x4 w[U];
+    // load tile t (p = t / H_kv, g = t % H_kv); slots past the length read as 0
+    __device__ __forceinline__ void load(const PrefillArgs& a, int64_t t, int lane) {
+        const int64_t p = t / a.H_kv;
+        g = (int)(t % a.H_kv);
+        b = a.page_req[p];
+        j = (int)(p - a.page_off[b]);
+        L = a.seq_lens[b];
+        pg = a.block_table[(int64_t)b * a.bt_stride + j];
+        const bool ok = (unsigned)pg < (unsigned)a.num_pages;
+        const uint16_t* src = (const uint16_t*)a.v_pages + ((int64_t)(ok ? pg : 0) * a.H_kv + g) * (D * kPage);
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int r = 64 * k + lane, s0 = 8 * (r & 1);
+            w[k] = (ok && L - kPage * j - s0 > 0) ? *(const u32x4*)(src + (r >> 1) * kPage + s0) : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    // value i of unit k, 0 past the length
+    __device__ __forceinline__ float value(int k, int i, int lane) const {
+        const int r = 64 * k + lane, live = L - kPage * j - 8 * (r & 1);
+        const uint32_t bits = (i & 1) ? (w[k][i >> 1] & 0xffff0000u) : (w[k][i >> 1] << 16);
+        return i < live ? __uint_as_float(bits) : 0.f;
+    }
+};
+
+__device__ __forceinline__ int64_t vcopy_tiles(const PrefillArgs& a) {
+    return (int64_t)a.page_off[a.B] * a.H_kv;
+}
+
+// largest |v| of each (page, head) tile, in tmax[tile]
+template <int D>
+__global__ void __launch_bounds__(256) vmax_kernel(PrefillArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * 4, n = vcopy_tiles(a);
+    for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < n; t += waves) {
+        VTile<D> v;
+        v.load(a, t, lane);
+        float m = 0.f;
+#pragma unroll
+        for (int k = 0; k < VTile<D>::U; ++k)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(v.value(k, i, lane)));
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+        if (lane == 0) a.tmax[t] = m;
+    }
+}
+
+// one wave per (request, KV head): vmax = float bits of the largest tile
+// maximum over the request's pages (0 for a request without copied pages)
+__global__ void __launch_bounds__(256) vreduce_kernel(PrefillArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= (int64_t)a.B * a.H_kv) return;
+    const int b = (int)(i / a.H_kv), g = (int)(i % a.H_kv);
+    const int p0 = a.page_off[b], np = a.page_off[b + 1] - p0;
+    float m = 0.f;
+    for (int j = lane; j < np; j += 64) m = fmaxf(m, a.tmax[((int64_t)p0 + j) * a.H_kv + g]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+    if (lane == 0) a.vmax[i] = __float_as_uint(m);
+}
+
+template <int D>
+__global__ void __launch_bounds__(256) vcopy_kernel(PrefillArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t waves = (int64_t)gridDim.x * 4, n = vcopy_tiles(a);
+    for (int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < n; t += waves) {
+        VTile<D> v;
+        v.load(a, t, lane);
+        const float sc = pow2f(vcopy_exp(a.vmax[(int64_t)v.b * a.H_kv + v.g]));
+        uint16_t* dst = a.vcopy + t * (int64_t)(D * kPage);   // tile t = (page, head) of the copy
+#pragma unroll
+        for (int k = 0; k < VTile<D>::U; ++k) {
+            const int r = 64 * k + lane;
+            u32x4 h;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const f32x2 x = {v.value(k, 2 * i, lane) * sc, v.value(k, 2 * i + 1, lane) * sc};
+                h[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, f16x2));   // round to nearest even
+            }
+            *(u32x4*)(dst + (r >> 1) * kPage + 8 * (r & 1)) = h;
+        }
+    }
 }
 
 // -------------------------------------------------------------- attention --
@@ -399,6 +556,10 @@ prefill_attn_kernel(PrefillArgs a) {
     const char* kbase = (const char*)a.k_pages + (int64_t)g * PB;
     const char* vbase = (const char*)a.v_pages + (int64_t)g * PB;
     const int64_t page_bytes = (int64_t)a.H_kv * PB;
+    // bf16 pools: the values come from the fp16 copy, whose pages of request
+    // b are consecutive from page_off[b] (same bytes per page as bf16)
+    const char* vbase16 = FP8 ? nullptr : (const char*)a.vcopy + (int64_t)g * PB;
+    const int64_t vpb = FP8 ? 0 : (int64_t)a.page_off[b];
     int64_t off1[PPS], off2[PPS];      // page byte offsets of steps s + 1 and s + 2
     auto pages_of = [&](int j, int64_t (&off)[PPS]) {
         const int e = PPS * (j % WIN);
@@ -448,6 +609,19 @@ prefill_attn_kernel(PrefillArgs a) {
             const int v = ((256 * k + 64 * w) % UPP) + lane;          // LDS unit within its page
             const int vg = FP8 ? v : isv ? v ^ (((v >> 3) ^ (v >> 4)) & 1) : v ^ (((v >> 3) & 1) << 2);
             __builtin_amdgcn_global_load_lds(base + o_pg + vg * 16, dst + 8 * (256 * k + 64 * w), 16, 0, 0);
+        }
+    };
+    // the fp16 value copy of step j (bf16 pools), laid out and swizzled as V;
+    // a step past the request's pages re-reads its last page
+    auto dma_v16 = [&](int j, uint16_t* dst) {
+#pragma unroll
+        for (int k = 0; k < PERH; ++k) {
+            constexpr int BPP = 256 / UPP;
+            const int pp = (256 * k) / UPP + (BPP == 2 ? (w >> 1) : 0);
+            const int64_t o_pg = (vpb + min(PPS * j + pp, np - 1)) * page_bytes;
+            const int v = ((256 * k + 64 * w) % UPP) + lane;
+            const int vg = v ^ (((v >> 3) ^ (v >> 4)) & 1);
+            __builtin_amdgcn_global_load_lds(vbase16 + o_pg + vg * 16, dst + 8 * (256 * k + 64 * w), 16, 0, 0);
         }
     };
     // V slots of keys >= L hold no token (NaN in a pool); P is 0 there, and
@@ -544,14 +718,15 @@ prefill_attn_kernel(PrefillArgs a) {
     refill(0);
     pages_of(0, off2);
     dma(kbase, off2, kb0, false);
-    dma(vbase, off2, vb0, true);
+    if constexpr (FP8) dma(vbase, off2, vb0, true);
+    else dma_v16(0, vb0);
     if (nsteps > 1) {
         pages_of(1, off1);
         dma(kbase, off1, kb1, false);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (KS > L) {
+    if (FP8 && KS > L) {   // (the fp16 copy holds zeros past the length)
         clear_tail(0, vb0);
         __syncthreads();
     }
@@ -568,13 +743,16 @@ prefill_attn_kernel(PrefillArgs a) {
         uint16_t* v_rd = P ? vb1 : vb0;   // V(s)
         uint16_t* v_wr = P ? vb0 : vb1;   // V(s + 1), over V(s - 1)
         const bool more_k = s + 2 < nsteps, more_v = s + 1 < nsteps;
-        if (more_v) dma(vbase, off1, v_wr, true);
+        if (more_v) {
+            if constexpr (FP8) dma(vbase, off1, v_wr, true);
+            else dma_v16(s + 1, v_wr);
+        }
         if (more_k) {
             if ((s + 2) % WIN == 0) refill(s + 2);
             pages_of(s + 2, off2);
             dma(kbase, off2, k_wr, false);
         }
-        uint32_t ph[NH][8], pl[NH][8];
+        uint32_t ph[NH][8];   // P as fp16 pairs
         if (s < wave_steps) {
             // keys above a column's position are masked only on the steps
             // the wave's diagonal crosses
@@ -612,15 +790,7 @@ prefill_attn_kernel(PrefillArgs a) {
                     const f32x2 pq = {__builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j], sl, -m)),
                                       __builtin_amdgcn_exp2f(__builtin_fmaf(sc[hh][j + 1], sl, -m))};
                     psum += pq.x + pq.y;
-                    if constexpr (FP8) {
-                        ph[hh][j / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pq, f16x2));
-                    } else {
-                        const bf16x2 hi2 = __builtin_convertvector(pq, bf16x2);   // round to nearest even
-                        ph[hh][j / 2] = __builtin_bit_cast(uint32_t, hi2);
-                        // the remainder is exact in fp32, then rounded again
-                        pl[hh][j / 2] = __builtin_bit_cast(
-                            uint32_t, __builtin_convertvector(pq - __builtin_convertvector(hi2, f32x2), bf16x2));
-                    }
+                    ph[hh][j / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pq, f16x2));   // RNE
                 }
             l += psum;
             // K reads run two MFMAs ahead of the S MFMAs, with the softmax
@@ -639,7 +809,7 @@ prefill_attn_kernel(PrefillArgs a) {
             // (bf16: group u is page u; fp8: keys 8 u .. 8 u + 7 of the
             // lane's page, both groups from one 16-byte V row)
             auto p_operand = [](const uint32_t (&p)[8], int u) {
-                return __builtin_bit_cast(bf16x8, u32x4{p[4 * u], p[4 * u + 1], p[4 * u + 2], p[4 * u + 3]});
+                return __builtin_bit_cast(f16x8, u32x4{p[4 * u], p[4 * u + 1], p[4 * u + 2], p[4 * u + 3]});
             };
             if constexpr (FP8) {
 #pragma unroll
@@ -650,9 +820,7 @@ prefill_attn_kernel(PrefillArgs a) {
 #pragma unroll
                         for (int u = 0; u < 2; ++u) {
                             const f16x8 va = widen16(u ? u32x2{vr.z, vr.w} : u32x2{vr.x, vr.y});
-                            const f16x8 pa = __builtin_bit_cast(
-                                f16x8, u32x4{ph[hh][4 * u], ph[hh][4 * u + 1], ph[hh][4 * u + 2], ph[hh][4 * u + 3]});
-                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pa, o[t], 0, 0, 0);
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, p_operand(ph[hh], u), o[t], 0, 0, 0);
                         }
                     }
             } else {
@@ -660,19 +828,17 @@ prefill_attn_kernel(PrefillArgs a) {
                 for (int hh = 0; hh < NH; ++hh)
 #pragma unroll
                     for (int u = 0; u < 2; ++u) {
-                        const bf16x8 bh = p_operand(ph[hh], u);
-                        const bf16x8 bl = p_operand(pl[hh], u);
+                        const f16x8 pa = p_operand(ph[hh], u);
 #pragma unroll
                         for (int t = 0; t < D / 32; ++t) {
-                            const bf16x8 va = v_operand(v_rd, hh, u, t);
-                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bh, o[t], 0, 0, 0);
-                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, bl, o[t], 0, 0, 0);
+                            const f16x8 va = __builtin_bit_cast(f16x8, v_operand(v_rd, hh, u, t));
+                            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(va, pa, o[t], 0, 0, 0);
                         }
                     }
             }
-            // V reads run four MFMAs ahead of the PV MFMAs (fp8: two reads,
-            // each feeding two)
-            constexpr int MF = 2;
+            // V reads run four MFMAs ahead of the PV MFMAs (fp8: two reads
+            // ahead, each feeding two)
+            constexpr int MF = FP8 ? 2 : 1;
             constexpr int NV = (FP8 ? 1 : 2) * NH * (D / 32);
             constexpr int VA = FP8 ? 2 : 4;
             __builtin_amdgcn_sched_group_barrier(0x100, VA, 0);
@@ -685,7 +851,7 @@ prefill_attn_kernel(PrefillArgs a) {
         if (more_v) {
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             __syncthreads();
-            if (KS * (s + 2) > L) {
+            if (FP8 && KS * (s + 2) > L) {
                 clear_tail(s + 1, v_wr);
                 __syncthreads();
             }
@@ -701,6 +867,8 @@ prefill_attn_kernel(PrefillArgs a) {
     if (bad && lane == 0) atomicOr(a.err, kErrPage);
     if (rw >= n) return;
     const float l_tot = l + swap_halves(l);
+    // fp8: the V scale; bf16: undo the value copy's 2^e
+    if constexpr (!FP8) v_scale = pow2f(-vcopy_exp(a.vmax[(int64_t)b * a.H_kv + g]));
     const float f = v_scale / l_tot;
     if (rw + c < n) {
         uint16_t* orow = a.out + (int64_t)(t0 + rw + c) * a.o_st + (int64_t)h * a.o_sh;
@@ -732,8 +900,25 @@ void launch_kv_write(const WriteArgs& a, int32_t* page_start, hipStream_t s) {
 }
 
 constexpr int kHalves = 2;   // 32-key halves per step: 64 keys, four pages
-void launch_prefill(const PrefillArgs& a, hipStream_t s) {
+void launch_prefill_prep(const PrefillArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(prefill_plan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a);
+    if (!a.fp8) {
+        const dim3 vgrid((unsigned)a.vgrid);
+        if (a.D == 128) {
+            hipLaunchKernelGGL(vmax_kernel<128>, vgrid, dim3(256), 0, s, a);
+        } else {
+            hipLaunchKernelGGL(vmax_kernel<64>, vgrid, dim3(256), 0, s, a);
+        }
+        hipLaunchKernelGGL(vreduce_kernel, dim3((unsigned)(((int64_t)a.B * a.H_kv + 3) / 4)), dim3(256), 0, s, a);
+        if (a.D == 128) {
+            hipLaunchKernelGGL(vcopy_kernel<128>, vgrid, dim3(256), 0, s, a);
+        } else {
+            hipLaunchKernelGGL(vcopy_kernel<64>, vgrid, dim3(256), 0, s, a);
+        }
+    }
+}
+
+void launch_prefill_attn(const PrefillArgs& a, hipStream_t s) {
     // an upper bound on tiles x query heads, rounded up to whole XCD rows
     const int64_t items = ((int64_t)(a.T + kPrefillRows - 1) / kPrefillRows + a.B) * a.H_q;
     const dim3 grid((unsigned)((items + kXcds - 1) / kXcds * kXcds));

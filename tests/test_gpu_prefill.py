@@ -163,6 +163,29 @@ def test_prefill_negative_zero_and_sharp_scales(kv):
         assert_close(_out_f64(out), _oracle_prefill(w, kp, vp), "bf16", f"scale {scale} {kv}")
 
 
+def test_prefill_value_magnitudes():
+    # bf16 values of each KV head at their own magnitude, 2^-100 to 2^16
+    # (past fp16's range): the fp16 value copy's per-head power-of-two scale
+    # keeps each head's output, divided by its factor, within the bound
+    factors = [2.0 ** 16, 2.0 ** -24, 1.0, 2.0 ** -100]
+    cached, new, H_q, H_kv, D = [20, 0, 300], [100, 70, 45], 8, 4, 128
+    w = wl.build_prefill(cached=cached, new=new, H_q=H_q, H_kv=H_kv, D=D, seed=5, device="cuda")
+    fac = torch.tensor(factors, dtype=torch.float32, device="cuda")
+    # powers of two: exact in bf16, and NaN poison stays NaN
+    w.v_pages.copy_((w.v_pages.float() * fac.view(1, H_kv, 1, 1)).to(torch.bfloat16))
+    w.v_new.copy_((w.v_new.float() * fac.view(1, H_kv, 1)).to(torch.bfloat16))
+    _write(w)
+    out = torch.full((w.T, H_q, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    _attend(w, w.q, out)
+    assert bl.device_errors() == 0
+    kp, vp = _host_pools(w)
+    ref = _oracle_prefill(w, kp, vp)
+    got = _out_f64(out)
+    G = H_q // H_kv
+    per_head = np.repeat(np.array(factors), G)[None, :, None]
+    assert_close(got / per_head, ref / per_head, "bf16", "per-head magnitudes")
+
+
 def _sweep_counts(rng, B, edge):
     out = []
     for _ in range(B):
