@@ -413,13 +413,13 @@ def main_prefill(args):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16/fp16",
         "data": "synthetic",
         "config": {
             "workload": args.workload, "requests": w.B, "tokens": w.T,
             "cached": [int(x) for x in w.cached], "new": [int(x) for x in w.new],
             "q_heads": w.H_q, "kv_heads": w.H_kv, "head_dim": w.D, "page_tokens": 16,
-            "kv_dtype": "fp8_e4m3fn" if args.kv == "fp8" else "bf16", "p_precision": "bf16 hi+lo", "seed": 0,
+            "kv_dtype": "fp8_e4m3fn" if args.kv == "fp8" else "bf16", "p_precision": "fp16", "seed": 0,
         },
         "attention_kernel_us": {
             "mean": round(r["kt"].mean() * 1e6, 2),
@@ -432,8 +432,9 @@ def main_prefill(args):
             "unit": "TFLOP/s",
             "frac": round(r["kernel_tflops"] / PEAK_BF16_TFLOPS, 4),
             "traffic": None,
-            "kernel": "prefill_attn_kernel (causal prompt attention, bf16 matrix cores"
-                      + (", fp8 codes widened to bf16 in registers)" if args.kv == "fp8" else ")"),
+            "kernel": "prefill_attn_kernel (causal prompt attention: QK^T on bf16 matrix cores, PV on fp16 ones"
+                      + (", fp8 codes widened exactly in registers)" if args.kv == "fp8"
+                         else ", over the fp16 value copy)"),
             "flops_per_launch": int(r["flops"]),
         },
     }
