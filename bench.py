@@ -56,12 +56,14 @@ def pct(a, q):
     return round(float(np.percentile(a, q)) * 1e6, 2)
 
 
-def decode_run(w, steps, warmup, **kw):
+def decode_run(w, steps, warmup, fused=False, **kw):
     """Warm up, reset the lengths, and time `steps` decode steps of `w`.
 
     Per step, two HIP events the library records bracket the attention
     kernel, and torch events on the same stream bracket the whole step
-    (append + attention + merge) and the attention call (kernel + merge)."""
+    (append + attention + merge) and the attention call (kernel + merge).
+    fused: each step is one bellman_decode_step call (the append inside the
+    attention kernel) instead of bellman_kv_append + bellman_decode_attention."""
     import torch
 
     import paper_2510_15330_amd as bl
@@ -73,9 +75,13 @@ def decode_run(w, steps, warmup, **kw):
     def step(i, kev=None, cev=None):
         if cev is not None:
             cev[0].record(stream)
-        bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
-        bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
-                            stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, events=kev, **kw)
+        if fused:
+            bl.decode_step(w.k_new[i], w.v_new[i], w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens,
+                           w.scale, out, stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, events=kev, **kw)
+        else:
+            bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, stream=stream)
+            bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
+                                stream=stream, k_scale=w.k_scale, v_scale=w.v_scale, events=kev, **kw)
         if cev is not None:
             cev[1].record(stream)
 
@@ -151,11 +157,11 @@ def wave_times_run(w, step=0, **kw):
     }
 
 
-def graph_run(w, steps, reps=3):
+def graph_run(w, steps, reps=3, fused=False):
     """The same `steps` decode steps captured in one HIP graph (after an
     eager run has grown the workspace) and replayed `reps` times from the
-    initial lengths; returns steps/s of the replays and whether the last
-    step's output equals the eager run's bit for bit."""
+    initial lengths; returns the last step's output and the steps/s of the
+    replays (fused: one bellman_decode_step call per step)."""
     import torch
 
     import paper_2510_15330_amd as bl
@@ -169,9 +175,13 @@ def graph_run(w, steps, reps=3):
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.graph(g, stream=side):
         for i in range(steps):
-            bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens)
-            bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
-                                k_scale=w.k_scale, v_scale=w.v_scale)
+            if fused:
+                bl.decode_step(w.k_new[i], w.v_new[i], w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens,
+                               w.scale, out, k_scale=w.k_scale, v_scale=w.v_scale)
+            else:
+                bl.kv_append(w.k_new[i], w.v_new[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens)
+                bl.decode_attention(w.q[i], w.k_pages, w.v_pages, w.block_table, w.seq_lens, w.scale, out,
+                                    k_scale=w.k_scale, v_scale=w.v_scale)
     times = []
     for _ in range(reps):
         w.seq_lens.copy_(lens0)
@@ -631,11 +641,23 @@ def main():
         gout, g_sps = graph_run(w8, n8)
         if not torch.equal(gout.view(torch.int16), eager_out.view(torch.int16)):
             raise RuntimeError("graph replay differs from the eager steps")
+        # the same steps through bellman_decode_step (append fused into the
+        # attention kernel): same pools, lengths and outputs bit for bit
+        rf = decode_run(w8, n8, args.warmup, fused=True)
+        fout, f_sps = graph_run(w8, n8, fused=True)
+        for o in (rf["out"], fout):
+            if not torch.equal(o.view(torch.int16), eager_out.view(torch.int16)):
+                raise RuntimeError("fused decode steps differ from the two-call steps")
         result["llama3_8b"] = dict(summary(w8, r8, n8), graph_steps_per_s=round(g_sps, 2),
-                                   graph_matches_eager=True)
+                                   graph_matches_eager=True,
+                                   fused_step={"steps_per_s": round(rf["steps_per_s"], 2),
+                                               "graph_steps_per_s": round(f_sps, 2),
+                                               "step_gpu_us_mean": round(rf["st"].mean() * 1e6, 2),
+                                               "matches_two_calls": True})
         log(f"[bench] llama3_8b: {r8['steps_per_s']:.1f} steps/s eager, {g_sps:.1f} from a graph, "
-            f"attention kernel {r8['kt'].mean() * 1e6:.1f} us")
-        del w8, r8, gout, eager_out
+            f"attention kernel {r8['kt'].mean() * 1e6:.1f} us; fused step {rf['steps_per_s']:.1f} eager, "
+            f"{f_sps:.1f} from a graph")
+        del w8, r8, gout, eager_out, rf, fout
         free_cuda()
 
         ns = wl.CONFIGS["stress_fp8"]["steps"]

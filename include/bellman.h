@@ -222,6 +222,34 @@ int bellman_decode_attention_noalloc(const bellman_tensor_t *q, const bellman_te
                                      bellman_tensor_t *out, const bellman_attn_opts_t *opts,
                                      void *stream);
 
+/* One decode step in one call: bellman_kv_append(k_new, v_new, ...) followed
+ * by bellman_decode_attention_opts(q, ...), with the same arguments, results
+ * and pool bytes, but no append launch (and no kernel boundary) between
+ * them.  The attention reads length seq_lens[b] + 1 for every request with
+ * 0 <= seq_lens[b] < maxP * 16; the wave that reads a (request, KV head)'s
+ * new position writes the new K and V rows there first (bf16 rows, fp8
+ * codes, or bf16 rows quantised into fp8 pools with the pools' dequant
+ * scales, exactly as the append does), and the merge pass then advances
+ * seq_lens as the append does (flag 1 where the position is outside the
+ * table or the pool).  One difference, for a position the append would
+ * refuse because its block-table entry lies outside the pool: the append
+ * leaves the request's attention over its old tokens, while here the
+ * attention reads the new position, finds the entry outside the pool, and
+ * writes that request's rows as NaN (flags 1 and 4).  The page that takes a
+ * request's new row must not be read by any other request of the same call
+ * (shared prefix pages are full, so this holds for them): the write and the
+ * other request's read are not ordered within the launch.  Built for the
+ * default steps only (opts pages_per_step 0, 1 or 2 and pipeline_depth 0 or
+ * 2 over bf16 pools; pages_per_step 0 or 4 and pipeline_depth 0 or 1 over
+ * fp8 pools) and without wave_times; other options return
+ * BELLMAN_ERR_UNSUPPORTED before anything is written.  Same workspace and
+ * graph-capture properties as bellman_decode_attention_opts. */
+int bellman_decode_step(const bellman_tensor_t *k_new, const bellman_tensor_t *v_new,
+                        const bellman_tensor_t *q, bellman_tensor_t *k_pages,
+                        bellman_tensor_t *v_pages, const bellman_tensor_t *block_table,
+                        bellman_tensor_t *seq_lens, float scale, bellman_tensor_t *out,
+                        const bellman_attn_opts_t *opts, void *stream);
+
 /* ----------------------------------------------------------- prompt path --
  * Before a request decodes, its prompt is prefilled (the step that sets the
  * time to first token, Sec. 3 "Our key proposal"; Sec. 4 "Setup and trace"):

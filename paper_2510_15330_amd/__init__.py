@@ -13,6 +13,7 @@ from ._binding import (  # noqa: F401
     calibrate_thresholds,
     decode_attention,
     decode_attention_noalloc,
+    decode_step,
     device_errors,
     kv_append,
     kv_write,

@@ -108,6 +108,8 @@ def library():
     lib.bellman_decode_attention_noalloc.argtypes = [T, T, T, T, T, ctypes.c_float, T,
                                                      ctypes.POINTER(AttnOpts), P]
     lib.bellman_decode_attention_noalloc.restype = ctypes.c_int
+    lib.bellman_decode_step.argtypes = [T, T, T, T, T, T, T, ctypes.c_float, T, ctypes.POINTER(AttnOpts), P]
+    lib.bellman_decode_step.restype = ctypes.c_int
     lib.bellman_probe_gather.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, P, P]
     lib.bellman_probe_gather.restype = ctypes.c_int
     lib.bellman_kv_write.argtypes = [T, T, T, T, T, T, T, P]
@@ -256,6 +258,24 @@ def decode_attention_noalloc(q, k_pages, v_pages, block_table, seq_lens, scale, 
     _check(library().bellman_decode_attention_noalloc(
         desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table), desc(seq_lens),
         ctypes.c_float(scale), desc(out), ctypes.byref(opts), _stream(stream)))
+
+
+def decode_step(k_new, v_new, q, k_pages, v_pages, block_table, seq_lens, scale, out, stream=None,
+                k_scale=None, v_scale=None, max_waves=0, xcd_skew=0, events=None, pages_per_step=0,
+                pipeline_depth=0, wave_times=None):
+    """bellman_decode_step: kv_append of (k_new, v_new) and decode_attention
+    of q in one call (the append fused into the attention launch)."""
+    _device_tensors(k_new, v_new, q, k_pages, v_pages, block_table, seq_lens, out, k_scale, v_scale, wave_times)
+    ev0 = ev1 = None
+    if events is not None:
+        ev0, ev1 = events[0].cuda_event, events[1].cuda_event
+        if not ev0 or not ev1:
+            raise ValueError("record each event once before passing it")
+    wt = None if wave_times is None else wave_times.data_ptr()
+    opts = AttnOpts(int(max_waves), int(xcd_skew), int(pages_per_step), int(pipeline_depth), ev0, ev1, wt)
+    _check(library().bellman_decode_step(
+        desc(k_new), desc(v_new), desc(q), desc(k_pages, k_scale), desc(v_pages, v_scale), desc(block_table),
+        desc(seq_lens), ctypes.c_float(scale), desc(out), ctypes.byref(opts), _stream(stream)))
 
 
 def probe_gather(pool, tile_bytes, sink, max_waves=0, stream=None):

@@ -240,7 +240,8 @@ int launch_status(const char* what) {
 // instead of the growable library workspace.
 int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages, const bellman_tensor_t* v_pages,
                      const bellman_tensor_t* block_table, const bellman_tensor_t* seq_lens, float scale,
-                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed) {
+                     bellman_tensor_t* out, const bellman_attn_opts_t* opts, void* stream, bool fixed,
+                     const bellman_tensor_t* k_new = nullptr, const bellman_tensor_t* v_new = nullptr) {
     g_last_error[0] = 0;
     int rc;
     PoolShape ps;
@@ -255,6 +256,16 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     if (!isfinite(scale)) return fail(BELLMAN_ERR_INVALID_ARG, "scale must be finite");
     if (H_q < 1 || H_q % ps.H_kv != 0)
         return fail(BELLMAN_ERR_INVALID_ARG, "query heads %lld not a multiple of KV heads %d", (long long)H_q, ps.H_kv);
+    // decode step: the new rows, as for bellman_kv_append
+    const bool step = k_new != nullptr || v_new != nullptr;
+    bool quant = false;
+    if (step) {
+        if ((rc = check_tensor(k_new, "k_new", 3))) return rc;
+        quant = ps.fp8 && k_new->dtype == BELLMAN_BF16;
+        const int32_t row_dtype = quant ? (int32_t)BELLMAN_BF16 : k_pages->dtype;
+        if ((rc = check_rows(k_new, "k_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
+        if ((rc = check_rows(v_new, "v_new", row_dtype, B, ps.H_kv, ps.D, 16))) return rc;
+    }
     const int64_t G = H_q / ps.H_kv;
     if (G > 16) return fail(BELLMAN_ERR_UNSUPPORTED, "GQA group %lld > 16", (long long)G);
     if (B > kMaxAttnBatch) return fail(BELLMAN_ERR_UNSUPPORTED, "batch %lld > %d", (long long)B, kMaxAttnBatch);
@@ -297,7 +308,12 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
         const double table_pages_per_wave = (double)B * ps.H_kv * (double)max_pages / (double)w_est;
         pps = ps.fp8 ? 4 : (table_pages_per_wave < kShortSharePages ? 1 : 2);
     }
+    if (step && !attention_step_built(pps, depth, ps.fp8))
+        return fail(BELLMAN_ERR_UNSUPPORTED,
+                    "decode step: built for the default steps only (bf16: 1 or 2 pages, depth 2; fp8: 4 pages, "
+                    "depth 1)");
     int64_t* wave_times = opts ? opts->wave_times : nullptr;
+    if (step && wave_times) return fail(BELLMAN_ERR_UNSUPPORTED, "decode step: wave_times is not built for it");
     if (wave_times && !attention_traced(pps, depth, ps.fp8, ps.D))
         return fail(BELLMAN_ERR_UNSUPPORTED,
                     "wave_times: traced kernels are built for head_dim 128 at the default steps only");
@@ -369,6 +385,14 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     a.part_ml = (float2*)(base + off_ml);
     a.part_o = (float*)(base + off_o);
     a.wave_times = wave_times;
+    a.k_new = step ? k_new->data : nullptr;
+    a.v_new = step ? v_new->data : nullptr;
+    a.new_sb = step ? k_new->stride[0] : 0;
+    a.new_sh = step ? k_new->stride[1] : 0;
+    a.vnew_sb = step ? v_new->stride[0] : 0;
+    a.vnew_sh = step ? v_new->stride[1] : 0;
+    a.quant = quant ? 1 : 0;
+    a.lens_rw = step ? (int32_t*)seq_lens->data : nullptr;
 
     hipEvent_t ev0 = opts ? (hipEvent_t)opts->event_begin : nullptr;
     hipEvent_t ev1 = opts ? (hipEvent_t)opts->event_end : nullptr;
@@ -548,6 +572,15 @@ int bellman_decode_attention_noalloc(const bellman_tensor_t* q, const bellman_te
                                      const bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
                                      const bellman_attn_opts_t* opts, void* stream) {
     return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, true);
+}
+
+int bellman_decode_step(const bellman_tensor_t* k_new, const bellman_tensor_t* v_new, const bellman_tensor_t* q,
+                        bellman_tensor_t* k_pages, bellman_tensor_t* v_pages, const bellman_tensor_t* block_table,
+                        bellman_tensor_t* seq_lens, float scale, bellman_tensor_t* out,
+                        const bellman_attn_opts_t* opts, void* stream) {
+    g_last_error[0] = 0;
+    if (!k_new || !v_new) return fail(BELLMAN_ERR_INVALID_ARG, "k_new and v_new are required");
+    return decode_attention(q, k_pages, v_pages, block_table, seq_lens, scale, out, opts, stream, false, k_new, v_new);
 }
 
 // ------------------------------------------------------------ prompt path --

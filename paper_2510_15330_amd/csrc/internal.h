@@ -75,6 +75,15 @@ struct AttnArgs {
                          // partial pieces (the request cut at its range's start, and at its end)
     float* part_o;       // [2 * waves * G * D]
     int64_t* wave_times; // optional [3 * waves] per-wave timing records (traced kernel), else null
+    // decode step (the append fused into this call), else k_new null: the
+    // attention reads length seq_lens[b] + 1 where 0 <= seq_lens[b] < maxP 16,
+    // the wave that reads a (request, head)'s new position first writes the
+    // new row there, and the merge pass advances the lengths
+    const void* k_new;   // [B, H_kv, D] rows in the pools' element type, or bf16 into fp8 pools
+    const void* v_new;
+    int64_t new_sb, new_sh, vnew_sb, vnew_sh;   // strides (elements)
+    int quant;           // 1: bf16 rows quantised into fp8 pools
+    int32_t* lens_rw;    // seq_lens, advanced by the merge pass
 };
 
 // Prompt KV write (prefill.hip).
@@ -129,6 +138,8 @@ void launch_kv_append(const AppendArgs& a, hipStream_t s);
 void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8, int grid, hipStream_t s);
 // Whether the attention kernel variant has a traced twin (wave_times).
 bool attention_traced(int pages_per_step, int depth, bool fp8, int D);
+// Whether the attention kernel variant has a decode-step twin (k_new set).
+bool attention_step_built(int pages_per_step, int depth, bool fp8);
 // Resident workgroups per CU of the attention kernel variant (occupancy).
 int attention_blocks_per_cu(int pages_per_step, int depth, bool fp8, int D);
 void launch_merge(const AttnArgs& a, hipStream_t s);

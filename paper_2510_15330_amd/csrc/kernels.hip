@@ -764,6 +764,94 @@ __device__ __forceinline__ void consume(const PageK<D, FP8>& r) { consume(r.k); 
 template <int D, bool FP8>
 __device__ __forceinline__ void consume(const PageV<D, FP8>& r) { consume(r.v); }
 
+// The length the attention reads for request b's stored length L (b < B):
+// clamped to the table, plus the new token in a decode step whose append
+// fits the table (a position outside the pool is flagged where it is read).
+template <bool STEP>
+__device__ __forceinline__ int attn_len(const AttnArgs& a, int L) {
+    const int maxL = a.max_pages * kPage;
+    if (STEP && L >= 0 && L < maxL) return L + 1;
+    return min(max(L, 0), maxL);
+}
+
+// Decode step: request b's new K and V rows of KV head g, to be written at
+// position L (the stored length) by the whole wave, as kv_append_kernel
+// does: K as 16-byte chunks (lanes 0 .. D/X - 1), V as D / 64 consecutive
+// dims a lane; fp8 pools take codes as they are or bf16 rows quantised with
+// the (request, head)'s scales.  row_load issues every read (block-table
+// entry, rows, scales) at once; row_store writes them, skipping a position
+// outside the pool (the merge pass flags it).
+struct NewRow {
+    int pg, slot, g;
+    u32x4 w, h;      // K chunk (and its second half when quantising)
+    uint32_t vv;     // this lane's V dims
+    float ks, vs;    // quantising scales
+};
+
+template <int D, bool FP8>
+__device__ __forceinline__ NewRow row_load(const AttnArgs& a, int b, int g, int L, int lane) {
+    constexpr int EB = FP8 ? 1 : 2;
+    constexpr int X = 16 / EB;                   // pool elements per K chunk
+    constexpr int VD = D / 64;                   // V dims a lane
+    NewRow r;
+    r.pg = a.block_table[(int64_t)b * a.bt_stride + (L >> 4)];
+    r.slot = L & (kPage - 1);
+    r.g = g;
+    const bool quant = FP8 && a.quant;
+    const int SB = quant ? 2 : EB;               // source element bytes
+    const char* kn = (const char*)a.k_new + ((int64_t)b * a.new_sb + (int64_t)g * a.new_sh) * SB;
+    const char* vn = (const char*)a.v_new + ((int64_t)b * a.vnew_sb + (int64_t)g * a.vnew_sh) * SB;
+    r.w = u32x4{0u, 0u, 0u, 0u};
+    r.h = u32x4{0u, 0u, 0u, 0u};
+    if (lane < D / X) {
+        r.w = *(const u32x4*)(kn + (int64_t)lane * X * SB);
+        if (quant) r.h = *(const u32x4*)(kn + (int64_t)lane * X * SB + 16);
+    }
+    if (quant || EB == 2) r.vv = VD == 2 ? *(const uint32_t*)(vn + (int64_t)lane * 4) : *(const uint16_t*)(vn + (int64_t)lane * 2);
+    else r.vv = VD == 2 ? *(const uint16_t*)(vn + (int64_t)lane * 2) : *(const uint8_t*)(vn + lane);
+    r.ks = quant ? a.k_scale[(int64_t)b * a.H_kv + g] : 0.f;
+    r.vs = quant ? a.v_scale[(int64_t)b * a.H_kv + g] : 0.f;
+    return r;
+}
+
+template <int D, bool FP8>
+__device__ __forceinline__ void row_store(const AttnArgs& a, const NewRow& r, int lane) {
+    constexpr int EB = FP8 ? 1 : 2;
+    constexpr int X = 16 / EB;
+    constexpr int VD = D / 64;
+    if ((unsigned)r.pg >= (unsigned)a.num_pages) return;
+    const bool quant = FP8 && a.quant;
+    char* kp = (char*)a.k_pages + ((int64_t)r.pg * a.H_kv + r.g) * ((int64_t)D * kPage * EB);
+    char* vp = (char*)a.v_pages + ((int64_t)r.pg * a.H_kv + r.g) * ((int64_t)D * kPage * EB);
+    if (lane < D / X) {
+        u32x4 w = r.w;
+        if (quant) {   // 16 bf16 -> 16 e4m3fn codes with the K scale
+            const uint32_t in[8] = {r.w.x, r.w.y, r.w.z, r.w.w, r.h.x, r.h.y, r.h.z, r.h.w};
+            uint32_t ow[4];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                ow[k] = quantize_e4m3fn(__uint_as_float(in[2 * k] << 16), r.ks) |
+                        (quantize_e4m3fn(__uint_as_float(in[2 * k] & 0xffff0000u), r.ks) << 8) |
+                        (quantize_e4m3fn(__uint_as_float(in[2 * k + 1] << 16), r.ks) << 16) |
+                        (quantize_e4m3fn(__uint_as_float(in[2 * k + 1] & 0xffff0000u), r.ks) << 24);
+            w = u32x4{ow[0], ow[1], ow[2], ow[3]};
+        }
+        *(u32x4*)(kp + ((int64_t)lane * kPage + r.slot) * 16) = w;
+    }
+#pragma unroll
+    for (int i = 0; i < VD; ++i) {
+        char* dst = vp + ((int64_t)(lane * VD + i) * kPage + r.slot) * EB;
+        if (quant) {
+            const uint32_t bits = (r.vv >> (16 * i)) & 0xffffu;
+            *(uint8_t*)dst = (uint8_t)quantize_e4m3fn(__uint_as_float(bits << 16), r.vs);
+        } else if (EB == 2) {
+            *(uint16_t*)dst = (uint16_t)(r.vv >> (16 * i));
+        } else {
+            *(uint8_t*)dst = (uint8_t)(r.vv >> (8 * i));
+        }
+    }
+}
+
 // A position in a wave's stream: step x, the `len` consecutive pages from
 // page p of request b, KV head g.  Wave-uniform.
 struct Cursor {
@@ -781,7 +869,7 @@ __device__ __forceinline__ void cursor_len(Cursor& c) {
 
 // Step to the next unit.  A cursor that would leave the range keeps its last
 // position (so loads issued for it stay in bounds) and stops being live.
-template <int PP>
+template <int PP, bool STEP>
 __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1) {
     if (!c.live) return;
     if (c.x + 1 >= r1) {
@@ -797,7 +885,7 @@ __device__ __forceinline__ void cursor_next(Cursor& c, const AttnArgs& a, int r1
             // units remain, so a later request with pages exists
             do {
                 ++c.b;
-                c.L = min(max(a.seq_lens[c.b], 0), a.max_pages * kPage);
+                c.L = attn_len<STEP>(a, a.seq_lens[c.b]);
                 c.np = (c.L + kPage - 1) / kPage;
             } while (c.np == 0 && c.b + 1 < a.B);
         }
@@ -820,7 +908,7 @@ constexpr int kHwRegHwId = 4 | (31 << 11);     // HW_ID, bits 31:0
 // real-time clock (100 MHz) when it starts and when it has written its last
 // result, and (XCD id << 32) | HW_ID: a timing record, not a change of the
 // computation.
-template <int D, bool FP8, int PP, int DEPTH, bool TRACE>
+template <int D, bool FP8, int PP, int DEPTH, bool TRACE, bool STEP>
 __global__ void __launch_bounds__(kAttnBlock) __attribute__((amdgpu_waves_per_eu(DEPTH == 1 ? 2 : 1, DEPTH == 1 ? 2 : 1)))
 attn_mfma_kernel(AttnArgs a) {
     constexpr int NT = D / 16;
@@ -858,11 +946,10 @@ attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
         for (int k = 0; k < kPlanPerLane; ++k) {
             const int b = b0 + kPlanPerLane * lane + k;
-            int L = b < a.B ? a.seq_lens[b] : 0;
-            if (L < 0 || L > maxL) {
-                bad_len = true;
-                L = L < 0 ? 0 : maxL;
-            }
+            // slots past the batch hold no request: length 0, no units
+            const int Ls = b < a.B ? a.seq_lens[b] : 0;
+            if (Ls < 0 || Ls > maxL) bad_len = true;
+            const int L = b < a.B ? attn_len<STEP>(a, Ls) : 0;
             Lk[k] = L;
             uk[k] = ((L + kPage - 1) / kPage + PP - 1) / PP * a.H_kv;
             sum += uk[k];
@@ -951,6 +1038,36 @@ attn_mfma_kernel(AttnArgs a) {
     sg = __builtin_amdgcn_readfirstlane(sg);
     sp = __builtin_amdgcn_readfirstlane(sp);
     sL = __builtin_amdgcn_readfirstlane(sL);
+
+    // Decode step: this wave writes the new row of every (request, head)
+    // whose last unit (the one holding the new position) lies in its range,
+    // before it issues any page load, walking segment by segment from the
+    // range's start.  A segment that ends inside the range is followed by
+    // another unit of the range, so the walk stays inside the batch.  The
+    // stored length is the attention length less one below the table's end;
+    // only a full-width attention length needs the stored one read back.
+    if constexpr (STEP) {
+        int b = sb, g = sg, L = sL, x0 = r0 - sp / PP;   // segment (b, g), its first unit x0
+        for (;;) {
+            const int last = x0 + ((L + kPage - 1) / kPage + PP - 1) / PP - 1;
+            if (last >= r1) break;                        // runs past the range: another wave's
+            const int Ls = L < maxL ? L - 1 : a.seq_lens[b];
+            if (Ls >= 0 && Ls < maxL) row_store<D, FP8>(a, row_load<D, FP8>(a, b, g, Ls, lane), lane);
+            x0 = last + 1;
+            if (x0 >= r1) break;
+            if (++g == a.H_kv) {
+                g = 0;
+                do {                                      // the next request with units
+                    ++b;
+                    L = attn_len<STEP>(a, a.seq_lens[b]);
+                } while (L == 0 && b + 1 < a.B);
+                if (L == 0) break;
+            }
+        }
+        // the rows are in memory before this wave reads any page
+        __builtin_amdgcn_s_waitcnt(0);
+    }
+
     Cursor cur[DEPTH + 2];
     {
         cur[0].b = sb;
@@ -965,7 +1082,7 @@ attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int j = 1; j < DEPTH + 2; ++j) {
         cur[j] = cur[j - 1];
-        cursor_next<PP>(cur[j], a, r1);
+        cursor_next<PP, STEP>(cur[j], a, r1);
     }
 
     // Block-table entries of a step: lane i < PP reads page p + i, clamped to
@@ -1142,7 +1259,7 @@ attn_mfma_kernel(AttnArgs a) {
         if (C.live && (C.p + C.len >= C.np || C.x + 1 >= r1)) finish(C, vs);
 #pragma unroll
         for (int j = 0; j < DEPTH + 1; ++j) cur[j] = cur[j + 1];
-        cursor_next<PP>(cur[DEPTH + 1], a, r1);
+        cursor_next<PP, STEP>(cur[DEPTH + 1], a, r1);
     };
 
     // One exit, after a whole round of DEPTH + 1 steps.  An exit between
@@ -1178,6 +1295,21 @@ attn_mfma_kernel(AttnArgs a) {
 // that began in it, combine that request's pieces.
 template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
+    if (a.k_new != nullptr) {
+        // decode step: advance the length of every request whose new row
+        // fitted (as kv_append_kernel does); flag the others
+        const int maxL = a.max_pages * kPage;
+        for (int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x; b < a.B; b += (int64_t)gridDim.x * 256) {
+            const int L = a.lens_rw[b];
+            bool ok = L >= 0 && L < maxL;
+            if (ok) {
+                const int pg = a.block_table[b * a.bt_stride + (L >> 4)];
+                ok = (unsigned)pg < (unsigned)a.num_pages;
+            }
+            if (ok) a.lens_rw[b] = L + 1;
+            else atomicOr(a.err, kErrAppendSlot);
+        }
+    }
     const int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (256 / kWaveSize) + (threadIdx.x >> 6));
     if (w >= a.waves) return;
     const int lane = threadIdx.x & (kWaveSize - 1);
@@ -1211,21 +1343,34 @@ void launch_kv_append(const AppendArgs& a, hipStream_t s) {
 template <int D, bool FP8, int PP, int DEPTH>
 constexpr bool kTraced = D == 128 && (FP8 ? (PP == 4 && DEPTH == 1) : (PP <= 2 && DEPTH == 2));
 
+// The shapes built with a decode-step twin (the append fused in): the
+// library's default steps, both head sizes.
+template <bool FP8, int PP, int DEPTH>
+constexpr bool kStepBuilt = FP8 ? (PP == 4 && DEPTH == 1) : (PP <= 2 && DEPTH == 2);
+
 template <int D, bool FP8, int PP, int DEPTH>
 struct Variant {
     static void launch(const AttnArgs& a, int grid, hipStream_t s) {
+        if (a.k_new != nullptr) {   // the host launches the step only where it is built
+            if constexpr (kStepBuilt<FP8, PP, DEPTH>)
+                hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, false, true>), dim3(grid), dim3(kAttnBlock),
+                                   0, s, a);
+            return;
+        }
         if constexpr (kTraced<D, FP8, PP, DEPTH>) {
             if (a.wave_times) {
-                hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, true>), dim3(grid), dim3(kAttnBlock), 0, s, a);
+                hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, true, false>), dim3(grid), dim3(kAttnBlock),
+                                   0, s, a);
                 return;
             }
         }
-        hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, false>), dim3(grid), dim3(kAttnBlock), 0, s, a);
+        hipLaunchKernelGGL((attn_mfma_kernel<D, FP8, PP, DEPTH, false, false>), dim3(grid), dim3(kAttnBlock), 0, s,
+                           a);
     }
     static int occupancy() {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<D, FP8, PP, DEPTH, false>, kAttnBlock,
-                                                         0) != hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, attn_mfma_kernel<D, FP8, PP, DEPTH, false, false>,
+                                                         kAttnBlock, 0) != hipSuccess ||
             nb < 1)
             nb = 1;
         return nb;
@@ -1268,6 +1413,10 @@ void launch_attention(const AttnArgs& a, int pages_per_step, int depth, bool fp8
 
 bool attention_traced(int pages_per_step, int depth, bool fp8, int D) {
     if (D != 128) return false;
+    return fp8 ? (pages_per_step == 4 && depth == 1) : (pages_per_step <= 2 && depth == 2);
+}
+
+bool attention_step_built(int pages_per_step, int depth, bool fp8) {
     return fp8 ? (pages_per_step == 4 && depth == 1) : (pages_per_step <= 2 && depth == 2);
 }
 

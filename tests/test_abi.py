@@ -148,6 +148,34 @@ def test_append_rejects(B, name, mut, code, msg):
     assert msg in B.last_error()
 
 
+def step(B_, g):
+    lib = B_.library()
+    return lib.bellman_decode_step(g["kn"], g["vn"], g["q"], g["k"], g["v"], g["bt"], g["sl"], 0.125, g["out"],
+                                   None, None)
+
+
+STEP_CASES = [
+    ("k_new null", lambda B_, g: g.update(kn=None), ERR_INVALID, "k_new and v_new"),
+    ("v_new null", lambda B_, g: g.update(vn=None), ERR_INVALID, "k_new and v_new"),
+    ("k_new heads", lambda B_, g: g.update(kn=t(B_.BF16, [4, 4, 128])), ERR_INVALID, "k_new: shape"),
+    ("v_new dtype", lambda B_, g: g.update(vn=t(B_.FP32, [4, 8, 128])), ERR_INVALID, "v_new: dtype"),
+    ("misaligned v_new", lambda B_, g: g.update(vn=t(B_.BF16, [4, 8, 128], data=FAKE + 2)), ERR_UNSUPPORTED, "aligned"),
+    ("fp8 rows into bf16 pools", lambda B_, g: g.update(kn=t(B_.FP8_E4M3FN, [4, 8, 128]), vn=t(B_.FP8_E4M3FN, [4, 8, 128])),
+     ERR_INVALID, "k_new: dtype"),
+    ("out rows", lambda B_, g: g.update(out=t(B_.BF16, [3, 32, 128])), ERR_INVALID, "out"),
+]
+
+
+@pytest.mark.parametrize("name,mut,code,msg", STEP_CASES, ids=[c[0] for c in STEP_CASES])
+def test_step_rejects(B, name, mut, code, msg):
+    # the one-call decode step validates its rows as the append does and the
+    # rest as the attention does, before any HIP call
+    g = good(B)
+    mut(B, g)
+    assert step(B, g) == code
+    assert msg in B.last_error()
+
+
 def prompt(B_, g, T=40, Bsz=4):
     g.update(pq=t(B_.BF16, [T, 32, 128]), pout=t(B_.BF16, [T, 32, 128]), qs=t(B_.INT32, [Bsz + 1]),
              pkn=t(B_.BF16, [T, 8, 128]), pvn=t(B_.BF16, [T, 8, 128]))
