@@ -100,9 +100,12 @@ typedef struct bellman_tensor {
  *                 (page block_table[b][L/16], slot L%16), then seq_lens[b]
  *                 becomes L + 1.
  * The write is bit-exact (a byte copy, or the quantisation above) and
- * touches nothing else.  A request whose slot lies
- * outside the block table or the pool is skipped (no byte written, length
- * unchanged) and flagged in the device error word.
+ * changes nothing else: the bytes around the new slot that share a 32-byte
+ * sector with it (the neighbouring slot's K chunk, the rest of each V dim
+ * row) are read and written back unchanged, so that every sector is written
+ * whole.  Hence no two requests of one call may append into the same page.
+ * A request whose slot lies outside the block table or the pool is skipped
+ * (no byte written, length unchanged) and flagged in the device error word.
  */
 int bellman_kv_append(const bellman_tensor_t *k_new, const bellman_tensor_t *v_new,
                       bellman_tensor_t *k_pages, bellman_tensor_t *v_pages,
