@@ -1309,6 +1309,18 @@ attn_mfma_kernel(AttnArgs a) {
         if constexpr (DEPTH >= 2) step(std::integral_constant<int, 2>{});
         if constexpr (DEPTH >= 3) step(std::integral_constant<int, 3>{});
         if (!cur[0].live) break;
+        if constexpr (DEPTH == 1) {
+            // Two workgroups share each CU at this depth (one wave of each per
+            // SIMD), and the wave arbiter favours the older: it finished well
+            // ahead and left the other alone on its CU (per-wave timing
+            // records, 512-request fp8 batch).  A wave with more of its range
+            // left now issues first.
+            const int q = (int)((int64_t)(cur[0].x - r0) * 4 / (r1 - r0));
+            if (q <= 0) __builtin_amdgcn_s_setprio(3);
+            else if (q == 1) __builtin_amdgcn_s_setprio(2);
+            else if (q == 2) __builtin_amdgcn_s_setprio(1);
+            else __builtin_amdgcn_s_setprio(0);
+        }
     }
     if (bad_pages) atomicOr(a.err, kErrPage);
     // The request this wave's range ends in, if it began inside the range and
