@@ -155,11 +155,13 @@ typedef struct bellman_attn_opts {
                              requests (results agree within rounding). */
     int32_t xcd_skew;     /* share weights of the waves of even- and odd-numbered
                              XCDs (workgroup i runs on XCD i mod 8), applied only
-                             when every wave gets at least 256 steps:
-                             0 = the library's choice (k = 10 on a whole 256-CU
-                             device with one workgroup per CU, equal shares
-                             otherwise); -1 = equal shares; k in 1..255 = weights
-                             256 + k : 256 - k.  Results agree within rounding. */
+                             when every wave gets at least 384 pages (steps x
+                             pages per step):
+                             0 = the library's choice (on a whole 256-CU device
+                             k = 10 with one workgroup per CU, k = 6 with two;
+                             equal shares otherwise); -1 = equal shares; k in
+                             1..255 = weights 256 + k : 256 - k.  Results agree
+                             within rounding. */
     int32_t pages_per_step; /* 16-token pages per softmax update: 1 or 2 (bf16),
                                1, 2 or 4 (fp8); 0 = the library's choice
                                (4 for fp8 pools; for bf16 pools 1 when

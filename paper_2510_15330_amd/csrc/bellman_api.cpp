@@ -34,6 +34,7 @@ int fail(int code, const char* fmt, ...) {
 // ------------------------------------------------------------- workspace ---
 
 constexpr int kXcdSkew = 10;          // share weights 266 : 246, even : odd XCDs (measured best of 0-28)
+constexpr int kXcdSkew2 = 6;          // the same with two workgroups per CU (fp8 stress batch: best of 0, 6, 12, 20)
 constexpr int kMaxAttnBatch = 8192;  // lengths every attention wave reads to find its share
 constexpr double kShortSharePages = 512;   // below this many table pages a wave: one page per step
 
@@ -376,9 +377,9 @@ int decode_attention(const bellman_tensor_t* q, const bellman_tensor_t* k_pages,
     a.waves = (int)waves;
     a.pp = pps;
     // The default XCD weights were measured on a whole MI355X (256 CUs,
-    // workgroup i on XCD i mod 8) with one workgroup per CU; partitioned
-    // devices and two workgroups per CU (depth 1) keep equal shares.
-    if (skew_opt == 0) a.skew = (bpc == 1 && g_cu_count[dev] == 256) ? kXcdSkew : 0;
+    // workgroup i on XCD i mod 8), with one and with two workgroups per CU;
+    // partitioned devices keep equal shares.
+    if (skew_opt == 0) a.skew = g_cu_count[dev] == 256 ? (bpc == 1 ? kXcdSkew : kXcdSkew2) : 0;
     else a.skew = skew_opt < 0 ? 0 : skew_opt;
     a.err = err;
     a.cuts = (int4*)(base + off_cuts);

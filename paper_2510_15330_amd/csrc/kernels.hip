@@ -1018,7 +1018,7 @@ attn_mfma_kernel(AttnArgs a) {
         P += __builtin_amdgcn_readfirstlane(wave_sum(load_lens(b0)));
         zero_empty(b0);
     }
-    const int skew = share_skew(a.skew, P, a.waves);
+    const int skew = share_skew(a.skew, P, a.waves, PP);
     const int r0 = share_bound(w, P, a.waves, skew);
     const int r1 = share_bound(w + 1, P, a.waves, skew);
     // wave 0 raises the length flag
@@ -1372,7 +1372,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     const int b = __builtin_amdgcn_readfirstlane(c.x), g = __builtin_amdgcn_readfirstlane(c.y);
     const int wl = __builtin_amdgcn_readfirstlane(c.z), P = __builtin_amdgcn_readfirstlane(c.w);
     MergeAcc<D> m;
-    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves), nh, qg, ml0, o0);
+    m.fold_waves(a, w, wl, P, share_skew(a.skew, P, a.waves, a.pp), nh, qg, ml0, o0);
     if (n < a.G) m.store(a, b, g * a.G + n, qg);
 }
 

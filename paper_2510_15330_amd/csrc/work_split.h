@@ -17,8 +17,8 @@
 // 256 + k and the others 256 - k, and wave w's range starts at unit
 // floor(C(w) P / C(W)), C the cumulative weight (k = 0: equal shares
 // [floor(w P / W), floor((w + 1) P / W))).  The skew applies only to long
-// shares (at least kSkewMinSteps steps a wave), where the rate difference,
-// not the ramp, sets the finish.
+// shares (at least kSkewMinPages pages a wave: P steps of PP pages each),
+// where the rate difference, not the ramp, sets the finish.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,12 +26,12 @@
 
 namespace bellman {
 
-constexpr int kSkewMinSteps = 256;   // steps a wave from which the skew applies
+constexpr int kSkewMinPages = 384;   // pages a wave from which the skew applies
 constexpr int kMaxSkew = 255;        // weights stay positive
 
-// The skew in force for P units over W waves.
-__host__ __device__ inline int share_skew(int skew, int P, int W) {
-    return (int64_t)P >= (int64_t)kSkewMinSteps * W ? skew : 0;
+// The skew in force for P units of PP pages over W waves.
+__host__ __device__ inline int share_skew(int skew, int P, int W, int PP) {
+    return (int64_t)P * PP >= (int64_t)kSkewMinPages * W ? skew : 0;
 }
 
 // C(w): summed weight of waves 0 .. w-1 (period of 8 waves: 4 of an

@@ -4,7 +4,7 @@
 
 extern "C" {
 
-int ws_skew(int skew, int P, int W) { return bellman::share_skew(skew, P, W); }
+int ws_skew(int skew, int P, int W, int PP) { return bellman::share_skew(skew, P, W, PP); }
 
 // out[0..W]: first unit of each wave, and P.
 void ws_bounds(int P, int W, int skew, int* out) {

@@ -305,16 +305,21 @@ def test_random_shapes_and_splits(seed):
                 assert np.all(got[b] == 0.0)
 
 
-def test_long_shares_with_weighted_split():
-    # shares of 256 steps or more a wave take the even/odd-XCD weights, also
-    # with wave counts that do not fill a period of eight
+@pytest.mark.parametrize("kv,pps,depth", [("bf16", 2, 2), ("fp8", 4, 1)])
+def test_long_shares_with_weighted_split(kv, pps, depth):
+    # shares of 384 pages or more a wave take the even/odd-XCD weights (one
+    # workgroup per CU at depth 2, two at depth 1), also with wave counts
+    # that do not fill a period of eight
     rng = np.random.default_rng(8192)
-    case = dn.random_case(rng, 2, 32, 8, 128, [8192, 3000], "bf16")
+    case = dn.random_case(rng, 2, 32, 8, 128, [8192, 3000], kv)
+    if kv == "fp8":   # unit-sized values, where the absolute bound holds
+        case["k_scale"] = (rng.uniform(0.5, 1.5, size=(2, 8)) / 40.0).astype(np.float32)
+        case["v_scale"] = (rng.uniform(0.5, 1.5, size=(2, 8)) / 40.0).astype(np.float32)
     scale = float(np.float32(1.0 / np.sqrt(128)))
-    ref = oracle_case(case, scale)
+    ref = oracle_case(case, scale, kv)
     for waves in (1, 3, 5, 7, 9):
-        got = run_case(dev_case(case), scale, max_waves=waves, pages_per_step=2, pipeline_depth=2)
-        G.assert_close(got, ref, "bf16", f"long shares waves={waves}")
+        got = run_case(dev_case(case, kv), scale, max_waves=waves, pages_per_step=pps, pipeline_depth=depth)
+        G.assert_close(got, ref, kv, f"long shares waves={waves}")
 
 
 @pytest.mark.parametrize("B,kv", [(2500, "bf16"), (8192, "fp8")])

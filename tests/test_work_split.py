@@ -27,7 +27,7 @@ def lib(tmp_path_factory):
                            SHIM, "-o", out])
     L = ctypes.CDLL(out)
     i32, P = ctypes.c_int, ctypes.c_void_p
-    L.ws_skew.argtypes = [i32, i32, i32]
+    L.ws_skew.argtypes = [i32, i32, i32, i32]
     L.ws_skew.restype = i32
     L.ws_bounds.argtypes = [i32, i32, i32, P]
     L.ws_bounds.restype = None
@@ -72,10 +72,13 @@ def check(lib, P, W, skew, xs=None):
 
 
 def test_skew_applies_to_long_shares_only(lib):
+    # from 384 pages a wave: P steps of PP pages each
     for W in (1, 7, 1024, 2048):
-        assert lib.ws_skew(10, 256 * W - 1, W) == 0
-        assert lib.ws_skew(10, 256 * W, W) == 10
-        assert lib.ws_skew(0, 1 << 30, W) == 0
+        for PP in (1, 2, 4):
+            n = 384 * W // PP + (1 if (384 * W) % PP else 0)   # fewest steps reaching 384 W pages
+            assert lib.ws_skew(10, n - 1, W, PP) == 0
+            assert lib.ws_skew(10, n, W, PP) == 10
+        assert lib.ws_skew(0, 1 << 29, W, 4) == 0
 
 
 def test_exhaustive_small(lib):
