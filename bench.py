@@ -9,7 +9,8 @@ U{6000..12000} + generated lognormal(median 500, sigma 0.5) clipped to 1500,
 JSON line: the same batch with beLLMan's per-request caps {100, 200, 400};
 equal versus XCD-weighted work shares on the headline batch; the
 Llama-3-8B-shaped batch (64 requests, 100 steps, eager and replayed from one
-HIP graph); the 512-request fp8 stress batch; and the prompt path (write +
+HIP graph, and the same steps through the one-call bellman_decode_step); the
+512-request fp8 stress batch; and the prompt path (write +
 causal prompt attention of four 6-12k-token prompts).  Inputs are synthetic
 and resident in HBM before timing.
 
