@@ -415,6 +415,51 @@ def test_append_out_of_table_is_skipped():
     assert (before_k != after_k).sum() > 0
 
 
+@pytest.mark.parametrize("kv,D", [("bf16", 128), ("bf16", 64), ("fp8", 128), ("fp8", 64)])
+def test_append_every_slot_keeps_the_rest_of_each_sector(kv, D):
+    """The append writes whole 32-byte sectors, reading back the bytes around
+    the new slot: over pools of arbitrary bytes (NaN patterns included), a
+    request at every slot 0..15, twice over, the whole pools must equal the
+    oracle's byte for byte."""
+    rng = np.random.default_rng(77 + D)
+    H_kv, maxP = 4, 3
+    lens = np.concatenate([np.arange(16), 16 + np.arange(16)[::-1]]).astype(np.int32)   # slots 0..15 on pages 0 and 1
+    B = len(lens)
+    NP = B * maxP + 3
+    bt = rng.permutation(NP)[:B * maxP].astype(np.int32).reshape(B, maxP)
+    if kv == "bf16":
+        kp = rng.integers(0, 1 << 16, size=(NP, H_kv, D // 8, 16, 8)).astype(np.uint16)
+        vp = rng.integers(0, 1 << 16, size=(NP, H_kv, D, 16)).astype(np.uint16)
+        kn = rng.integers(0, 1 << 16, size=(B, H_kv, D)).astype(np.uint16)
+        vn = rng.integers(0, 1 << 16, size=(B, H_kv, D)).astype(np.uint16)
+        code = oracle.BF16
+    else:
+        kp = rng.integers(0, 256, size=(NP, H_kv, D // 16, 16, 16)).astype(np.uint8)
+        vp = rng.integers(0, 256, size=(NP, H_kv, D, 16)).astype(np.uint8)
+        kn = rng.integers(0, 256, size=(B, H_kv, D)).astype(np.uint8)
+        vn = rng.integers(0, 256, size=(B, H_kv, D)).astype(np.uint8)
+        code = oracle.FP8_E4M3FN
+    ref_k, ref_v, ref_sl = kp.copy(), vp.copy(), lens.copy()
+    oracle.kv_append(kn, vn, ref_k, ref_v, bt, ref_sl, code)
+    t = lambda x: torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    if kv == "bf16":
+        dk, dv = t(kp.view(np.int16)).view(torch.bfloat16), t(vp.view(np.int16)).view(torch.bfloat16)
+        dkn, dvn = t(kn.view(np.int16)).view(torch.bfloat16), t(vn.view(np.int16)).view(torch.bfloat16)
+        ks = vs = None
+    else:
+        dk, dv, dkn, dvn = t(kp), t(vp), t(kn), t(vn)
+        ks = vs = torch.ones((B, H_kv), dtype=torch.float32, device="cuda")
+    dsl = t(lens)
+    bl.kv_append(dkn, dvn, dk, dv, t(bt), dsl, k_scale=ks, v_scale=vs)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    assert np.array_equal(dsl.cpu().numpy(), ref_sl)
+    view = (lambda x: x.view(torch.int16).cpu().numpy().view(np.uint16)) if kv == "bf16" else (lambda x: x.cpu().numpy())
+    gk, gv = view(dk), view(dv)
+    assert np.array_equal(gk, ref_k), f"K pool differs at {int((gk != ref_k).sum())} elements"
+    assert np.array_equal(gv, ref_v), f"V pool differs at {int((gv != ref_v).sum())} elements"
+
+
 def test_empty_batch_is_noop():
     q = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
     k = torch.zeros((4, 2, 8, 16, 8), dtype=torch.bfloat16, device="cuda")
