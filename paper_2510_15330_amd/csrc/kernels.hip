@@ -578,11 +578,14 @@ __device__ __forceinline__ void transpose4(int (&r)[8]) {
 
 // One step of PP fp8 pages: scores on fp8 MFMA, online softmax, then
 // O += V^T P^T with the step's 4*PP tokens per lane group (zero-padded to the
-// instruction's 32-element blocks).  V codes of slots >= nv are zeroed.
+// instruction's 32-element blocks).  Unless the step is `full` (PP pages of
+// 16 tokens, the common case), scores of slots >= nv are masked and the V
+// codes of those slots are zeroed in place (vx is a ring slot that is
+// reloaded before its next use).
 template <int D, int PP>
 __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> (&kx)[PP],
-                                         const PageV<D, true> (&vx)[PP], const Q8& q8, float sl,
-                                         const int (&nv)[PP], int qg) {
+                                         PageV<D, true> (&vx)[PP], const Q8& q8, float sl,
+                                         const int (&nv)[PP], int qg, bool full) {
     constexpr int NT = D / 16;
     float x[4 * PP];
     float mx = -INFINITY;
@@ -602,11 +605,16 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
         s4 = mfma_f8(ka, q8.hi, s4, q8.s_hi);
         s4 = mfma_f8(ka, q8.lo, s4, q8.s_lo);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            x[4 * i + r] = (4 * qg + r < nv[i]) ? s4[r] * sl : -INFINITY;
-            mx = fmaxf(mx, x[4 * i + r]);
-        }
+        for (int r = 0; r < 4; ++r) x[4 * i + r] = s4[r] * sl;
     }
+    if (!full) {
+#pragma unroll
+        for (int i = 0; i < PP; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) x[4 * i + r] = (4 * qg + r < nv[i]) ? x[4 * i + r] : -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < 4 * PP; ++i) mx = fmaxf(mx, x[i]);
     mx = group_max4(mx);
     const float m_new = fmaxf(st.m, mx);
     if (__any(m_new > st.m)) {
@@ -649,17 +657,22 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
         const i32x8 bph = {ph[0], ph[1], ph[2], ph[3], 0, 0, 0, 0};
         const i32x8 bpl = {pl[0], pl[1], pl[2], pl[3], 0, 0, 0, 0};
         // codes of slots >= nv are zeroed (a tail slot may hold any byte)
-        const int nvl = qg == 0 ? nv[0] : qg == 1 ? nv[1] : qg == 2 ? nv[2] : nv[3];
-        uint32_t mk[4];
+        if (!full) {
+            const int nvl = qg == 0 ? nv[0] : qg == 1 ? nv[1] : qg == 2 ? nv[2] : nv[3];
+            uint32_t mk[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int k = nvl - 4 * j;
-            mk[j] = k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+            for (int j = 0; j < 4; ++j) {
+                const int k = nvl - 4 * j;
+                mk[j] = k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) vx[j].v[t] &= mk[j];
         }
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            const i32x8 av = {(int)(vx[0].v[t] & mk[0]), (int)(vx[1].v[t] & mk[1]),
-                              (int)(vx[2].v[t] & mk[2]), (int)(vx[3].v[t] & mk[3]), 0, 0, 0, 0};
+            const i32x8 av = {(int)vx[0].v[t], (int)vx[1].v[t], (int)vx[2].v[t], (int)vx[3].v[t], 0, 0, 0, 0};
             st.o[t] = mfma_f8(av, bph, st.o[t], kE8M0One - 8);
             st.o[t] = mfma_f8(av, bpl, st.o[t], kE8M0One - 12);
         }
@@ -675,8 +688,10 @@ __device__ __forceinline__ void fp8_step(AttnState<D>& st, const PageK<D, true> 
 #pragma unroll
         for (int i = 0; i < PP; ++i) {
             uint32_t w = vx[i].v[t];
-            const int k = nv[i] - 4 * qg;  // live codes among this lane's four
-            w &= k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+            if (!full) {
+                const int k = nv[i] - 4 * qg;  // live codes among this lane's four
+                w &= k >= 4 ? 0xffffffffu : (k <= 0 ? 0u : (1u << (8 * k)) - 1u);
+            }
             va[i] = (int)w;
         }
         const i32x8 av = {va[0], va[1], va[2], va[3], va[4], va[5], va[6], va[7]};
@@ -1275,7 +1290,7 @@ attn_mfma_kernel(AttnArgs a) {
             int nv[PP];
 #pragma unroll
             for (int i = 0; i < PP; ++i) nv[i] = (i == 0 || C.len > i) ? min(kPage, C.L - (C.p + i) * kPage) : 0;
-            fp8_step<D, PP>(st, kb[sc_], vb[sc_], q8, sl, nv, qg);
+            fp8_step<D, PP>(st, kb[sc_], vb[sc_], q8, sl, nv, qg, C.len == PP && C.L >= (C.p + PP) * kPage);
         } else if constexpr (PP == 1) {
             const f32x4 s4 = page_scores<D, FP8>(kb[sc_][0], qb[sc_]);
             page_pv<D, FP8>(st, s4, vb[sc_][0], sl, min(kPage, C.L - C.p * kPage), qg);
