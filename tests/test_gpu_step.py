@@ -244,3 +244,38 @@ def test_step_rejects_unbuilt_shapes():
         _step(c, 0.1, pipeline_depth=1)
     torch.cuda.synchronize()
     assert torch.equal(c["sl"].cpu(), torch.tensor([5, 40], dtype=torch.int32))
+
+
+def test_step_empty_batch_is_noop():
+    q = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros((4, 2, 8, 16, 8), dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros((4, 2, 64, 16), dtype=torch.bfloat16, device="cuda")
+    rows = torch.empty((0, 2, 64), dtype=torch.bfloat16, device="cuda")
+    bt = torch.empty((0, 1), dtype=torch.int32, device="cuda")
+    sl = torch.empty((0,), dtype=torch.int32, device="cuda")
+    out = torch.empty((0, 8, 64), dtype=torch.bfloat16, device="cuda")
+    bl.decode_step(rows, rows.clone(), q, k, v, bt, sl, 0.125, out)
+    torch.cuda.synchronize()
+    assert bl.device_errors() == 0
+    assert torch.equal(k, torch.zeros_like(k)) and torch.equal(v, torch.zeros_like(v))
+
+
+def test_step_negative_length_matches_two_calls():
+    # a negative stored length: both paths flag it (length 2, append 1), write
+    # no row for it, leave its length alone and give it zero rows; the other
+    # requests advance as usual
+    lens = [5, 40, 17]
+    base = _state(31, 3, 16, 4, 128, lens, "bf16")
+    base["sl"][1] = -3
+    for kw in (dict(), dict(max_waves=5)):
+        a, b = _clone(base), _clone(base)
+        _two_calls(a, 0.1, **kw)
+        torch.cuda.synchronize()
+        ea = bl.device_errors()
+        _step(b, 0.1, **kw)
+        torch.cuda.synchronize()
+        eb = bl.device_errors()
+        assert ea == eb == 1 | 2, (ea, eb)
+        _same(a, b, f"negative length {kw}")
+        assert b["sl"].cpu().tolist() == [6, -3, 18]
+        assert torch.all(b["out"][1].float() == 0)
